@@ -1,0 +1,251 @@
+"""Benchmark of the CE-Router routed block on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload N] [--no-cpu-baseline]
+
+One step = one fused routed block (ce_routed_block: core/expansion scoring ->
+per-sequence TopK -> SwiGLU FFN on the retained rows -> residual scatter) over
+the whole synthetic batch, with inputs resident in HBM. Buffer sets (hidden
+states + every weight) rotate so the working set exceeds twice the 256 MB
+last-level cache. Prints ONE JSON line (rank 0, one GPU).
+
+`value` = input tokens per second (every token of the batch is routed: scored,
+then kept or bypassed). The roofline entry covers the dominant kernel, the
+gate/up + SwiGLU GEMM, timed per launch with HIP events on the stream it runs
+on; its HBM traffic comes from the committed rocprofv3 counter summary when
+that summary matches the current kernel source, else null.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "routed tokens/sec per layer (score+topk+FFN+scatter); % MFMA / HBM peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
+PEAK_HBM_GBS = 8000.0
+MALL_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_gateup_showo2_understanding_traffic.json")
+KERNEL_SOURCES = ["paper_2608_29291_amd/csrc/ce_ffn.hip", "paper_2608_29291_amd/csrc/ce_device.hpp"]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic():
+    """HBM bytes per gate/up launch from the committed counter summary, if current."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, n_seq: int, min_seconds: float = 10.0, max_reps: int = 10):
+    """The oracle (float64 NumPy) on the first n_seq sequences, repeated until
+    about min_seconds of CPU work; reports tokens per second over all runs."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+                      or [1])
+    except Exception:  # pragma: no cover - threadpoolctl missing
+        threads = os.cpu_count() or 1
+    hi = int(wl.seq_offsets[n_seq])
+    offs = wl.seq_offsets[: n_seq + 1]
+    reps, total = 0, 0.0
+    while reps < max_reps and (reps == 0 or total < min_seconds):
+        t0 = time.perf_counter()
+        oracle.routed_block(wl.hidden[:hi], wl.flags[:hi], offs, wl.t[:n_seq], wl.keep, wl.scorer, wl.ffn)
+        total += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(reps * hi / total, 1), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n_seq} of {wl.B} sequences ({hi} tokens) x {reps} runs, one routed block each "
+                      f"in float64 NumPy, {total:.1f} s total on {platform.processor() or platform.machine()} "
+                      f"({os.cpu_count()} logical CPUs visible, BLAS threads {threads})"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
+    ap.add_argument("--step3", type=int, default=25, help="denoising step of workload 3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seqs", type=int, default=0, help="sequences in the oracle sample (0 = auto)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the routed block shards by sequence with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_29291_amd as ce
+    from ce_workloads import CONFIG_NAMES, CONFIG_DESCRIPTIONS, make_config
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wid = args.workload
+    log(f"generating workload {wid}: {CONFIG_DESCRIPTIONS[wid]}")
+    wl = make_config(wid, step=args.step3 if wid == 3 else None)
+    bf16 = wl.dtype == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    dtc = ce.CE_BF16 if bf16 else ce.CE_F32
+    cap = ce.ce_kept_count_host(wl.seq_offsets, wl.flags, float(wl.keep))
+    T, d, F = wl.T, wl.d, wl.d_ff
+
+    def up(x, dtype=None):
+        t = torch.from_numpy(np.ascontiguousarray(x))
+        return (t.to(dtype) if dtype is not None else t).to(dev)
+
+    batch = ce.Batch(up(wl.seq_offsets), up(wl.flags), up(wl.t), float(wl.keep), cap)
+    sw = wl.scorer
+    opt = lambda x: None if x is None else up(x.astype(np.float32))
+    base_scorer = ce.Scorer(up(sw.w1_core, dt), up(sw.w2_core), up(sw.w1_exp, dt), up(sw.w2_exp),
+                            b1_core=opt(sw.b1_core), b2_core=float(sw.b2_core), b1_exp=opt(sw.b1_exp),
+                            b2_exp=opt(sw.b2_exp))
+    base_ffn = ce.FFN([up(f.w_gate, dt) for f in wl.ffn], [up(f.w_up, dt) for f in wl.ffn],
+                      [up(f.w_down, dt) for f in wl.ffn])
+    base_h = up(wl.hidden, dt)
+    elem = 2 if bf16 else 4
+    set_bytes = (T * d + (sw.r_core + sw.n_seg * sw.r_exp) * d + 3 * d * F * len(wl.ffn)) * elem
+    n_sets = max(2, int(np.ceil(2 * MALL_BYTES / set_bytes)))
+    log(f"T={T} Kt={cap} d={d} F={F}; rotating {n_sets} buffer sets of {set_bytes / 2**20:.0f} MiB")
+    sets = [(base_h, base_scorer, base_ffn)]
+    for _ in range(n_sets - 1):
+        sc = ce.Scorer(*(x.clone() if x is not None else None for x in
+                         (base_scorer.w1_core, base_scorer.w2_core, base_scorer.w1_exp, base_scorer.w2_exp,
+                          base_scorer.b1_core)), b2_core=base_scorer.b2_core,
+                       b1_exp=None if base_scorer.b1_exp is None else base_scorer.b1_exp.clone(),
+                       b2_exp=None if base_scorer.b2_exp is None else base_scorer.b2_exp.clone())
+        ff = ce.FFN([w.clone() for w in base_ffn.w_gate], [w.clone() for w in base_ffn.w_up],
+                    [w.clone() for w in base_ffn.w_down])
+        sets.append((base_h.clone(), sc, ff))
+    ws = ce.alloc_workspace(ce.CE_WS_BLOCK, batch, d, F, dtc, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        h, sc, ff = sets[i % n_sets]
+        ce.ce_routed_block(batch, h, h, sc, ff, ws, stream=stream)
+
+    # ---- whole routed block ----
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert ce.ce_workspace_status(ws) == 0, "device status error"
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"routed block: {ms * 1e3:.1f} us/step")
+
+    # ---- per-stage launches (staged entry points on the same data) ----
+    logits = torch.empty(T, device=dev)
+    kept_idx = torch.empty(cap, dtype=torch.int32, device=dev)
+    kept_off = torch.empty(wl.B + 1, dtype=torch.int32, device=dev)
+    compact = torch.empty((cap, d), dtype=dt, device=dev)
+    act = torch.empty((cap, F), dtype=dt, device=dev)
+    ffn_out = torch.empty((cap, d), dtype=dt, device=dev)
+    ws_topk = ce.alloc_workspace(ce.CE_WS_TOPK, batch, d, F, dtc, device=dev)
+    ws_ffn = ce.alloc_workspace(ce.CE_WS_FFN, batch, d, F, dtc, device=dev)
+    h0, sc0, ff0 = sets[0]
+    ce.ce_score(batch, h0, sc0, logits, stream=stream)
+    ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk, hidden=h0, compact=compact,
+                       stream=stream)
+    torch.cuda.synchronize()
+
+    def timed(fn, reps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for i in range(reps):
+            evs[i][0].record(stream)
+            fn(i)
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in evs])) * 1e3  # us
+
+    reps = max(args.steps, 10)
+    stages = {
+        "score": timed(lambda i: ce.ce_score(batch, sets[i % n_sets][0], sets[i % n_sets][1], logits,
+                                             stream=stream), reps),
+        "topk_compact": timed(lambda i: ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk,
+                                                           stream=stream), reps),
+        "ffn_gateup": timed(lambda i: ce.ce_ffn_gateup(batch, compact, kept_idx, kept_off,
+                                                       sets[i % n_sets][2], act, ws_ffn, stream=stream),
+                            reps),
+        "ffn_down": timed(lambda i: ce.ce_ffn_down(batch, act, kept_idx, kept_off, sets[i % n_sets][2],
+                                                   ffn_out, ws_ffn, stream=stream), reps),
+    }
+    log("stages (us): " + ", ".join(f"{k}={v:.1f}" for k, v in stages.items()))
+
+    gateup_flops = 4.0 * cap * d * F  # gate and up: 2 GEMMs of Kt x d x F, 2 flops per MAC
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    achieved = gateup_flops / (stages["ffn_gateup"] * 1e-6) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": load_traffic(),
+                "kernel": "ffn_gemm_kernel gate/up + SwiGLU (ce_ffn_gateup)",
+                "flops_per_launch": gateup_flops}
+
+    block_flops = (2.0 * cap * d * 3 * F
+                   + 2.0 * float(np.sum((wl.flags & 2) == 0)) * d * sw.r_core
+                   + 2.0 * float(np.sum(((wl.flags & 1) != 0) & ((wl.flags & 2) == 0))) * d * sw.r_exp)
+    result = {
+        "metric": METRIC,
+        "value": round(T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": CONFIG_NAMES[wid], "description": CONFIG_DESCRIPTIONS[wid], "B": wl.B,
+                   "T": T, "kept_rows": cap, "d": d, "d_ff": F, "r_core": sw.r_core, "r_exp": sw.r_exp,
+                   "keep": float(wl.keep), "ffn_sets": len(wl.ffn), "buffer_sets": n_sets,
+                   "parallelism": "single GPU"},
+        "kept_tokens_per_s": round(cap / (ms * 1e-3), 1),
+        "block_tflops": round(block_flops / (ms * 1e-3) / 1e12, 2),
+        "stages_us": {k: round(v, 2) for k, v in stages.items()},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
+        log(f"oracle CPU baseline on {n_seq} sequence(s)...")
+        result["cpu_baseline"] = cpu_baseline(wl, n_seq)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

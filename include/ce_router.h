@@ -1,0 +1,274 @@
+/*
+ * ce_router.h -- C ABI of the CE-Router routed-block library for MI355X (gfx950).
+ *
+ * One routed layer of a unified multimodal backbone, as defined in the paper
+ * "Accelerating Unified Multimodal Models with Core-Expansion Routing and
+ * Unified Computation Scheduling":
+ *
+ *   1. score     core + expansion routing logits per token       (section 3.2, Eq. 4)
+ *   2. topk      per-sequence TopK of the logits -> retained set  (section 3.4, Eq. 6)
+ *   3. compact   retained tokens packed into a shorter sequence   (section 3.4, after Eq. 6)
+ *   4. ffn       SwiGLU FFN on the packed rows only
+ *   5. scatter   residual merge; dropped tokens take the bypass   (section 3.4, after Eq. 6)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument documented as "device" is GPU memory on the current
+ *   HIP device, owned by the caller, contiguous, 16-byte aligned. "host"
+ *   pointers are ordinary CPU memory, read before the call returns.
+ * - The library allocates no memory and keeps no pointer after a call
+ *   returns. All work is enqueued on `stream` (a hipStream_t; NULL = the
+ *   default stream); calls return without waiting for it. There are no
+ *   device-to-host copies and no synchronisation on the hot path.
+ * - Arguments are validated on the host before anything is launched; a
+ *   negative status means nothing was enqueued.
+ * - Values known only on the device (how many tokens each sequence keeps,
+ *   the packed row count Kt, MoT group sizes) never leave the device. Grids
+ *   are sized from host-known upper bounds (kept_capacity); surplus tiles
+ *   exit early. If the device finds inconsistent data (bad seq_offsets,
+ *   Kt > kept_capacity) it never reads or writes out of bounds; it records
+ *   the problem in the workspace status word (ce_workspace_status).
+ * - Element types: hidden states and the scorer/FFN weight matrices share
+ *   one dtype (CE_F32 or CE_BF16); biases, second-layer scorer vectors,
+ *   timesteps and logits are float32; indices are int32.
+ * - Shape limits: d % 64 == 0, d_ff % 64 == 0, scorer ranks % 32 == 0 and
+ *   r_core + r_exp <= 512, 1 <= n_seg <= 16, B >= 1, 0 <= T < 2^31.
+ * - Matrices are row-major in the nn.Linear layout [out_features x in_features].
+ * - Functions are stateless; concurrent calls on different streams are safe
+ *   as long as they use different workspaces and outputs.
+ */
+#ifndef CE_ROUTER_H
+#define CE_ROUTER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+    CE_OK = 0,
+    CE_ERR_INVALID_ARG = -1, /* null pointer, bad size, value out of range     */
+    CE_ERR_UNSUPPORTED = -2, /* shape/dtype outside the supported limits      */
+    CE_ERR_WORKSPACE = -3,   /* workspace pointer null or smaller than needed */
+    CE_ERR_HIP = -4          /* a HIP runtime call failed (launch, query)     */
+};
+
+/* ---- element types ----------------------------------------------------- */
+enum { CE_F32 = 0, CE_BF16 = 1 };
+
+/* ---- per-token flags (uint8) ------------------------------------------- */
+enum {
+    CE_TOK_GEN = 1,  /* generation token: scored by core + expansion e_{m(t)}  */
+                     /* (Eq. 4); in a two-set MoT FFN it uses weight set 1.   */
+                     /* Clear: understanding token, core only, weight set 0.  */
+    CE_TOK_KEEP = 2  /* always retained (text / structure token); not scored, */
+                     /* not counted in K; its logit is reported as +inf.       */
+};
+
+/* ---- device status word bits (ce_workspace_status) ---------------------- */
+enum {
+    CE_DEV_BAD_OFFSETS = 1,  /* seq_offsets not non-decreasing within [0, T]   */
+    CE_DEV_OVERFLOW = 2      /* total retained rows Kt exceeded kept_capacity  */
+};
+
+/* ---- workspace kinds ---------------------------------------------------- */
+enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2 };
+
+/*
+ * A ragged batch of B sequences packed back to back: sequence b owns tokens
+ * [seq_offsets[b], seq_offsets[b+1]).
+ *   seq_offsets   device int32 [B+1], seq_offsets[0] = 0, non-decreasing, last = T
+ *   flags         device uint8 [T], CE_TOK_* bits; other bits ignored
+ *   t             device float32 [B], denoising timestep of sequence b in [0, 1]
+ *                 (read only for sequences holding generation tokens; values
+ *                 outside [0, 1] are clamped to the first / last segment)
+ *   keep          keep ratio r in [0, 1]: sequence b retains its KEEP tokens
+ *                 plus k_b = ceil(keep * n_b) of its n_b routable tokens
+ *                 (ce_num_keep), exactly, on the float32 value of keep
+ *   kept_capacity host upper bound on Kt = sum_b (A_b + k_b) (A_b = KEEP count);
+ *                 sizes kept_idx / compact / FFN buffers; T always suffices
+ */
+typedef struct ce_batch {
+    int32_t B;
+    int32_t T;
+    const int32_t* seq_offsets;
+    const uint8_t* flags;
+    const float* t;
+    float keep;
+    int32_t kept_capacity;
+} ce_batch;
+
+/*
+ * Router of one layer (section 3.2): one core scorer shared by both tasks and
+ * every generation segment, plus n_seg generation expansion scorers, each a
+ * token-wise two-layer MLP with a scalar output:
+ *     s(h) = w2 . SiLU(W1 h + b1) + b2
+ * Understanding tokens: l = c(h). Generation tokens: l = c(h) + e_{m(t)}(h),
+ * with m(t) = min(floor(n_seg * t), n_seg - 1) (equal-width segments of t).
+ *   w1_core  device dtype   [r_core x d]
+ *   b1_core  device float32 [r_core] or NULL (zero)
+ *   w2_core  device float32 [r_core]
+ *   b2_core  host scalar
+ *   w1_exp   device dtype   [n_seg x r_exp x d]   (may be NULL if r_exp == 0)
+ *   b1_exp   device float32 [n_seg x r_exp] or NULL
+ *   w2_exp   device float32 [n_seg x r_exp]
+ *   b2_exp   device float32 [n_seg] or NULL
+ */
+typedef struct ce_scorer_w {
+    int32_t d, r_core, r_exp, n_seg;
+    int32_t dtype;
+    const void* w1_core;
+    const float* b1_core;
+    const float* w2_core;
+    float b2_core;
+    const void* w1_exp;
+    const float* b1_exp;
+    const float* w2_exp;
+    const float* b2_exp;
+} ce_scorer_w;
+
+/*
+ * SwiGLU FFN weight sets: y = W_down (SiLU(W_gate x) * (W_up x)).
+ * n_sets = 1, or 2 for a mixture-of-transformers block where each retained
+ * token uses set (flags & CE_TOK_GEN).
+ *   w_gate[s], w_up[s]  device dtype [d_ff x d]
+ *   w_down[s]           device dtype [d x d_ff]
+ */
+typedef struct ce_ffn_w {
+    int32_t d, d_ff, n_sets;
+    int32_t dtype;
+    const void* w_gate[2];
+    const void* w_up[2];
+    const void* w_down[2];
+} ce_ffn_w;
+
+/* Human-readable name of a status code (static string). */
+const char* ce_status_string(int status);
+
+/* Library version string, e.g. "ce_router 0.1.0 gfx950". */
+const char* ce_version(void);
+
+/*
+ * k = ceil(keep * n) evaluated exactly on the float32 value of keep (section
+ * 3.4 / appendix A.2 define r = K / N; the rounding is this library's
+ * reading). Returns -1 if keep is outside [0, 1] or NaN, or n < 0.
+ */
+int32_t ce_num_keep(float keep, int32_t n_routable);
+
+/*
+ * Host helper: exact Kt = sum_b (A_b + ce_num_keep(keep, n_b - A_b)) from
+ * host copies of seq_offsets [B+1] and flags [T]. Returns -1 on bad input.
+ */
+int64_t ce_kept_count_host(int32_t B, int32_t T, const int32_t* seq_offsets_host,
+                           const uint8_t* flags_host, float keep);
+
+/*
+ * Workspace bytes needed by an entry point (which = CE_WS_*), for this batch
+ * (B, T, kept_capacity), hidden size d, FFN width d_ff and dtype. The
+ * workspace is caller-owned device memory, 256-byte aligned; its contents on
+ * entry do not matter.
+ */
+size_t ce_workspace_size(int which, const ce_batch* batch, int32_t d, int32_t d_ff, int dtype);
+
+/*
+ * Read the device status word (CE_DEV_* bits) written into a workspace by
+ * the last ce_topk_compact / ce_routed_block call that used it. Synchronises
+ * `stream`. Debug / test helper, not for the hot path.
+ */
+int ce_workspace_status(const void* ws, uint32_t* status_out, void* stream);
+
+/*
+ * Step 1 -- routing logits (section 3.2, Eq. 4) and scores (Eq. 6).
+ *   hidden  device dtype [T x d]
+ *   logits  device float32 [T] out: Eq. 4 logit; +inf for KEEP tokens
+ *   probs   device float32 [T] out or NULL: sigmoid(logit) (Eq. 6)
+ * Errors: CE_ERR_INVALID_ARG for null pointers / sizes, CE_ERR_UNSUPPORTED
+ * for shapes outside the limits, CE_ERR_HIP on a failed launch.
+ */
+int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w,
+             float* logits, float* probs, void* stream);
+
+/*
+ * Steps 2-3 -- per-sequence TopK and packing (section 3.4, Eq. 6).
+ * Among the routable (non-KEEP) tokens of each sequence, the k_b tokens
+ * first in the order (larger logit first; equal logits -> lower token index;
+ * -0 == +0; NaN below -inf) are retained, together with every KEEP token.
+ *   logits       device float32 [T] (values of KEEP tokens are ignored)
+ *   hidden       device dtype [T x d], read only if compact != NULL
+ *   kept_idx     device int32 [kept_capacity] out: retained token indices,
+ *                ascending within each sequence, sequences in order
+ *   kept_offsets device int32 [B+1] out: sequence b's retained tokens are
+ *                kept_idx[kept_offsets[b] .. kept_offsets[b+1])
+ *   token_pos    device int32 [T] out or NULL: position of each token in
+ *                kept_idx, -1 for dropped tokens
+ *   compact      device dtype [kept_capacity x d] out or NULL: row j = hidden[kept_idx[j]]
+ *   ws           device workspace of ce_workspace_size(CE_WS_TOPK, ...) bytes
+ */
+int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidden,
+                    int dtype, int32_t d, int32_t* kept_idx, int32_t* kept_offsets,
+                    int32_t* token_pos, void* compact, void* ws, size_t ws_bytes,
+                    void* stream);
+
+/*
+ * Step 4 -- SwiGLU FFN on the packed rows.
+ *   compact      device dtype [kept_capacity x d]: packed rows (row j is token kept_idx[j])
+ *   kept_idx     device int32 [kept_capacity] (needed for the MoT set choice)
+ *   kept_offsets device int32 [B+1]: Kt = kept_offsets[B] rows are processed
+ *   ffn_out      device dtype [kept_capacity x d] out: FFN(row j), no residual
+ *   ws           device workspace of ce_workspace_size(CE_WS_FFN, ...) bytes
+ *                (holds the [kept_capacity x d_ff] SwiGLU activations)
+ */
+int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
+                  const int32_t* kept_offsets, const ce_ffn_w* w, void* ffn_out,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step 4 in two launches (same result as ce_routed_ffn):
+ *   ce_ffn_gateup  act[j] = SiLU(W_gate x_j) * (W_up x_j), x_j = compact[j]; act is the
+ *                  intermediate activation z of the FFN (section 3.4, Eq. 8 scores FFN
+ *                  channels from it). act: device dtype [kept_capacity x d_ff], packed order.
+ *   ce_ffn_down    ffn_out[j] = W_down act[j]; ffn_out: device dtype [kept_capacity x d].
+ * Arguments otherwise as ce_routed_ffn; ws: ce_workspace_size(CE_WS_FFN, ...) bytes
+ * (the act region of the workspace is not used by these two calls).
+ */
+int ce_ffn_gateup(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
+                  const int32_t* kept_offsets, const ce_ffn_w* w, void* act, void* ws,
+                  size_t ws_bytes, void* stream);
+int ce_ffn_down(const ce_batch* batch, const void* act, const int32_t* kept_idx,
+                const int32_t* kept_offsets, const ce_ffn_w* w, void* ffn_out, void* ws,
+                size_t ws_bytes, void* stream);
+
+/*
+ * Step 5 -- residual merge (section 3.4: dropped tokens take the bypass path):
+ *   hidden_out[kept_idx[j]] = hidden_in[kept_idx[j]] + ffn_out[j]   (fp32 add, one rounding)
+ *   hidden_out[i] = hidden_in[i] for dropped i
+ * hidden_in == hidden_out is allowed (in place: dropped rows are not touched);
+ * out of place, every dropped row is copied (extra traffic).
+ */
+int ce_scatter_residual(const ce_batch* batch, const void* ffn_out, const int32_t* kept_idx,
+                        const int32_t* kept_offsets, int dtype, int32_t d,
+                        const void* hidden_in, void* hidden_out, void* stream);
+
+/*
+ * Steps 1-5 fused: score -> TopK -> SwiGLU FFN over the retained rows
+ * (gathered directly from hidden_in) -> residual scatter into hidden_out.
+ *   hidden_in / hidden_out  device dtype [T x d] (may alias: in place)
+ *   logits_out       device float32 [T] or NULL
+ *   kept_idx_out     device int32 [kept_capacity] or NULL
+ *   kept_offsets_out device int32 [B+1] or NULL
+ *   ws               device workspace of ce_workspace_size(CE_WS_BLOCK, ...) bytes
+ * Scorer and FFN must agree on d and dtype.
+ */
+int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_out,
+                    const ce_scorer_w* scorer, const ce_ffn_w* ffn, float* logits_out,
+                    int32_t* kept_idx_out, int32_t* kept_offsets_out, void* ws,
+                    size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CE_ROUTER_H */

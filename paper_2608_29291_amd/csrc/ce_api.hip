@@ -1,0 +1,335 @@
+// C-ABI entry points of the CE-Router routed-block library (declared in
+// include/ce_router.h). Each entry point validates on the host, carves the
+// caller's workspace, then enqueues its kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include "ce_host.hpp"
+#include "ce_launch.hpp"
+
+using namespace ce;
+
+namespace {
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? CE_OK : CE_ERR_HIP; }
+
+#define CE_TRY(expr)                          \
+  do {                                        \
+    const hipError_t _e = (expr);             \
+    if (_e != hipSuccess) return CE_ERR_HIP;  \
+  } while (0)
+
+#define CE_CHECK(expr)               \
+  do {                               \
+    const int _s = (expr);           \
+    if (_s != CE_OK) return _s;      \
+  } while (0)
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+ScoreArgs make_score_args(const ce_batch* b, const void* hidden, const ce_scorer_w* w, float* logits,
+                          float* probs) {
+  const int elem = elem_size(w->dtype);
+  ScoreArgs a;
+  a.hidden = static_cast<const char*>(hidden);
+  a.h_ld = (int64_t)w->d * elem;
+  a.k_bytes = w->d * elem;
+  a.B = b->B;
+  a.T = b->T;
+  a.seq_offsets = b->seq_offsets;
+  a.flags = b->flags;
+  a.t = b->t;
+  a.w1c = static_cast<const char*>(w->w1_core);
+  a.b1c = w->b1_core;
+  a.w2c = w->w2_core;
+  a.b2c = w->b2_core;
+  a.w1e = static_cast<const char*>(w->w1_exp);
+  a.b1e = w->b1_exp;
+  a.w2e = w->w2_exp;
+  a.b2e = w->b2_exp;
+  a.r_core = w->r_core;
+  a.r_exp = w->r_exp;
+  a.n_seg = w->n_seg;
+  a.logits = logits;
+  a.probs = probs;
+  return a;
+}
+
+// gate/up: tokens (row map2[map1[j]] of `tok`) -> act[omap1[j]] (or act[j])
+FfnGemmArgs gateup_args(const ce_ffn_w* w, const ce_batch* b, const char* tok, const int32_t* map1,
+                        const int32_t* map2, char* act, const int32_t* omap1, const int32_t* kt,
+                        const int32_t* n0) {
+  const int elem = elem_size(w->dtype);
+  FfnGemmArgs a = {};
+  for (int s = 0; s < 2; ++s) {
+    const int ss = s < w->n_sets ? s : 0;
+    a.w0[s] = static_cast<const char*>(w->w_gate[ss]);
+    a.w1[s] = static_cast<const char*>(w->w_up[ss]);
+  }
+  a.w_ld = (int64_t)w->d * elem;
+  a.n_feat = w->d_ff;
+  a.k_bytes = w->d * elem;
+  a.tok = tok;
+  a.tok_ld = (int64_t)w->d * elem;
+  a.map1 = map1;
+  a.map2 = map2;
+  a.out = act;
+  a.out_ld = (int64_t)w->d_ff * elem;
+  a.omap1 = omap1;
+  a.omap2 = nullptr;
+  a.kt_ptr = kt;
+  a.cap = b->kept_capacity;
+  a.n0_ptr = n0;
+  a.n_sets = w->n_sets;
+  return a;
+}
+
+// down: act[map1[j]] (or act[j]) -> out[omap2[omap1[j]]] (+ res at the same row)
+FfnGemmArgs down_args(const ce_ffn_w* w, const ce_batch* b, const char* act, const int32_t* map1,
+                      char* out, const int32_t* omap1, const int32_t* omap2, const char* res,
+                      const int32_t* kt, const int32_t* n0) {
+  const int elem = elem_size(w->dtype);
+  FfnGemmArgs a = {};
+  for (int s = 0; s < 2; ++s) {
+    const int ss = s < w->n_sets ? s : 0;
+    a.w0[s] = static_cast<const char*>(w->w_down[ss]);
+    a.w1[s] = nullptr;
+  }
+  a.w_ld = (int64_t)w->d_ff * elem;
+  a.n_feat = w->d;
+  a.k_bytes = w->d_ff * elem;
+  a.tok = act;
+  a.tok_ld = (int64_t)w->d_ff * elem;
+  a.map1 = map1;
+  a.map2 = nullptr;
+  a.out = out;
+  a.out_ld = (int64_t)w->d * elem;
+  a.omap1 = omap1;
+  a.omap2 = omap2;
+  a.res = res;
+  a.res_ld = (int64_t)w->d * elem;
+  a.kt_ptr = kt;
+  a.cap = b->kept_capacity;
+  a.n0_ptr = n0;
+  a.n_sets = w->n_sets;
+  return a;
+}
+
+// Shared argument checks of the staged FFN calls; on success fills the
+// MoT grouping (launching the group kernel when there are two weight sets).
+int ffn_prologue(const ce_batch* batch, const void* in, const int32_t* kept_idx,
+                 const int32_t* kept_offsets, const ce_ffn_w* w, const void* out, void* ws,
+                 size_t ws_bytes, hipStream_t s, int32_t** grp, int32_t** n0) {
+  CE_CHECK(check_batch(batch, false));
+  CE_CHECK(check_ffn(w));
+  if (!kept_offsets) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && (!in || !kept_idx || !out)) return CE_ERR_INVALID_ARG;
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d_ff,
+                               elem_size(w->dtype));
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  *grp = nullptr;
+  *n0 = nullptr;
+  if (batch->kept_capacity == 0) return CE_OK;
+  if (w->n_sets == 2) {
+    *grp = at<int32_t>(ws, L.grp_rows);
+    *n0 = at<int32_t>(ws, L.grp_n0);
+    CE_TRY(launch_group(kept_idx, kept_offsets, batch->B, batch->kept_capacity, batch->T,
+                        batch->flags, *grp, *n0, s));
+  }
+  return CE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ce_workspace_status(const void* ws, uint32_t* status_out, void* stream) {
+  if (!ws || !status_out) return CE_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  CE_TRY(hipMemcpyAsync(status_out, ws, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  CE_TRY(hipStreamSynchronize(s));
+  return CE_OK;
+}
+
+int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w, float* logits,
+             float* probs, void* stream) {
+  CE_CHECK(check_batch(batch, w != nullptr && w->r_exp > 0));
+  CE_CHECK(check_scorer(w));
+  if (batch->T > 0 && (!hidden || !logits)) return CE_ERR_INVALID_ARG;
+  if (batch->T == 0) return CE_OK;
+  const ScoreArgs a = make_score_args(batch, hidden, w, logits, probs);
+  return hip_status(launch_score(a, w->dtype == CE_BF16, static_cast<hipStream_t>(stream)));
+}
+
+int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidden, int dtype,
+                    int32_t d, int32_t* kept_idx, int32_t* kept_offsets, int32_t* token_pos,
+                    void* compact, void* ws, size_t ws_bytes, void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  if (!kept_offsets) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && !logits) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && !kept_idx) return CE_ERR_INVALID_ARG;
+  if (compact) {
+    CE_CHECK(check_dtype_d(dtype, d));
+    if (batch->T > 0 && !hidden) return CE_ERR_INVALID_ARG;
+  }
+  const int elem = compact ? elem_size(dtype) : 4;
+  const WsLayout L = ws_layout(CE_WS_TOPK, batch->B, batch->T, batch->kept_capacity, 0, elem);
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* info = at<int32_t>(ws, L.seq_info);
+  CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));
+  SelectArgs sa;
+  sa.logits = logits;
+  sa.flags = batch->flags;
+  sa.info = info;
+  sa.B = batch->B;
+  sa.keep = batch->keep;
+  sa.cap = batch->kept_capacity;
+  sa.kept_idx = kept_idx;
+  sa.kept_offsets = kept_offsets;
+  sa.token_pos = token_pos;
+  sa.status = at<uint32_t>(ws, L.status);
+  CE_TRY(launch_select(sa, s));
+  if (compact)
+    CE_TRY(launch_gather(static_cast<const char*>(hidden), (int64_t)d * elem, kept_idx, kept_offsets,
+                         batch->B, batch->kept_capacity, static_cast<char*>(compact), s));
+  return CE_OK;
+}
+
+int ce_ffn_gateup(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
+                  const int32_t* kept_offsets, const ce_ffn_w* w, void* act, void* ws,
+                  size_t ws_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t *grp, *n0;
+  CE_CHECK(ffn_prologue(batch, compact, kept_idx, kept_offsets, w, act, ws, ws_bytes, s, &grp, &n0));
+  if (batch->kept_capacity == 0) return CE_OK;
+  const FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr,
+                                    static_cast<char*>(act), grp, kept_offsets + batch->B, n0);
+  CE_TRY(launch_ffn_gateup(g, w->dtype == CE_BF16, s));
+  return CE_OK;
+}
+
+int ce_ffn_down(const ce_batch* batch, const void* act, const int32_t* kept_idx,
+                const int32_t* kept_offsets, const ce_ffn_w* w, void* ffn_out, void* ws,
+                size_t ws_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t *grp, *n0;
+  CE_CHECK(ffn_prologue(batch, act, kept_idx, kept_offsets, w, ffn_out, ws, ws_bytes, s, &grp, &n0));
+  if (batch->kept_capacity == 0) return CE_OK;
+  const FfnGemmArgs dn = down_args(w, batch, static_cast<const char*>(act), grp,
+                                   static_cast<char*>(ffn_out), grp, nullptr, nullptr,
+                                   kept_offsets + batch->B, n0);
+  CE_TRY(launch_ffn_down(dn, w->dtype == CE_BF16, s));
+  return CE_OK;
+}
+
+int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
+                  const int32_t* kept_offsets, const ce_ffn_w* w, void* ffn_out, void* ws,
+                  size_t ws_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t *grp, *n0;
+  CE_CHECK(ffn_prologue(batch, compact, kept_idx, kept_offsets, w, ffn_out, ws, ws_bytes, s, &grp,
+                        &n0));
+  if (batch->kept_capacity == 0) return CE_OK;
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d_ff,
+                               elem_size(w->dtype));
+  const bool bf16 = w->dtype == CE_BF16;
+  const int32_t* kt = kept_offsets + batch->B;
+  // activations stay in grouped GEMM order inside the workspace
+  char* act = at<char>(ws, L.act);
+  const FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr, act,
+                                    nullptr, kt, n0);
+  CE_TRY(launch_ffn_gateup(g, bf16, s));
+  const FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr,
+                                   nullptr, kt, n0);
+  CE_TRY(launch_ffn_down(dn, bf16, s));
+  return CE_OK;
+}
+
+int ce_scatter_residual(const ce_batch* batch, const void* ffn_out, const int32_t* kept_idx,
+                        const int32_t* kept_offsets, int dtype, int32_t d, const void* hidden_in,
+                        void* hidden_out, void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  CE_CHECK(check_dtype_d(dtype, d));
+  if (!kept_offsets) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && (!hidden_in || !hidden_out)) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && (!ffn_out || !kept_idx)) return CE_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int elem = elem_size(dtype);
+  if (hidden_in != hidden_out)
+    CE_TRY(launch_copy_rows(static_cast<const char*>(hidden_in), static_cast<char*>(hidden_out),
+                            (int64_t)d * elem, batch->T, nullptr, s));
+  CE_TRY(launch_scatter(static_cast<const char*>(ffn_out), kept_idx, kept_offsets, batch->B,
+                        batch->kept_capacity, batch->T, d, dtype == CE_BF16,
+                        static_cast<const char*>(hidden_in), static_cast<char*>(hidden_out), s));
+  return CE_OK;
+}
+
+int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_out,
+                    const ce_scorer_w* scorer, const ce_ffn_w* ffn, float* logits_out,
+                    int32_t* kept_idx_out, int32_t* kept_offsets_out, void* ws, size_t ws_bytes,
+                    void* stream) {
+  CE_CHECK(check_batch(batch, scorer != nullptr && scorer->r_exp > 0));
+  CE_CHECK(check_scorer(scorer));
+  CE_CHECK(check_ffn(ffn));
+  if (scorer->d != ffn->d || scorer->dtype != ffn->dtype) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && (!hidden_in || !hidden_out)) return CE_ERR_INVALID_ARG;
+  const int elem = elem_size(ffn->dtype);
+  const WsLayout L = ws_layout(CE_WS_BLOCK, batch->B, batch->T, batch->kept_capacity, ffn->d_ff, elem);
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf16 = ffn->dtype == CE_BF16;
+  float* logits = logits_out ? logits_out : at<float>(ws, L.logits);
+  int32_t* kept_idx = kept_idx_out ? kept_idx_out : at<int32_t>(ws, L.kept_idx);
+  int32_t* kept_off = kept_offsets_out ? kept_offsets_out : at<int32_t>(ws, L.kept_off);
+  int32_t* token_pos = at<int32_t>(ws, L.token_pos);
+  int32_t* info = at<int32_t>(ws, L.seq_info);
+
+  // 1. routing logits (Eq. 4)
+  if (batch->T > 0) {
+    const ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
+    CE_TRY(launch_score(sa, bf16, s));
+  }
+  // 2-3. per-sequence TopK + packed index maps (Eq. 6)
+  CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));
+  SelectArgs sel;
+  sel.logits = logits;
+  sel.flags = batch->flags;
+  sel.info = info;
+  sel.B = batch->B;
+  sel.keep = batch->keep;
+  sel.cap = batch->kept_capacity;
+  sel.kept_idx = kept_idx;
+  sel.kept_offsets = kept_off;
+  sel.token_pos = token_pos;
+  sel.status = at<uint32_t>(ws, L.status);
+  CE_TRY(launch_select(sel, s));
+  // bypass path for a separate output buffer: dropped rows copied unchanged
+  if (hidden_in != hidden_out)
+    CE_TRY(launch_copy_rows(static_cast<const char*>(hidden_in), static_cast<char*>(hidden_out),
+                            (int64_t)ffn->d * elem, batch->T, token_pos, s));
+  if (batch->kept_capacity == 0) return CE_OK;
+  // 4. SwiGLU FFN on the retained rows, gathered straight from hidden_in
+  const int32_t* kt = kept_off + batch->B;
+  int32_t* grp = nullptr;
+  int32_t* n0 = nullptr;
+  if (ffn->n_sets == 2) {
+    grp = at<int32_t>(ws, L.grp_rows);
+    n0 = at<int32_t>(ws, L.grp_n0);
+    CE_TRY(launch_group(kept_idx, kept_off, batch->B, batch->kept_capacity, batch->T, batch->flags,
+                        grp, n0, s));
+  }
+  char* act = at<char>(ws, L.act);
+  const FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx,
+                                    act, nullptr, kt, n0);
+  CE_TRY(launch_ffn_gateup(g, bf16, s));
+  // 5. down projection + residual, scattered straight into the token rows
+  const FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
+                                   kept_idx, static_cast<const char*>(hidden_in), kt, n0);
+  CE_TRY(launch_ffn_down(dn, bf16, s));
+  return CE_OK;
+}
+
+}  // extern "C"

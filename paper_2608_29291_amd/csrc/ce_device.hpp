@@ -1,0 +1,148 @@
+// Device helpers shared by the CE-Router kernels (gfx950 / CDNA4 only).
+//
+// Tiles are staged through LDS in 16-byte chunks: one tile row holds
+// KB = 128 bytes of the contraction dimension (64 bf16 or 32 fp32 values) as
+// 8 chunks, stored at chunk slot (c ^ (row & 7)) so that the 16-byte MFMA
+// fragment reads of 8 consecutive rows hit distinct LDS banks.
+//
+// MFMA operand convention used everywhere: the "A" operand (output rows) is a
+// weight matrix row block (features / scorer ranks), the "B" operand (output
+// columns) is a block of 32 token rows. Both are K-contiguous in memory. For a
+// 32-byte step of K, lane l supplies chunk (2*s + l/32) of row (l % 32) for both
+// operands, so A and B always agree on which K values meet. The 32x32 output
+// block then holds, in lane l and accumulator v:
+//   column (token)  = l % 32
+//   row (feature)   = 8*(v/4) + 4*(l/32) + (v%4)
+// i.e. 4 consecutive features per (lane, v/4): outputs are stored as 8-byte
+// (bf16) or 16-byte (fp32) vectors.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ce {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kKB = 128;     // bytes of K per staged tile row
+constexpr int kChunks = 8;   // 16-byte chunks per staged tile row
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// float32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float silu_f32(float x) { return x / (1.0f + __expf(-x)); }
+
+// LDS byte offset of chunk c of tile row r (XOR swizzle over 8 chunks).
+__device__ __forceinline__ int lds_chunk_off(int r, int c) {
+  return (r * kChunks + (c ^ (r & 7))) * 16;
+}
+
+// One 32-byte K step on a 32x32 block. `a` and `b` are this lane's 16-byte
+// chunks of the A (weights) and B (tokens) operands.
+template <bool kBF16>
+__device__ __forceinline__ void mfma_step(f32x16_t& acc, const u32x4_t& a, const u32x4_t& b) {
+  if constexpr (kBF16) {
+    bf16x8_t av = __builtin_bit_cast(bf16x8_t, a);
+    bf16x8_t bv = __builtin_bit_cast(bf16x8_t, b);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bv, acc, 0, 0, 0);
+  } else {
+    // fp32: each 16-byte chunk holds 4 K values; 4 MFMAs of K = 2 (one value
+    // per lane half) cover the 8 values of the step.
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ u32x4_t lds_read16(const char* lds, int off) {
+  return *reinterpret_cast<const u32x4_t*>(lds + off);
+}
+
+__device__ __forceinline__ void lds_write16(char* lds, int off, const u32x4_t& v) {
+  *reinterpret_cast<u32x4_t*>(lds + off) = v;
+}
+
+__device__ __forceinline__ u32x4_t gload16(const char* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+}
+
+__device__ __forceinline__ u32x4_t gload16_cached(const char* p) {
+  return *reinterpret_cast<const u32x4_t*>(p);
+}
+
+// Store 4 consecutive output values (fp32 accumulators) as dtype.
+template <bool kBF16>
+__device__ __forceinline__ void store4(char* p, float a, float b, float c, float d) {
+  if constexpr (kBF16) {
+    u32x2_t v;
+    v.x = f32_to_bf16(a) | (f32_to_bf16(b) << 16);
+    v.y = f32_to_bf16(c) | (f32_to_bf16(d) << 16);
+    *reinterpret_cast<u32x2_t*>(p) = v;
+  } else {
+    f32x4_t v = {a, b, c, d};
+    *reinterpret_cast<f32x4_t*>(p) = v;
+  }
+}
+
+// Load 4 consecutive values of dtype as fp32.
+template <bool kBF16>
+__device__ __forceinline__ f32x4_t load4(const char* p) {
+  f32x4_t r;
+  if constexpr (kBF16) {
+    u32x2_t v = *reinterpret_cast<const u32x2_t*>(p);
+    r.x = bf16_to_f32(v.x & 0xffffu);
+    r.y = bf16_to_f32(v.x >> 16);
+    r.z = bf16_to_f32(v.y & 0xffffu);
+    r.w = bf16_to_f32(v.y >> 16);
+  } else {
+    r = *reinterpret_cast<const f32x4_t*>(p);
+  }
+  return r;
+}
+
+// Order-preserving uint32 key of a float32 logit: larger logit -> larger key;
+// -0 and +0 share a key; every NaN maps to 0, below -inf (0x007fffff).
+__device__ __forceinline__ uint32_t logit_key(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// k = ceil(keep * n), exact, on the float32 bit pattern of keep (keep in [0, 1]).
+__device__ __forceinline__ int32_t num_keep_dev(float keep, int32_t n) {
+  if (n <= 0) return 0;
+  uint32_t u = __float_as_uint(keep);
+  if (u == 0u || u == 0x80000000u) return 0;
+  int e = (int)((u >> 23) & 0xffu);
+  uint64_t m = u & 0x7fffffu;
+  int ex;
+  if (e == 0) {
+    ex = -149;
+  } else {
+    m |= 0x800000u;
+    ex = e - 150;
+  }
+  uint64_t p = m * (uint64_t)(uint32_t)n;
+  if (ex >= 0) return (int32_t)(p << ex);
+  int s = -ex;
+  if (s >= 63) return p ? 1 : 0;
+  uint64_t k = (p + ((1ull << s) - 1ull)) >> s;
+  return (int32_t)k;
+}
+
+}  // namespace ce

@@ -1,0 +1,233 @@
+// SwiGLU FFN over the packed (retained) rows: the gate/up GEMM with the SwiGLU
+// epilogue, and the down GEMM with an optional residual-scatter epilogue.
+//
+// Both are "weights x tokens" GEMMs on MFMA (bf16 32x32x16 with fp32
+// accumulation, or fp32 32x32x2 for fp32 data), staged through a double-buffered,
+// XOR-swizzled LDS tile with one barrier per 128-byte K step.
+//
+// Row mapping: GEMM row j (packed order, grouped by FFN set for MoT) maps to a
+// source row through up to two index arrays: r = map2[map1[j]] (each level is
+// skipped when its pointer is NULL). This lets the same kernel read rows
+// straight out of the full hidden-state matrix (the gather fused into the A
+// loads) or out of a packed buffer, and write results straight back to the
+// token rows (the scatter fused into the epilogue).
+//
+// The number of packed rows Kt and the size n0 of the first MoT group live in
+// device memory; the grid is sized from the host-known capacity and tiles past
+// Kt exit at once.
+#include "ce_device.hpp"
+#include "ce_launch.hpp"
+
+namespace ce {
+
+namespace {
+
+__device__ __forceinline__ int map_row(int j, const int32_t* m1, const int32_t* m2) {
+  int r = m1 ? m1[j] : j;
+  return m2 ? m2[r] : r;
+}
+
+// kMode 0: gate/up + SwiGLU -> out[orow(j)][f]
+// kMode 1: down (+ residual) -> out[orow(j)][f]
+template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT>
+__global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
+  constexpr int kElem = kBF16 ? 2 : 4;
+  constexpr int kWaves = kWW * kWT;
+  static_assert(kWaves == 4, "4 waves per workgroup");
+  constexpr int kWRw = kWR / kWW;  // weight rows per wave
+  constexpr int kTRw = kTR / kWT;  // token rows per wave
+  constexpr int kMW = kWRw / 32;
+  constexpr int kMT = kTRw / 32;
+  static_assert(kMode == 1 || (kMW % 2) == 0, "gate/up blocks come in pairs");
+  constexpr int kWLoads = kWR * kChunks / 256;
+  constexpr int kTLoads = kTR * kChunks / 256;
+  constexpr int kStage = (kWR + kTR) * kKB;
+
+  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int ww = wave % kWW;
+  const int wt = wave / kWW;
+
+  // ---- which packed rows this tile covers (grouped by weight set) ----
+  int kt = *a.kt_ptr;
+  kt = kt < 0 ? 0 : (kt > a.cap ? a.cap : kt);
+  int n0 = kt;
+  if (a.n_sets == 2 && a.n0_ptr) {
+    n0 = *a.n0_ptr;
+    n0 = n0 < 0 ? 0 : (n0 > kt ? kt : n0);
+  }
+  const int tiles0 = (n0 + kTR - 1) / kTR;
+  int set, row_lo, row_hi;
+  if ((int)blockIdx.x < tiles0) {
+    set = 0;
+    row_lo = blockIdx.x * kTR;
+    row_hi = min(row_lo + kTR, n0);
+  } else {
+    set = 1;
+    row_lo = n0 + (blockIdx.x - tiles0) * kTR;
+    row_hi = min(row_lo + kTR, kt);
+  }
+  if (row_lo >= row_hi) return;
+
+  const int n_feat = a.n_feat;
+  const int f_tile = (kMode == 0) ? kWR / 2 : kWR;
+  const int f0 = blockIdx.y * f_tile;
+
+  // ---- per-thread source row pointers (fixed over the K loop) ----
+  const int cchunk = tid & 7;
+  const char* wsrc[kWLoads];
+#pragma unroll
+  for (int i = 0; i < kWLoads; ++i) {
+    const int r = i * 32 + (tid >> 3);
+    int feat;
+    const char* base;
+    if constexpr (kMode == 0) {
+      const int blk = r >> 5;
+      feat = f0 + 32 * (blk >> 1) + (r & 31);
+      base = (blk & 1) ? a.w1[set] : a.w0[set];
+    } else {
+      feat = f0 + r;
+      base = a.w0[set];
+    }
+    wsrc[i] = (feat < n_feat) ? base + (int64_t)feat * a.w_ld + cchunk * 16 : nullptr;
+  }
+  const char* tsrc[kTLoads];
+#pragma unroll
+  for (int i = 0; i < kTLoads; ++i) {
+    const int r = i * 32 + (tid >> 3);
+    const int j = row_lo + r;
+    tsrc[i] = (j < row_hi) ? a.tok + (int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + cchunk * 16
+                           : nullptr;
+  }
+
+  u32x4_t wreg[kWLoads], treg[kTLoads];
+  auto gload = [&](int kb) {
+    const int koff = kb * kKB;
+#pragma unroll
+    for (int i = 0; i < kWLoads; ++i) {
+      if (wsrc[i]) wreg[i] = gload16_cached(wsrc[i] + koff);
+      else wreg[i] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < kTLoads; ++i) {
+      if (tsrc[i]) treg[i] = gload16_cached(tsrc[i] + koff);
+      else treg[i] = u32x4_t{0u, 0u, 0u, 0u};
+    }
+  };
+  auto lstore = [&](int buf) {
+    char* s = smem + buf * kStage;
+#pragma unroll
+    for (int i = 0; i < kWLoads; ++i) lds_write16(s, lds_chunk_off(i * 32 + (tid >> 3), cchunk), wreg[i]);
+#pragma unroll
+    for (int i = 0; i < kTLoads; ++i)
+      lds_write16(s + kWR * kKB, lds_chunk_off(i * 32 + (tid >> 3), cchunk), treg[i]);
+  };
+
+  f32x16_t acc[kMW][kMT];
+#pragma unroll
+  for (int i = 0; i < kMW; ++i)
+#pragma unroll
+    for (int j = 0; j < kMT; ++j) acc[i][j] = f32x16_t{};
+
+  const int nk = a.k_bytes / kKB;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+
+  const int lrow = lane & 31;
+  const int lhalf = lane >> 5;
+  for (int kb = 0; kb < nk; ++kb) {
+    if (kb + 1 < nk) gload(kb + 1);
+    const char* s = smem + (kb & 1) * kStage;
+    const char* sw = s;
+    const char* st = s + kWR * kKB;
+#pragma unroll
+    for (int step = 0; step < 4; ++step) {
+      const int c = 2 * step + lhalf;
+      u32x4_t fa[kMW], fb[kMT];
+#pragma unroll
+      for (int i = 0; i < kMW; ++i) fa[i] = lds_read16(sw, lds_chunk_off(ww * kWRw + 32 * i + lrow, c));
+#pragma unroll
+      for (int j = 0; j < kMT; ++j) fb[j] = lds_read16(st, lds_chunk_off(wt * kTRw + 32 * j + lrow, c));
+#pragma unroll
+      for (int i = 0; i < kMW; ++i)
+#pragma unroll
+        for (int j = 0; j < kMT; ++j) mfma_step<kBF16>(acc[i][j], fa[i], fb[j]);
+    }
+    if (kb + 1 < nk) lstore((kb + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue ----
+#pragma unroll
+  for (int j = 0; j < kMT; ++j) {
+    const int jr = row_lo + wt * kTRw + 32 * j + lrow;
+    if (jr >= row_hi) continue;
+    if constexpr (kMode == 0) {
+      char* orow = a.out + (int64_t)map_row(jr, a.omap1, a.omap2) * a.out_ld;
+#pragma unroll
+      for (int p = 0; p < kMW / 2; ++p) {
+        const int fb = f0 + 32 * (ww * (kMW / 2) + p) + 4 * lhalf;
+        if (fb >= n_feat) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16_t& ag = acc[2 * p][j];
+          const f32x16_t& au = acc[2 * p + 1][j];
+          float v0 = silu_f32(ag[4 * g + 0]) * au[4 * g + 0];
+          float v1 = silu_f32(ag[4 * g + 1]) * au[4 * g + 1];
+          float v2 = silu_f32(ag[4 * g + 2]) * au[4 * g + 2];
+          float v3 = silu_f32(ag[4 * g + 3]) * au[4 * g + 3];
+          store4<kBF16>(orow + (int64_t)(fb + 8 * g) * kElem, v0, v1, v2, v3);
+        }
+      }
+    } else {
+      const int orow_idx = map_row(jr, a.omap1, a.omap2);
+      char* orow = a.out + (int64_t)orow_idx * a.out_ld;
+      const char* rrow = a.res ? a.res + (int64_t)orow_idx * a.res_ld : nullptr;
+#pragma unroll
+      for (int i = 0; i < kMW; ++i) {
+        const int fb = f0 + ww * kWRw + 32 * i + 4 * lhalf;
+        if (fb >= n_feat) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int f = fb + 8 * g;
+          float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
+          float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+          if (rrow) {
+            f32x4_t r = load4<kBF16>(rrow + (int64_t)f * kElem);
+            v0 += r.x; v1 += r.y; v2 += r.z; v3 += r.w;
+          }
+          store4<kBF16>(orow + (int64_t)f * kElem, v0, v1, v2, v3);
+        }
+      }
+    }
+  }
+}
+
+template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT>
+hipError_t launch_one(const FfnGemmArgs& a, hipStream_t stream) {
+  const int f_tile = (kMode == 0) ? kWR / 2 : kWR;
+  const int tiles_x = (a.cap + kTR - 1) / kTR + (a.n_sets - 1);
+  const int tiles_y = (a.n_feat + f_tile - 1) / f_tile;
+  if (tiles_x <= 0 || tiles_y <= 0) return hipSuccess;
+  dim3 grid(tiles_x, tiles_y);
+  hipLaunchKernelGGL((ffn_gemm_kernel<kBF16, kMode, kWR, kTR, kWW, kWT>), grid, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
+  if (bf16) return launch_one<true, 0, 128, 128, 2, 2>(a, stream);
+  return launch_one<false, 0, 128, 128, 2, 2>(a, stream);
+}
+
+hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
+  if (bf16) return launch_one<true, 1, 128, 128, 2, 2>(a, stream);
+  return launch_one<false, 1, 128, 128, 2, 2>(a, stream);
+}
+
+}  // namespace ce

@@ -1,0 +1,161 @@
+// Host-only part of the C ABI (validation, workspace layout, keep-count rule,
+// status strings). Pure C++: no HIP headers.
+#include "ce_host.hpp"
+
+#include <math.h>
+#include <string.h>
+
+namespace ce {
+
+static size_t align_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+int elem_size(int dtype) {
+  if (dtype == CE_BF16) return 2;
+  if (dtype == CE_F32) return 4;
+  return 0;
+}
+
+WsLayout ws_layout(int which, int B, int T, int cap, int d_ff, int elem) {
+  WsLayout L;
+  memset(&L, 0, sizeof(L));
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + (bytes ? bytes : 1));
+    return at;
+  };
+  const size_t sB = (size_t)(B < 0 ? 0 : B);
+  const size_t sT = (size_t)(T < 0 ? 0 : T);
+  const size_t sC = (size_t)(cap < 0 ? 0 : cap);
+  const size_t sF = (size_t)(d_ff < 0 ? 0 : d_ff);
+  L.status = take(16);
+  if (which == CE_WS_TOPK || which == CE_WS_BLOCK) L.seq_info = take(3 * sB * 4);
+  if (which == CE_WS_BLOCK) {
+    L.kept_off = take((sB + 1) * 4);
+    L.kept_idx = take(sC * 4);
+    L.token_pos = take(sT * 4);
+    L.logits = take(sT * 4);
+  }
+  if (which == CE_WS_FFN || which == CE_WS_BLOCK) {
+    L.grp_rows = take(sC * 4);
+    L.grp_n0 = take(4);
+    L.act = take(sC * sF * (size_t)elem);
+  }
+  L.total = off;
+  return L;
+}
+
+int32_t num_keep_host(float keep, int32_t n) {
+  if (n < 0) return -1;
+  if (!(keep >= 0.0f && keep <= 1.0f)) return -1;  // also rejects NaN
+  if (n == 0 || keep == 0.0f) return 0;
+  uint32_t u;
+  memcpy(&u, &keep, 4);
+  const int e = (int)((u >> 23) & 0xffu);
+  uint64_t m = u & 0x7fffffu;
+  int ex;
+  if (e == 0) {
+    ex = -149;
+  } else {
+    m |= 0x800000u;
+    ex = e - 150;
+  }
+  // keep = m * 2^ex exactly; k = ceil(m * n / 2^-ex) in 64-bit integers
+  const uint64_t p = m * (uint64_t)(uint32_t)n;  // < 2^55
+  if (ex >= 0) return (int32_t)(p << ex);
+  const int s = -ex;
+  if (s >= 63) return p ? 1 : 0;
+  return (int32_t)((p + ((1ull << s) - 1ull)) >> s);
+}
+
+int check_batch(const ce_batch* b, bool need_t) {
+  if (!b) return CE_ERR_INVALID_ARG;
+  if (b->B < 1 || b->T < 0 || b->kept_capacity < 0) return CE_ERR_INVALID_ARG;
+  if (!b->seq_offsets) return CE_ERR_INVALID_ARG;
+  if (b->T > 0 && !b->flags) return CE_ERR_INVALID_ARG;
+  if (need_t && !b->t) return CE_ERR_INVALID_ARG;
+  if (!(b->keep >= 0.0f && b->keep <= 1.0f)) return CE_ERR_INVALID_ARG;
+  return CE_OK;
+}
+
+int check_dtype_d(int dtype, int32_t d) {
+  if (dtype != CE_F32 && dtype != CE_BF16) return CE_ERR_UNSUPPORTED;
+  if (d <= 0 || (d % 64) != 0) return CE_ERR_UNSUPPORTED;
+  return CE_OK;
+}
+
+int check_scorer(const ce_scorer_w* w) {
+  if (!w) return CE_ERR_INVALID_ARG;
+  int st = check_dtype_d(w->dtype, w->d);
+  if (st != CE_OK) return st;
+  if (w->r_core < 32 || (w->r_core % 32) != 0) return CE_ERR_UNSUPPORTED;
+  if (w->r_exp < 0 || (w->r_exp % 32) != 0) return CE_ERR_UNSUPPORTED;
+  if (w->r_core + w->r_exp > kMaxRanks) return CE_ERR_UNSUPPORTED;
+  if (w->n_seg < 1 || w->n_seg > kMaxSeg) return CE_ERR_UNSUPPORTED;
+  if (!w->w1_core || !w->w2_core) return CE_ERR_INVALID_ARG;
+  if (w->r_exp > 0 && (!w->w1_exp || !w->w2_exp)) return CE_ERR_INVALID_ARG;
+  if (!isfinite(w->b2_core)) return CE_ERR_INVALID_ARG;
+  return CE_OK;
+}
+
+int check_ffn(const ce_ffn_w* w) {
+  if (!w) return CE_ERR_INVALID_ARG;
+  int st = check_dtype_d(w->dtype, w->d);
+  if (st != CE_OK) return st;
+  if (w->d_ff <= 0 || (w->d_ff % 64) != 0) return CE_ERR_UNSUPPORTED;
+  if (w->n_sets != 1 && w->n_sets != 2) return CE_ERR_UNSUPPORTED;
+  for (int s = 0; s < w->n_sets; ++s)
+    if (!w->w_gate[s] || !w->w_up[s] || !w->w_down[s]) return CE_ERR_INVALID_ARG;
+  return CE_OK;
+}
+
+int check_ws(const void* ws, size_t ws_bytes, size_t need) {
+  if (!ws || ws_bytes < need) return CE_ERR_WORKSPACE;
+  if (((uintptr_t)ws % kWsAlign) != 0) return CE_ERR_WORKSPACE;
+  return CE_OK;
+}
+
+}  // namespace ce
+
+extern "C" {
+
+const char* ce_status_string(int status) {
+  switch (status) {
+    case CE_OK: return "CE_OK";
+    case CE_ERR_INVALID_ARG: return "CE_ERR_INVALID_ARG: null pointer, bad size or value out of range";
+    case CE_ERR_UNSUPPORTED: return "CE_ERR_UNSUPPORTED: shape or dtype outside the supported limits";
+    case CE_ERR_WORKSPACE: return "CE_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case CE_ERR_HIP: return "CE_ERR_HIP: a HIP runtime call failed";
+    default: return "unknown ce_router status";
+  }
+}
+
+const char* ce_version(void) { return "ce_router 0.1.0 gfx950"; }
+
+int32_t ce_num_keep(float keep, int32_t n_routable) { return ce::num_keep_host(keep, n_routable); }
+
+int64_t ce_kept_count_host(int32_t B, int32_t T, const int32_t* offs, const uint8_t* flags,
+                           float keep) {
+  if (B < 1 || T < 0 || !offs || (T > 0 && !flags)) return -1;
+  if (!(keep >= 0.0f && keep <= 1.0f)) return -1;
+  if (offs[0] != 0 || offs[B] != T) return -1;
+  int64_t total = 0;
+  for (int b = 0; b < B; ++b) {
+    const int lo = offs[b], hi = offs[b + 1];
+    if (hi < lo || lo < 0 || hi > T) return -1;
+    int a = 0;
+    for (int i = lo; i < hi; ++i) a += (flags[i] & CE_TOK_KEEP) ? 1 : 0;
+    total += a + ce::num_keep_host(keep, hi - lo - a);
+  }
+  return total;
+}
+
+size_t ce_workspace_size(int which, const ce_batch* batch, int32_t d, int32_t d_ff, int dtype) {
+  (void)d;
+  if (!batch || (which != CE_WS_TOPK && which != CE_WS_FFN && which != CE_WS_BLOCK)) return 0;
+  const int elem = ce::elem_size(dtype);
+  if (!elem) return 0;
+  return ce::ws_layout(which, batch->B, batch->T, batch->kept_capacity, d_ff, elem).total;
+}
+
+}  // extern "C"

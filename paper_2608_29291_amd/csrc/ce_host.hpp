@@ -1,0 +1,44 @@
+// Host-only logic of the C ABI: argument validation, workspace layout and the
+// exact keep-count rule. No HIP calls here, so this part also builds and runs
+// on a machine without a GPU.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ce_router.h"
+
+namespace ce {
+
+constexpr size_t kWsAlign = 256;
+constexpr int kMaxRanks = 512;
+constexpr int kMaxSeg = 16;
+
+// Byte offsets of each workspace region (0 = region absent for that kind).
+struct WsLayout {
+  size_t status;     // uint32 status word (+ padding)
+  size_t seq_info;   // int32 [3 * B]
+  size_t kept_off;   // int32 [B + 1]  (block path, when the caller passes none)
+  size_t kept_idx;   // int32 [cap]    (block path)
+  size_t token_pos;  // int32 [T]      (block path)
+  size_t logits;     // float [T]      (block path)
+  size_t grp_rows;   // int32 [cap]    (MoT grouping)
+  size_t grp_n0;     // int32          (MoT group size)
+  size_t act;        // dtype [cap * d_ff] SwiGLU activations
+  size_t total;
+};
+
+WsLayout ws_layout(int which, int B, int T, int cap, int d_ff, int elem);
+
+int elem_size(int dtype);  // 2 for bf16, 4 for f32, 0 if unknown
+
+int32_t num_keep_host(float keep, int32_t n);
+
+// Validation: each returns CE_OK or a negative status.
+int check_batch(const ce_batch* b, bool need_t);
+int check_dtype_d(int dtype, int32_t d);
+int check_scorer(const ce_scorer_w* w);
+int check_ffn(const ce_ffn_w* w);
+int check_ws(const void* ws, size_t ws_bytes, size_t need);
+
+}  // namespace ce

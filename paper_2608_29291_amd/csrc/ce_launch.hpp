@@ -1,0 +1,100 @@
+// Internal launcher interface between the C-ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ce {
+
+// One "weights x tokens" FFN GEMM (see ce_ffn.hip).
+struct FfnGemmArgs {
+  // weights: rows = output features, K-contiguous; per set.
+  //   gate/up mode: w0 = W_gate, w1 = W_up; down mode: w0 = W_down.
+  const char* w0[2];
+  const char* w1[2];
+  int64_t w_ld;     // bytes per weight row
+  int n_feat;       // output features (d_ff or d)
+  int k_bytes;      // bytes of the contraction per row (multiple of 128)
+  // tokens: GEMM row j reads row map2[map1[j]] of `tok`
+  const char* tok;
+  int64_t tok_ld;
+  const int32_t* map1;
+  const int32_t* map2;
+  // output: row omap2[omap1[j]] of `out` (each level skipped when NULL)
+  char* out;
+  int64_t out_ld;
+  const int32_t* omap1;
+  const int32_t* omap2;
+  const char* res;  // down only: residual rows (same row map as out), or NULL
+  int64_t res_ld;
+  // sizes on the device
+  const int32_t* kt_ptr;  // number of packed rows (clamped to cap)
+  int cap;
+  const int32_t* n0_ptr;  // rows in the first weight set (MoT), or NULL
+  int n_sets;
+};
+
+hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream);
+hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream);
+
+struct ScoreArgs {
+  const char* hidden;
+  int64_t h_ld;        // bytes per hidden row
+  int k_bytes;         // d * elem
+  int B, T;
+  const int32_t* seq_offsets;
+  const uint8_t* flags;
+  const float* t;
+  const char* w1c;     // [r_core x d]
+  const float* b1c;
+  const float* w2c;
+  float b2c;
+  const char* w1e;     // [n_seg x r_exp x d]
+  const float* b1e;
+  const float* w2e;
+  const float* b2e;
+  int r_core, r_exp, n_seg;
+  float* logits;
+  float* probs;
+};
+hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream);
+
+// Per-sequence summary written by the count kernel: {lo, len, keep_count | bad<<31}.
+hipError_t launch_seq_info(const int32_t* seq_offsets, const uint8_t* flags, int B, int T,
+                           int32_t* info, hipStream_t stream);
+
+struct SelectArgs {
+  const float* logits;
+  const uint8_t* flags;
+  const int32_t* info;
+  int B;
+  float keep;
+  int cap;
+  int32_t* kept_idx;
+  int32_t* kept_offsets;
+  int32_t* token_pos;  // or NULL
+  uint32_t* status;
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
+
+// MoT: stable partition of the packed rows by FFN set (GEN bit).
+// Entries of kept_idx outside [0, T) count as weight set 0.
+hipError_t launch_group(const int32_t* kept_idx, const int32_t* kept_offsets, int B, int cap,
+                        int T, const uint8_t* flags, int32_t* grp_rows, int32_t* n0,
+                        hipStream_t stream);
+
+// compact[j] = hidden[kept_idx[j]] for j < Kt
+hipError_t launch_gather(const char* hidden, int64_t row_bytes, const int32_t* kept_idx,
+                         const int32_t* kept_offsets, int B, int cap, char* compact,
+                         hipStream_t stream);
+
+// out[kept_idx[j]] = in[kept_idx[j]] + ffn[j] for j < Kt (entries outside [0, T) skipped)
+hipError_t launch_scatter(const char* ffn_out, const int32_t* kept_idx, const int32_t* kept_offsets,
+                          int B, int cap, int T, int d, bool bf16, const char* h_in, char* h_out,
+                          hipStream_t stream);
+
+// out[i] = in[i] for every row (token_pos == NULL) or for rows with token_pos[i] < 0
+hipError_t launch_copy_rows(const char* h_in, char* h_out, int64_t row_bytes, int T,
+                            const int32_t* token_pos, hipStream_t stream);
+
+}  // namespace ce

@@ -1,0 +1,219 @@
+"""C ABI on the CPU: every declared symbol is exported, host-side rules and
+argument validation. Nothing here launches a kernel: each call below fails
+host validation before any HIP call is made.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from ce_workloads import config_layout, build_layout, small_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ce_router.h")
+
+ce = pytest.importorskip("paper_2608_29291_amd")
+
+FAKE = 0x10000  # never dereferenced: validation fails first
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(ce_[a-z_]+)\s*\(", txt)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) == 13
+    for n in names:
+        assert hasattr(ce.lib, n), n
+    assert set(names) == set(ce.EXPORTED)
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in ce.ce_version()
+    for code in (0, -1, -2, -3, -4):
+        assert ce.lib.ce_status_string(code).startswith(b"CE_")
+
+
+@pytest.mark.parametrize("keep", [0.0, 0.1, 0.25, 0.3, 0.35, 0.4, 0.5, 0.8, 0.95, 1.0,
+                                  1e-30, 0.999999940395355, 0.3333333])
+def test_num_keep_matches_oracle(keep):
+    for n in [0, 1, 2, 7, 100, 729, 1000, 4096, 8192, 123457, 2 ** 31 - 1]:
+        assert ce.ce_num_keep(keep, n) == oracle.num_keep(np.float32(keep), n), (keep, n)
+
+
+def test_num_keep_rejects():
+    assert ce.ce_num_keep(1.5, 10) == -1
+    assert ce.ce_num_keep(-0.1, 10) == -1
+    assert ce.ce_num_keep(float("nan"), 10) == -1
+    assert ce.ce_num_keep(0.5, -1) == -1
+
+
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 5])
+def test_kept_count_host_matches_oracle(i):
+    offs, flags = build_layout(config_layout(i))
+    keep = {1: 0.5, 2: 0.35, 3: 0.5, 4: 0.4, 5: 0.3}[i]
+    logits = np.random.default_rng(i).standard_normal(len(flags)).astype(np.float32)
+    sel = oracle.select(logits, flags, offs, np.float32(keep))
+    assert ce.ce_kept_count_host(offs, flags, keep) == len(sel["kept_idx"])
+
+
+def test_kept_count_host_rejects_bad_offsets():
+    flags = np.zeros(10, np.uint8)
+    assert ce.ce_kept_count_host(np.array([0, 5, 3, 10], np.int32), flags, 0.5) == -1
+    assert ce.ce_kept_count_host(np.array([1, 10], np.int32), flags, 0.5) == -1
+    assert ce.ce_kept_count_host(np.array([0, 9], np.int32), flags, 0.5) == -1
+
+
+def _batch(B=2, T=100, keep=0.5, cap=100, t=FAKE):
+    return ce.CEBatch(B, T, FAKE, FAKE, t, keep, cap)
+
+
+def _scorer(d=256, r_c=64, r_e=32, n_seg=4, dtype=ce.CE_BF16):
+    return ce.CEScorerW(d, r_c, r_e, n_seg, dtype, FAKE, None, FAKE, 0.0, FAKE, None, FAKE, None)
+
+
+def _ffn(d=256, F=512, n_sets=1, dtype=ce.CE_BF16):
+    w = ce.CEFFNW(d, F, n_sets, dtype)
+    for s in range(min(n_sets, 2)):
+        w.w_gate[s] = FAKE
+        w.w_up[s] = FAKE
+        w.w_down[s] = FAKE
+    return w
+
+
+def score(b, w, hidden=FAKE, logits=FAKE):
+    return ce.lib.ce_score(ctypes.byref(b) if b is not None else None, hidden,
+                           ctypes.byref(w) if w is not None else None, logits, None, None)
+
+
+@pytest.mark.parametrize("mut,code", [
+    (lambda b, w: (None, w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (b, None), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (_batch(B=0), w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (_batch(T=-1), w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (_batch(keep=1.5), w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (_batch(keep=float("nan")), w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (_batch(t=None), w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (b, _scorer(d=100)), ce.CE_ERR_UNSUPPORTED),
+    (lambda b, w: (b, _scorer(dtype=7)), ce.CE_ERR_UNSUPPORTED),
+    (lambda b, w: (b, _scorer(r_c=48)), ce.CE_ERR_UNSUPPORTED),
+    (lambda b, w: (b, _scorer(r_c=0)), ce.CE_ERR_UNSUPPORTED),
+    (lambda b, w: (b, _scorer(r_c=512, r_e=32)), ce.CE_ERR_UNSUPPORTED),
+    (lambda b, w: (b, _scorer(n_seg=0)), ce.CE_ERR_UNSUPPORTED),
+    (lambda b, w: (b, _scorer(n_seg=17)), ce.CE_ERR_UNSUPPORTED),
+])
+def test_score_validation(mut, code):
+    b, w = mut(_batch(), _scorer())
+    assert score(b, w) == code
+
+
+def test_score_null_buffers():
+    assert score(_batch(), _scorer(), hidden=None) == ce.CE_ERR_INVALID_ARG
+    assert score(_batch(), _scorer(), logits=None) == ce.CE_ERR_INVALID_ARG
+    w = _scorer()
+    w.w1_core = None
+    assert score(_batch(), w) == ce.CE_ERR_INVALID_ARG
+    w = _scorer()
+    w.w1_exp = None
+    assert score(_batch(), w) == ce.CE_ERR_INVALID_ARG
+
+
+def test_topk_validation_and_workspace():
+    b = _batch()
+    need = ce.lib.ce_workspace_size(ce.CE_WS_TOPK, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    assert need >= 256 and need % 256 == 0
+    f = ce.lib.ce_topk_compact
+    # workspace too small / missing / misaligned
+    assert f(ctypes.byref(b), FAKE, None, 0, 0, FAKE, FAKE, None, None, FAKE, need - 1, None) == ce.CE_ERR_WORKSPACE
+    assert f(ctypes.byref(b), FAKE, None, 0, 0, FAKE, FAKE, None, None, None, need, None) == ce.CE_ERR_WORKSPACE
+    assert f(ctypes.byref(b), FAKE + 8, None, 0, 0, FAKE, FAKE, None, None, FAKE + 8, need, None) == ce.CE_ERR_WORKSPACE
+    # null outputs
+    assert f(ctypes.byref(b), FAKE, None, 0, 0, None, FAKE, None, None, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), FAKE, None, 0, 0, FAKE, None, None, None, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), None, None, 0, 0, FAKE, FAKE, None, None, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    # compact requested with a bad d / dtype / no hidden
+    assert f(ctypes.byref(b), FAKE, FAKE, ce.CE_BF16, 100, FAKE, FAKE, None, FAKE, FAKE, need, None) == ce.CE_ERR_UNSUPPORTED
+    assert f(ctypes.byref(b), FAKE, FAKE, 5, 256, FAKE, FAKE, None, FAKE, FAKE, need, None) == ce.CE_ERR_UNSUPPORTED
+    assert f(ctypes.byref(b), FAKE, None, ce.CE_BF16, 256, FAKE, FAKE, None, FAKE, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+
+
+def test_ffn_validation():
+    b = _batch()
+    f = ce.lib.ce_routed_ffn
+    need = ce.lib.ce_workspace_size(ce.CE_WS_FFN, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    assert need >= 100 * 512 * 2
+    assert f(ctypes.byref(b), FAKE, FAKE, FAKE, ctypes.byref(_ffn()), FAKE, FAKE, need - 256, None) == ce.CE_ERR_WORKSPACE
+    assert f(ctypes.byref(b), FAKE, FAKE, FAKE, ctypes.byref(_ffn(F=100)), FAKE, FAKE, need, None) == ce.CE_ERR_UNSUPPORTED
+    assert f(ctypes.byref(b), FAKE, FAKE, FAKE, ctypes.byref(_ffn(n_sets=3)), FAKE, FAKE, need, None) == ce.CE_ERR_UNSUPPORTED
+    w = _ffn(n_sets=2)
+    w.w_down[1] = None
+    assert f(ctypes.byref(b), FAKE, FAKE, FAKE, ctypes.byref(w), FAKE, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), None, FAKE, FAKE, ctypes.byref(_ffn()), FAKE, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), FAKE, FAKE, None, ctypes.byref(_ffn()), FAKE, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+
+
+def test_scatter_and_block_validation():
+    b = _batch()
+    assert ce.lib.ce_scatter_residual(ctypes.byref(b), FAKE, FAKE, FAKE, ce.CE_BF16, 72, FAKE, FAKE, None) == ce.CE_ERR_UNSUPPORTED
+    assert ce.lib.ce_scatter_residual(ctypes.byref(b), FAKE, FAKE, None, ce.CE_BF16, 256, FAKE, FAKE, None) == ce.CE_ERR_INVALID_ARG
+    fb = ce.lib.ce_routed_block
+    need = ce.lib.ce_workspace_size(ce.CE_WS_BLOCK, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    sw, fw = _scorer(), _ffn()
+    assert fb(ctypes.byref(b), FAKE, FAKE, ctypes.byref(sw), ctypes.byref(fw), None, None, None, FAKE, need - 256, None) == ce.CE_ERR_WORKSPACE
+    assert fb(ctypes.byref(b), FAKE, FAKE, ctypes.byref(_scorer(d=512)), ctypes.byref(fw), None, None, None, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    assert fb(ctypes.byref(b), FAKE, FAKE, ctypes.byref(_scorer(dtype=ce.CE_F32)), ctypes.byref(fw), None, None, None, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+    assert fb(ctypes.byref(b), None, FAKE, ctypes.byref(sw), ctypes.byref(fw), None, None, None, FAKE, need, None) == ce.CE_ERR_INVALID_ARG
+
+
+def test_workspace_sizes_grow_with_capacity():
+    small = _batch(cap=10)
+    big = _batch(cap=1000)
+    for which in (ce.CE_WS_FFN, ce.CE_WS_BLOCK):
+        a = ce.lib.ce_workspace_size(which, ctypes.byref(small), 256, 512, ce.CE_BF16)
+        c = ce.lib.ce_workspace_size(which, ctypes.byref(big), 256, 512, ce.CE_BF16)
+        assert c - a >= 990 * 512 * 2
+    assert ce.lib.ce_workspace_size(9, ctypes.byref(small), 256, 512, ce.CE_BF16) == 0
+    assert ce.lib.ce_workspace_size(ce.CE_WS_BLOCK, ctypes.byref(small), 256, 512, 3) == 0
+
+
+def test_host_logic_under_sanitizers(tmp_path):
+    """Host-only build of the validation / keep-count code with ASan + UBSan (g++, no HIP)."""
+    src = os.path.join(ROOT, "paper_2608_29291_amd", "csrc", "ce_host.cpp")
+    drv = tmp_path / "drv.c"
+    drv.write_text(r'''
+#include <stdio.h>
+#include <stdint.h>
+#include "ce_router.h"
+int main(void) {
+  int32_t offs[4] = {0, 3, 3, 10};
+  uint8_t flags[10] = {2, 0, 0, 0, 2, 0, 0, 0, 0, 0};
+  int64_t kt = ce_kept_count_host(3, 10, offs, flags, 0.5f);
+  int ok = (kt == 1 + 1 + 0 + 1 + 3) && ce_num_keep(0.35f, 729) == 256 && ce_num_keep(1.0f, 5) == 5
+           && ce_num_keep(0.0f, 5) == 0 && ce_num_keep(1e-30f, 2147483647) == 1
+           && ce_num_keep(2.0f, 5) == -1;
+  ce_batch b = {2, 100, (const int32_t*)16, (const uint8_t*)16, 0, 0.5f, 50};
+  size_t a = ce_workspace_size(CE_WS_BLOCK, &b, 256, 512, CE_BF16);
+  ok = ok && a > 50 * 512 * 2 && (a % 256) == 0;
+  printf("%s %lld %zu\n", ok ? "OK" : "FAIL", (long long)kt, a);
+  return ok ? 0 : 1;
+}
+''')
+    exe = tmp_path / "drv"
+    cmd_cpp = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+               f"-I{os.path.join(ROOT, 'include')}", "-c", src, "-o", str(tmp_path / "host.o")]
+    cmd_c = ["gcc", "-O1", "-g", "-fsanitize=address,undefined", f"-I{os.path.join(ROOT, 'include')}",
+             "-c", str(drv), "-o", str(tmp_path / "drv.o")]
+    cmd_ld = ["g++", "-fsanitize=address,undefined", str(tmp_path / "host.o"), str(tmp_path / "drv.o"),
+              "-o", str(exe)]
+    for cmd in (cmd_cpp, cmd_c, cmd_ld):
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0 and r.stdout.startswith("OK"), r.stdout + r.stderr

@@ -1,0 +1,352 @@
+"""GPU parity of every C-ABI entry point against the oracle, on small seeded
+workloads that span several tiles with ragged tails, and on edge cases.
+
+Bars (written here, derived in the design notes):
+  logits        max|dl| / max(max|l|, 1) <= 1e-5 (fp32) / 1e-4 (bf16)
+  selection     bit-exact kept_idx / kept_offsets / token_pos when fed the oracle's logits
+  FFN / block   max|dY| / max|Y| over retained rows <= 1e-5 (fp32) / 2e-2 (bf16),
+                against the oracle run on the GPU's own selection
+  bypass        dropped rows bitwise equal to the input
+"""
+import numpy as np
+import pytest
+
+import oracle
+from ce_workloads import TOK_GEN, TOK_KEEP, bf16_bits, bf16_to_f32, make_workload, small_workload
+
+pytestmark = pytest.mark.gpu
+
+KINDS = ["und", "gen", "mixed", "mot", "interleaved"]
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import gpu_util
+    return gpu_util
+
+
+def wl_for(kind, dtype, seed=0, **kw):
+    if dtype == "f32":
+        kw.setdefault("d", 128)
+        kw.setdefault("F", 192)
+    return small_workload(kind, seed=seed, dtype=dtype, **kw)
+
+
+# ---------------------------------------------------------------- ce_score
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", KINDS)
+def test_score(G, kind, dtype):
+    import torch
+    wl = wl_for(kind, dtype, seed=1)
+    dw = G.DevWorkload(wl)
+    logits = torch.full((wl.T,), float("nan"), device="cuda")
+    probs = torch.full((wl.T,), float("nan"), device="cuda")
+    import paper_2608_29291_amd as ce
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits, probs)
+    torch.cuda.synchronize()
+    l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    err = G.logit_err(G.host(logits), l64)
+    print(f"[score {kind} {dtype}] rel err {err:.3e}")
+    assert err <= G.LOGIT_TOL[dtype]
+    p = G.host(probs)
+    pref = oracle.sigmoid(l64)
+    assert np.max(np.abs(p - pref)) <= 1e-5
+
+
+@pytest.mark.parametrize("rank", [(32, 0), (64, 64), (256, 256), (32, 480)])
+def test_score_rank_shapes(G, rank):
+    import torch
+    import paper_2608_29291_amd as ce
+    r_c, r_e = rank
+    wl = make_workload("ranks", [[(100, TOK_GEN), (40, 0), (5, TOK_KEEP)], [(70, 0)]], d=192, F=64,
+                       r_c=r_c, r_e=max(r_e, 32), keep=0.5, dtype="bf16", seed=3, biases=True)
+    if r_e == 0:
+        # no expansion scorer: generation tokens use the core only
+        wl.scorer.w1_exp = wl.scorer.w1_exp[:, :0]
+        wl.scorer.w2_exp = wl.scorer.w2_exp[:, :0]
+        wl.scorer.b1_exp = wl.scorer.b1_exp[:, :0]
+        wl.scorer.b2_exp = np.zeros_like(wl.scorer.b2_exp)
+    dw = G.DevWorkload(wl)
+    if r_e == 0:
+        dw.scorer.b2_exp = None
+    logits = torch.empty(wl.T, device="cuda")
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits)
+    torch.cuda.synchronize()
+    l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    assert G.logit_err(G.host(logits), l64) <= 1e-4
+
+
+def test_score_segments_follow_t(G):
+    """Every segment boundary of t picks the right expansion."""
+    import torch
+    import paper_2608_29291_amd as ce
+    ts = [0.0, 0.2499, 0.25, 0.4999, 0.5, 0.74, 0.75, 1.0]
+    wl = make_workload("seg", [[(70, TOK_GEN)]] * len(ts), d=128, F=64, r_c=32, r_e=32, keep=0.5,
+                       dtype="bf16", seed=5, t_values=ts, biases=True)
+    dw = G.DevWorkload(wl)
+    logits = torch.empty(wl.T, device="cuda")
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits)
+    torch.cuda.synchronize()
+    l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    assert G.logit_err(G.host(logits), l64) <= 1e-4
+
+
+# ---------------------------------------------------------------- ce_topk_compact
+def run_topk(G, wl, logits32, compact=False, cap=None):
+    import torch
+    import paper_2608_29291_amd as ce
+    dw = G.DevWorkload(wl, kept_capacity=cap)
+    kept_idx, kept_off = dw.new_idx()
+    token_pos = torch.full((max(wl.T, 1),), -9, dtype=torch.int32, device="cuda")
+    ws = dw.ws(ce.CE_WS_TOPK)
+    lg = G.to_dev(np.asarray(logits32, np.float32)) if wl.T else torch.empty(1, device="cuda")
+    comp = None
+    if compact:
+        comp = torch.zeros((max(dw.cap, 1), wl.d), dtype=G.tdtype(wl), device="cuda")
+    ce.ce_topk_compact(dw.batch, lg, kept_idx, kept_off, ws, token_pos=token_pos,
+                       hidden=dw.hidden if compact else None, compact=comp)
+    torch.cuda.synchronize()
+    st = ce.ce_workspace_status(ws)
+    return dw, G.host(kept_idx), G.host(kept_off), G.host(token_pos), comp, st
+
+
+def check_topk_exact(G, wl, logits32):
+    dw, kidx, koff, tpos, _, st = run_topk(G, wl, logits32)
+    ref = oracle.select(logits32, wl.flags, wl.seq_offsets, wl.keep)
+    assert st == 0
+    np.testing.assert_array_equal(koff, ref["kept_offsets"])
+    np.testing.assert_array_equal(kidx[:len(ref["kept_idx"])], ref["kept_idx"])
+    np.testing.assert_array_equal(tpos[:wl.T], ref["token_pos"])
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("keep", [0.0, 0.3, 0.5, 0.77, 1.0])
+def test_topk_given_oracle_logits(G, kind, keep):
+    wl = small_workload(kind, seed=2, dtype="bf16", keep=keep, d=64, F=64, r_c=32, r_e=32)
+    _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    check_topk_exact(G, wl, l32)
+
+
+@pytest.mark.parametrize("mode", ["ints", "zeros", "special", "dup_pairs"])
+@pytest.mark.parametrize("keep", [0.1, 0.5, 0.9])
+def test_topk_ties_and_specials(G, mode, keep):
+    rng = np.random.default_rng(11)
+    wl = small_workload("mixed", seed=4, dtype="bf16", keep=keep, d=64, F=64, r_c=32, r_e=32)
+    T = wl.T
+    if mode == "ints":
+        l32 = rng.integers(-3, 4, size=T).astype(np.float32)
+    elif mode == "zeros":
+        l32 = np.where(rng.random(T) < 0.5, np.float32(0.0), np.float32(-0.0)).astype(np.float32)
+    elif mode == "special":
+        l32 = rng.choice(np.array([0.0, -0.0, 1.0, -1.0, np.inf, -np.inf, np.nan, 1e-45, -1e-45],
+                                  np.float32), size=T)
+    else:
+        l32 = np.repeat(rng.standard_normal((T + 1) // 2).astype(np.float32), 2)[:T]
+    check_topk_exact(G, wl, l32)
+
+
+def test_topk_long_sequence_global_path(G):
+    """A 20000-token sequence (keys do not fit in LDS) and a short one."""
+    wl = make_workload("long", [[(20000, 0), (77, TOK_KEEP)], [(300, 0)]], d=64, F=64, r_c=32,
+                       r_e=32, keep=0.37, dtype="bf16", seed=6)
+    rng = np.random.default_rng(1)
+    l32 = rng.integers(-50, 50, size=wl.T).astype(np.float32)  # many ties
+    check_topk_exact(G, wl, l32)
+
+
+def test_topk_empty_and_all_kept(G):
+    wl = make_workload("empty", [[(0, 0)], [(10, TOK_KEEP)], [(0, 0)], [(5, 0), (3, TOK_KEEP)], [(1, 0)]],
+                       d=64, F=64, r_c=32, r_e=32, keep=0.5, dtype="bf16", seed=7)
+    l32 = np.random.default_rng(2).standard_normal(wl.T).astype(np.float32)
+    check_topk_exact(G, wl, l32)
+
+
+def test_topk_many_sequences(G):
+    lens = np.random.default_rng(3).integers(0, 60, size=300)
+    wl = make_workload("many", [[(int(n), 0), (2, TOK_KEEP)] for n in lens], d=64, F=64, r_c=32,
+                       r_e=32, keep=0.45, dtype="bf16", seed=8)
+    l32 = np.random.default_rng(4).standard_normal(wl.T).astype(np.float32)
+    check_topk_exact(G, wl, l32)
+
+
+def test_topk_gather(G):
+    wl = small_workload("mixed", seed=5, dtype="bf16", d=192, F=64, r_c=32, r_e=32)
+    _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    dw, kidx, koff, _, comp, st = run_topk(G, wl, l32, compact=True)
+    assert st == 0
+    kt = int(koff[-1])
+    np.testing.assert_array_equal(G.host(comp)[:kt], wl.hidden[kidx[:kt]])
+
+
+def test_topk_overflow_is_reported_and_bounded(G):
+    """kept_capacity below Kt: status flag set, nothing written past the capacity."""
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = small_workload("und", seed=6, dtype="bf16", d=64, F=64, r_c=32, r_e=32, keep=0.5)
+    _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    ref = oracle.select(l32, wl.flags, wl.seq_offsets, wl.keep)
+    kt = len(ref["kept_idx"])
+    cap = kt - 37
+    dw = G.DevWorkload(wl, kept_capacity=cap)
+    guard = torch.full((cap + 64,), -5, dtype=torch.int32, device="cuda")
+    kept_off = torch.empty(wl.B + 1, dtype=torch.int32, device="cuda")
+    ws = dw.ws(ce.CE_WS_TOPK)
+    ce.ce_topk_compact(dw.batch, G.to_dev(l32), guard[:cap], kept_off, ws)
+    torch.cuda.synchronize()
+    assert ce.ce_workspace_status(ws) & ce.CE_DEV_OVERFLOW
+    g = G.host(guard)
+    np.testing.assert_array_equal(g[:cap], ref["kept_idx"][:cap])
+    assert np.all(g[cap:] == -5)
+    np.testing.assert_array_equal(G.host(kept_off), ref["kept_offsets"])
+
+
+def test_topk_bad_offsets_are_reported(G):
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = small_workload("und", seed=7, dtype="bf16", d=64, F=64, r_c=32, r_e=32)
+    dw = G.DevWorkload(wl, kept_capacity=wl.T)
+    bad = wl.seq_offsets.copy()
+    bad[1], bad[2] = bad[2], bad[1]  # decreasing
+    dw.batch.seq_offsets = G.to_dev(bad.astype(np.int32))
+    kept_idx = torch.empty(wl.T, dtype=torch.int32, device="cuda")
+    kept_off = torch.empty(wl.B + 1, dtype=torch.int32, device="cuda")
+    ws = dw.ws(ce.CE_WS_TOPK)
+    l32 = np.random.default_rng(0).standard_normal(wl.T).astype(np.float32)
+    ce.ce_topk_compact(dw.batch, G.to_dev(l32), kept_idx, kept_off, ws)
+    torch.cuda.synchronize()
+    assert ce.ce_workspace_status(ws) & ce.CE_DEV_BAD_OFFSETS
+
+
+# ---------------------------------------------------------------- ce_routed_ffn + ce_scatter_residual
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", KINDS)
+def test_staged_ffn_and_scatter(G, kind, dtype):
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = wl_for(kind, dtype, seed=8) if dtype == "f32" else small_workload(kind, seed=8, dtype=dtype,
+                                                                           d=192, F=320)
+    l64, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    dw, kidx, koff, _, comp, st = run_topk(G, wl, l32, compact=True)
+    assert st == 0
+    kt = int(koff[-1])
+    kept_idx_d = G.to_dev(kidx.astype(np.int32))
+    kept_off_d = G.to_dev(koff.astype(np.int32))
+    ffn_out = torch.full_like(comp, float("nan"))
+    ws = dw.ws(ce.CE_WS_FFN)
+    ce.ce_routed_ffn(dw.batch, comp, kept_idx_d, kept_off_d, dw.ffn, ffn_out, ws)
+    torch.cuda.synchronize()
+    f_gpu = G.host(ffn_out)[:kt]
+    rows = kidx[:kt]
+    y_ref = oracle.routed_rows(wl.hidden, wl.flags, rows, wl.ffn) - wl.hidden[rows].astype(np.float64)
+    err = G.rel_err(f_gpu, y_ref)
+    print(f"[ffn {kind} {dtype}] rel err {err:.3e}")
+    assert err <= G.OUT_TOL[dtype]
+
+    # scatter, out of place then in place
+    h_out = torch.full_like(dw.hidden, 7.0)
+    ce.ce_scatter_residual(dw.batch, ffn_out, kept_idx_d, kept_off_d, dw.hidden, h_out)
+    h_in2 = dw.hidden.clone()
+    ce.ce_scatter_residual(dw.batch, ffn_out, kept_idx_d, kept_off_d, h_in2, h_in2)
+    torch.cuda.synchronize()
+    # exact expectation from IEEE definitions: fp32 add, one round to nearest even
+    want = wl.hidden.copy()
+    s = wl.hidden[rows].astype(np.float32) + f_gpu.astype(np.float32)
+    want[rows] = bf16_to_f32(bf16_bits(s)) if dtype == "bf16" else s
+    np.testing.assert_array_equal(G.host(h_out), want)
+    np.testing.assert_array_equal(G.host(h_in2), want)
+
+
+# ---------------------------------------------------------------- ce_routed_block
+def run_block(G, wl, inplace=True, want_logits=True):
+    import torch
+    import paper_2608_29291_amd as ce
+    dw = G.DevWorkload(wl)
+    ws = dw.ws(ce.CE_WS_BLOCK)
+    kept_idx, kept_off = dw.new_idx()
+    logits = torch.empty(max(wl.T, 1), device="cuda")
+    h_in = dw.hidden.clone()
+    h_out = h_in if inplace else torch.full_like(h_in, 3.0)
+    ce.ce_routed_block(dw.batch, h_in, h_out, dw.scorer, dw.ffn, ws,
+                       logits_out=logits if want_logits else None, kept_idx_out=kept_idx,
+                       kept_offsets_out=kept_off)
+    torch.cuda.synchronize()
+    st = ce.ce_workspace_status(ws)
+    return dict(y=G.host(h_out), logits=G.host(logits)[:wl.T], kidx=G.host(kept_idx),
+                koff=G.host(kept_off), status=st)
+
+
+def check_block(G, wl, r):
+    assert r["status"] == 0
+    l64, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    eps = G.logit_err(r["logits"], l64)
+    assert eps <= G.LOGIT_TOL[wl.dtype]
+    # the GPU's top-k of its own logits is exact
+    sel_g = oracle.select(r["logits"].astype(np.float32), wl.flags, wl.seq_offsets, wl.keep)
+    np.testing.assert_array_equal(r["koff"], sel_g["kept_offsets"])
+    kt = int(r["koff"][-1])
+    kept = r["kidx"][:kt]
+    np.testing.assert_array_equal(kept, sel_g["kept_idx"])
+    # and agrees with the oracle's own selection up to near-threshold swaps
+    sel_r = oracle.select(l32, wl.flags, wl.seq_offsets, wl.keep)
+    scale = max(1.0, float(np.max(np.abs(l64[np.isfinite(l64)]))) if np.isfinite(l64).any() else 1.0)
+    swaps = G.selection_swaps_ok(kept, l32, sel_r, wl.flags, wl.seq_offsets, eps * scale + 1e-30)
+    # outputs against the oracle block on the GPU's selection
+    ref = oracle.routed_block(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.keep, wl.scorer, wl.ffn,
+                              kept_override=kept)
+    err = G.rel_err(r["y"][kept], ref["y"][kept])
+    dropped = np.ones(wl.T, bool)
+    dropped[kept] = False
+    np.testing.assert_array_equal(r["y"][dropped], wl.hidden[dropped])
+    assert err <= G.OUT_TOL[wl.dtype], err
+    return err, swaps
+
+
+@pytest.mark.parametrize("inplace", [True, False])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind", KINDS)
+def test_block(G, kind, dtype, inplace):
+    wl = wl_for(kind, dtype, seed=9) if dtype == "f32" else small_workload(kind, seed=9, dtype=dtype,
+                                                                           d=192, F=320)
+    r = run_block(G, wl, inplace=inplace)
+    err, swaps = check_block(G, wl, r)
+    print(f"[block {kind} {dtype} inplace={inplace}] rel err {err:.3e} swaps {swaps}")
+
+
+def test_block_keep_one_is_dense(G):
+    wl = small_workload("mot", seed=10, dtype="bf16", keep=1.0)
+    wl.flags = (wl.flags & ~np.uint8(TOK_KEEP)).astype(np.uint8)
+    r = run_block(G, wl)
+    yd = oracle.dense_block(wl.hidden, wl.flags, wl.ffn)
+    assert G.rel_err(r["y"], yd) <= 2e-2
+    assert int(r["koff"][-1]) == wl.T
+
+
+def test_block_keep_zero_touches_only_kept(G):
+    wl = small_workload("und", seed=11, dtype="bf16", keep=0.0)
+    r = run_block(G, wl)
+    keep_rows = np.nonzero(wl.flags & TOK_KEEP)[0]
+    np.testing.assert_array_equal(r["kidx"][:int(r["koff"][-1])], keep_rows)
+    check_block(G, wl, r)
+
+
+def test_block_deterministic(G):
+    wl = small_workload("mot", seed=12, dtype="bf16", d=256, F=512)
+    a = run_block(G, wl)
+    b = run_block(G, wl)
+    for k in ("y", "logits", "kidx", "koff"):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_block_without_optional_outputs(G):
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = small_workload("gen", seed=13, dtype="bf16")
+    dw = G.DevWorkload(wl)
+    ws = dw.ws(ce.CE_WS_BLOCK)
+    h = dw.hidden.clone()
+    ce.ce_routed_block(dw.batch, h, h, dw.scorer, dw.ffn, ws)
+    torch.cuda.synchronize()
+    full = run_block(G, wl)
+    np.testing.assert_array_equal(G.host(h), full["y"])
