@@ -62,7 +62,7 @@ def load_traffic():
     return t.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, n_seq: int, min_seconds: float = 10.0, max_reps: int = 10):
+def cpu_baseline(wl, n_seq: int, min_seconds: float = 10.0, max_reps: int = 50):
     """The oracle (float64 NumPy) on the first n_seq sequences, repeated until
     about min_seconds of CPU work; reports tokens per second over all runs."""
     import oracle

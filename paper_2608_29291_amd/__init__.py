@@ -46,6 +46,11 @@ if not os.path.exists(LIB_PATH):
         f"{LIB_PATH} is missing: build it first with `python paper_2608_29291_amd/build.py` "
         "(hipcc, gfx950). There is no fallback path.")
 
+# torch ships its own libamdhip64 (soname libamdhip64.so.7). Loading torch
+# first makes this library bind to that same HIP runtime; loading it first
+# would pull in a second runtime that cannot see torch's allocations.
+import torch  # noqa: E402,F401
+
 lib = ctypes.CDLL(LIB_PATH)
 
 _p = ctypes.c_void_p

@@ -244,6 +244,25 @@ def test_staged_ffn_and_scatter(G, kind, dtype):
     print(f"[ffn {kind} {dtype}] rel err {err:.3e}")
     assert err <= G.OUT_TOL[dtype]
 
+    # the same FFN in two launches: act is the SwiGLU intermediate z, then W_down z
+    act = torch.full((max(dw.cap, 1), wl.d_ff), float("nan"), dtype=G.tdtype(wl), device="cuda")
+    out2 = torch.full_like(comp, float("nan"))
+    ce.ce_ffn_gateup(dw.batch, comp, kept_idx_d, kept_off_d, dw.ffn, act, ws)
+    ce.ce_ffn_down(dw.batch, act, kept_idx_d, kept_off_d, dw.ffn, out2, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(G.host(out2)[:kt], f_gpu)
+    x = wl.hidden[rows].astype(np.float64)
+    z_ref = np.empty((kt, wl.d_ff))
+    sets = (wl.flags[rows] & TOK_GEN) if len(wl.ffn) > 1 else np.zeros(kt, int)
+    for si, w in enumerate(wl.ffn):
+        sel = np.nonzero(sets == si)[0]
+        g = x[sel] @ w.w_gate.astype(np.float64).T
+        u = x[sel] @ w.w_up.astype(np.float64).T
+        z_ref[sel] = oracle.silu(g) * u
+    zerr = G.rel_err(G.host(act)[:kt], z_ref)
+    print(f"[gateup {kind} {dtype}] rel err {zerr:.3e}")
+    assert zerr <= G.OUT_TOL[dtype]
+
     # scatter, out of place then in place
     h_out = torch.full_like(dw.hidden, 7.0)
     ce.ce_scatter_residual(dw.batch, ffn_out, kept_idx_d, kept_off_d, dw.hidden, h_out)
