@@ -2,15 +2,23 @@
 // epilogue, and the down GEMM with an optional residual-scatter epilogue.
 //
 // Both are "weights x tokens" GEMMs on MFMA (bf16 32x32x16 with fp32
-// accumulation, or fp32 32x32x2 for fp32 data), staged through a double-buffered,
-// XOR-swizzled LDS tile with one barrier per 128-byte K step.
+// accumulation, or fp32 32x32x2 for fp32 data). A workgroup of 4 waves (2 x 2)
+// owns a kWR x kTR tile (weight rows x token rows); each wave owns a
+// (kWR/2) x (kTR/2) sub-tile of 32x32 MFMA blocks. K is streamed in 128-byte
+// steps through an XOR-swizzled LDS tile, double-buffered (one barrier per
+// step) or single-buffered with a register prefetch (two barriers per step).
 //
 // Row mapping: GEMM row j (packed order, grouped by FFN set for MoT) maps to a
 // source row through up to two index arrays: r = map2[map1[j]] (each level is
 // skipped when its pointer is NULL). This lets the same kernel read rows
-// straight out of the full hidden-state matrix (the gather fused into the A
-// loads) or out of a packed buffer, and write results straight back to the
-// token rows (the scatter fused into the epilogue).
+// straight out of the full hidden-state matrix (the gather fused into the
+// token loads) or out of a packed buffer, and write results straight back to
+// the token rows (the scatter fused into the epilogue).
+//
+// Tile order is XCD-aware: the hardware hands workgroup L to XCD L % 8, so the
+// linear id is remapped to give each XCD a contiguous range of tiles, ordered
+// feature-tile major; the weight tile a CU loads is then mostly shared with
+// the other CUs of its XCD through that XCD's L2.
 //
 // The number of packed rows Kt and the size n0 of the first MoT group live in
 // device memory; the grid is sized from the host-known capacity and tiles past
@@ -27,15 +35,15 @@ __device__ __forceinline__ int map_row(int j, const int32_t* m1, const int32_t* 
   return m2 ? m2[r] : r;
 }
 
+constexpr int kXcds = 8;
+
 // kMode 0: gate/up + SwiGLU -> out[orow(j)][f]
 // kMode 1: down (+ residual) -> out[orow(j)][f]
-template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT>
-__global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
+template <bool kBF16, int kMode, int kWR, int kTR, int kStages>
+__global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a, int n_tt, int n_ft) {
   constexpr int kElem = kBF16 ? 2 : 4;
-  constexpr int kWaves = kWW * kWT;
-  static_assert(kWaves == 4, "4 waves per workgroup");
-  constexpr int kWRw = kWR / kWW;  // weight rows per wave
-  constexpr int kTRw = kTR / kWT;  // token rows per wave
+  constexpr int kWRw = kWR / 2;  // weight rows per wave
+  constexpr int kTRw = kTR / 2;  // token rows per wave
   constexpr int kMW = kWRw / 32;
   constexpr int kMT = kTRw / 32;
   static_assert(kMode == 1 || (kMW % 2) == 0, "gate/up blocks come in pairs");
@@ -43,13 +51,21 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
   constexpr int kTLoads = kTR * kChunks / 256;
   constexpr int kStage = (kWR + kTR) * kKB;
 
-  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int ww = wave % kWW;
-  const int wt = wave / kWW;
+  const int ww = wave & 1;
+  const int wt = wave >> 1;
+
+  // ---- XCD-aware tile order ----
+  const int total = n_tt * n_ft;
+  const int per = (total + kXcds - 1) / kXcds;
+  const int w = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
+  if (w >= total) return;
+  const int ft = w / n_tt;
+  const int tt = w - ft * n_tt;
 
   // ---- which packed rows this tile covers (grouped by weight set) ----
   int kt = *a.kt_ptr;
@@ -61,69 +77,76 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
   }
   const int tiles0 = (n0 + kTR - 1) / kTR;
   int set, row_lo, row_hi;
-  if ((int)blockIdx.x < tiles0) {
+  if (tt < tiles0) {
     set = 0;
-    row_lo = blockIdx.x * kTR;
+    row_lo = tt * kTR;
     row_hi = min(row_lo + kTR, n0);
   } else {
     set = 1;
-    row_lo = n0 + (blockIdx.x - tiles0) * kTR;
+    row_lo = n0 + (tt - tiles0) * kTR;
     row_hi = min(row_lo + kTR, kt);
   }
   if (row_lo >= row_hi) return;
 
   const int n_feat = a.n_feat;
-  const int f_tile = (kMode == 0) ? kWR / 2 : kWR;
-  const int f0 = blockIdx.y * f_tile;
+  constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
+  const int f0 = ft * kFTile;
 
-  // ---- per-thread source row pointers (fixed over the K loop) ----
+  // ---- per-thread source rows (fixed over the K loop) ----
   const int cchunk = tid & 7;
-  const char* wsrc[kWLoads];
-#pragma unroll
-  for (int i = 0; i < kWLoads; ++i) {
-    const int r = i * 32 + (tid >> 3);
-    int feat;
-    const char* base;
-    if constexpr (kMode == 0) {
-      const int blk = r >> 5;
-      feat = f0 + 32 * (blk >> 1) + (r & 31);
-      base = (blk & 1) ? a.w1[set] : a.w0[set];
-    } else {
-      feat = f0 + r;
-      base = a.w0[set];
-    }
-    wsrc[i] = (feat < n_feat) ? base + (int64_t)feat * a.w_ld + cchunk * 16 : nullptr;
+  const int rsub = tid >> 3;  // 0..31
+  // weight row of load i: block i of the tile, row rsub inside it
+  const char* wbase0;
+  const char* wbase1;
+  int wfeat0;
+  if constexpr (kMode == 0) {
+    // tile blocks alternate gate (even) / up (odd) for features f0 + 32*(i/2) + rsub
+    wbase0 = a.w0[set];
+    wbase1 = a.w1[set];
+    wfeat0 = f0 + rsub;
+  } else {
+    wbase0 = a.w0[set];
+    wbase1 = a.w0[set];
+    wfeat0 = f0 + rsub;
   }
   const char* tsrc[kTLoads];
 #pragma unroll
   for (int i = 0; i < kTLoads; ++i) {
-    const int r = i * 32 + (tid >> 3);
-    const int j = row_lo + r;
+    const int j = row_lo + i * 32 + rsub;
     tsrc[i] = (j < row_hi) ? a.tok + (int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + cchunk * 16
                            : nullptr;
   }
 
   u32x4_t wreg[kWLoads], treg[kTLoads];
   auto gload = [&](int kb) {
-    const int koff = kb * kKB;
+    const int koff = kb * kKB + cchunk * 16;
 #pragma unroll
     for (int i = 0; i < kWLoads; ++i) {
-      if (wsrc[i]) wreg[i] = gload16_cached(wsrc[i] + koff);
+      int feat;
+      const char* base;
+      if constexpr (kMode == 0) {
+        feat = wfeat0 + 32 * (i >> 1);
+        base = (i & 1) ? wbase1 : wbase0;
+      } else {
+        feat = wfeat0 + 32 * i;
+        base = wbase0;
+      }
+      if (feat < n_feat) wreg[i] = gload16_cached(base + (int64_t)feat * a.w_ld + koff);
       else wreg[i] = u32x4_t{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int i = 0; i < kTLoads; ++i) {
-      if (tsrc[i]) treg[i] = gload16_cached(tsrc[i] + koff);
+      if (tsrc[i]) treg[i] = gload16_cached(tsrc[i] + kb * kKB);
       else treg[i] = u32x4_t{0u, 0u, 0u, 0u};
     }
   };
   auto lstore = [&](int buf) {
     char* s = smem + buf * kStage;
 #pragma unroll
-    for (int i = 0; i < kWLoads; ++i) lds_write16(s, lds_chunk_off(i * 32 + (tid >> 3), cchunk), wreg[i]);
+    for (int i = 0; i < kWLoads; ++i) lds_write16(s, lds_chunk_off(i * 32 + rsub, cchunk), wreg[i]);
 #pragma unroll
     for (int i = 0; i < kTLoads; ++i)
-      lds_write16(s + kWR * kKB, lds_chunk_off(i * 32 + (tid >> 3), cchunk), treg[i]);
+      lds_write16(s + kWR * kKB, lds_chunk_off(i * 32 + rsub, cchunk), treg[i]);
   };
 
   f32x16_t acc[kMW][kMT];
@@ -132,18 +155,11 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
 #pragma unroll
     for (int j = 0; j < kMT; ++j) acc[i][j] = f32x16_t{};
 
-  const int nk = a.k_bytes / kKB;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-
   const int lrow = lane & 31;
   const int lhalf = lane >> 5;
-  for (int kb = 0; kb < nk; ++kb) {
-    if (kb + 1 < nk) gload(kb + 1);
-    const char* s = smem + (kb & 1) * kStage;
-    const char* sw = s;
-    const char* st = s + kWR * kKB;
+  auto compute = [&](int buf) {
+    const char* sw = smem + buf * kStage;
+    const char* st = sw + kWR * kKB;
 #pragma unroll
     for (int step = 0; step < 4; ++step) {
       const int c = 2 * step + lhalf;
@@ -157,8 +173,29 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
 #pragma unroll
         for (int j = 0; j < kMT; ++j) mfma_step<kBF16>(acc[i][j], fa[i], fb[j]);
     }
-    if (kb + 1 < nk) lstore((kb + 1) & 1);
-    __syncthreads();
+  };
+
+  const int nk = a.k_bytes / kKB;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  if constexpr (kStages == 2) {
+    for (int kb = 0; kb < nk; ++kb) {
+      if (kb + 1 < nk) gload(kb + 1);
+      compute(kb & 1);
+      if (kb + 1 < nk) lstore((kb + 1) & 1);
+      __syncthreads();
+    }
+  } else {
+    for (int kb = 0; kb < nk; ++kb) {
+      if (kb + 1 < nk) gload(kb + 1);
+      compute(0);
+      __syncthreads();
+      if (kb + 1 < nk) {
+        lstore(0);
+        __syncthreads();
+      }
+    }
   }
 
   // ---- epilogue ----
@@ -166,8 +203,9 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
   for (int j = 0; j < kMT; ++j) {
     const int jr = row_lo + wt * kTRw + 32 * j + lrow;
     if (jr >= row_hi) continue;
+    const int orow_idx = map_row(jr, a.omap1, a.omap2);
+    char* orow = a.out + (int64_t)orow_idx * a.out_ld;
     if constexpr (kMode == 0) {
-      char* orow = a.out + (int64_t)map_row(jr, a.omap1, a.omap2) * a.out_ld;
 #pragma unroll
       for (int p = 0; p < kMW / 2; ++p) {
         const int fb = f0 + 32 * (ww * (kMW / 2) + p) + 4 * lhalf;
@@ -184,8 +222,6 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
         }
       }
     } else {
-      const int orow_idx = map_row(jr, a.omap1, a.omap2);
-      char* orow = a.out + (int64_t)orow_idx * a.out_ld;
       const char* rrow = a.res ? a.res + (int64_t)orow_idx * a.res_ld : nullptr;
 #pragma unroll
       for (int i = 0; i < kMW; ++i) {
@@ -207,27 +243,39 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a) {
   }
 }
 
-template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT>
-hipError_t launch_one(const FfnGemmArgs& a, hipStream_t stream) {
-  const int f_tile = (kMode == 0) ? kWR / 2 : kWR;
-  const int tiles_x = (a.cap + kTR - 1) / kTR + (a.n_sets - 1);
-  const int tiles_y = (a.n_feat + f_tile - 1) / f_tile;
-  if (tiles_x <= 0 || tiles_y <= 0) return hipSuccess;
-  dim3 grid(tiles_x, tiles_y);
-  hipLaunchKernelGGL((ffn_gemm_kernel<kBF16, kMode, kWR, kTR, kWW, kWT>), grid, dim3(256), 0, stream, a);
+template <bool kBF16, int kMode, int kWR, int kTR, int kStages>
+hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
+  constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
+  const int n_tt = (a.cap + kTR - 1) / kTR + (a.n_sets - 1);
+  const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
+  if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
+  const int total = n_tt * n_ft;
+  const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
+  hipLaunchKernelGGL((ffn_gemm_kernel<kBF16, kMode, kWR, kTR, kStages>), dim3(grid), dim3(256), 0,
+                     stream, a, n_tt, n_ft);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// Tile shapes (weight rows x token rows, LDS stages):
+//   gate/up: 256 x 256, 2 stages (128 output features x 256 tokens per workgroup)
+//   down:    256 x 128, 2 stages (more, smaller tiles: d is only 1536-3584 wide)
+// fp32 data (tiny workloads) uses 128 x 128 tiles.
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
-  if (bf16) return launch_one<true, 0, 128, 128, 2, 2>(a, stream);
-  return launch_one<false, 0, 128, 128, 2, 2>(a, stream);
+#ifdef CE_FFN_GATEUP_CFG
+  return CE_FFN_GATEUP_CFG(a, bf16, stream);
+#endif
+  if (bf16) return launch_cfg<true, 0, 256, 256, 2>(a, stream);
+  return launch_cfg<false, 0, 128, 128, 2>(a, stream);
 }
 
 hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
-  if (bf16) return launch_one<true, 1, 128, 128, 2, 2>(a, stream);
-  return launch_one<false, 1, 128, 128, 2, 2>(a, stream);
+#ifdef CE_FFN_DOWN_CFG
+  return CE_FFN_DOWN_CFG(a, bf16, stream);
+#endif
+  if (bf16) return launch_cfg<true, 1, 256, 128, 2>(a, stream);
+  return launch_cfg<false, 1, 128, 128, 2>(a, stream);
 }
 
 }  // namespace ce
