@@ -2,8 +2,8 @@
 //
 // Tiles are staged through LDS in 16-byte chunks: one tile row holds
 // KB = 128 bytes of the contraction dimension (64 bf16 or 32 fp32 values) as
-// 8 chunks, stored at chunk slot (c ^ (row & 7)) so that the 16-byte MFMA
-// fragment reads of 8 consecutive rows hit distinct LDS banks.
+// 8 chunks, stored at an XOR-swizzled chunk slot (lds_chunk_off) so that the
+// 16-byte MFMA fragment reads of consecutive rows hit distinct LDS banks.
 //
 // MFMA operand convention used everywhere: the "A" operand (output rows) is a
 // weight matrix row block (features / scorer ranks), the "B" operand (output
@@ -46,8 +46,12 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
 __device__ __forceinline__ float silu_f32(float x) { return x / (1.0f + __expf(-x)); }
 
 // LDS byte offset of chunk c of tile row r (XOR swizzle over 8 chunks).
+// The XOR key (r ^ r>>3) & 7 differs for any 8 consecutive rows and also for
+// the 8 even (or 8 odd) rows of any 16 consecutive rows, so a 16-byte
+// fragment read of 8 or of 16 consecutive rows touches distinct banks whether
+// the LDS serves 128 or 256 bytes per clock.
 __device__ __forceinline__ int lds_chunk_off(int r, int c) {
-  return (r * kChunks + (c ^ (r & 7))) * 16;
+  return (r * kChunks + (c ^ ((r ^ (r >> 3)) & 7))) * 16;
 }
 
 // One 32-byte K step on a 32x32 block. `a` and `b` are this lane's 16-byte

@@ -2,11 +2,13 @@
 // epilogue, and the down GEMM with an optional residual-scatter epilogue.
 //
 // Both are "weights x tokens" GEMMs on MFMA (bf16 32x32x16 with fp32
-// accumulation, or fp32 32x32x2 for fp32 data). A workgroup of 4 waves (2 x 2)
+// accumulation, or fp32 32x32x2 for fp32 data). A workgroup of kWW x kWT waves
 // owns a kWR x kTR tile (weight rows x token rows); each wave owns a
-// (kWR/2) x (kTR/2) sub-tile of 32x32 MFMA blocks. K is streamed in 128-byte
-// steps through an XOR-swizzled LDS tile, double-buffered (one barrier per
-// step) or single-buffered with a register prefetch (two barriers per step).
+// (kWR/kWW) x (kTR/kWT) sub-tile of 32x32 MFMA blocks. K is streamed in
+// 128-byte steps through an XOR-swizzled LDS tile, double-buffered (one
+// barrier per step) or single-buffered with a register prefetch (two barriers
+// per step). With 8 waves, two waves share each SIMD, so one wave's MFMAs run
+// while the other waits on LDS.
 //
 // Row mapping: GEMM row j (packed order, grouped by FFN set for MoT) maps to a
 // source row through up to two index arrays: r = map2[map1[j]] (each level is
@@ -39,16 +41,21 @@ constexpr int kXcds = 8;
 
 // kMode 0: gate/up + SwiGLU -> out[orow(j)][f]
 // kMode 1: down (+ residual) -> out[orow(j)][f]
-template <bool kBF16, int kMode, int kWR, int kTR, int kStages>
-__global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a, int n_tt, int n_ft) {
+// kWW x kWT waves; each wave owns (kWR/kWW) x (kTR/kWT).
+template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT, int kStages>
+__global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a, int n_tt, int n_ft) {
+  constexpr int kThreads = 64 * kWW * kWT;
   constexpr int kElem = kBF16 ? 2 : 4;
-  constexpr int kWRw = kWR / 2;  // weight rows per wave
-  constexpr int kTRw = kTR / 2;  // token rows per wave
+  constexpr int kWRw = kWR / kWW;  // weight rows per wave
+  constexpr int kTRw = kTR / kWT;  // token rows per wave
   constexpr int kMW = kWRw / 32;
   constexpr int kMT = kTRw / 32;
   static_assert(kMode == 1 || (kMW % 2) == 0, "gate/up blocks come in pairs");
-  constexpr int kWLoads = kWR * kChunks / 256;
-  constexpr int kTLoads = kTR * kChunks / 256;
+  constexpr int kRowsPerPass = kThreads / kChunks;  // tile rows loaded per pass
+  constexpr int kWLoads = kWR / kRowsPerPass;
+  constexpr int kTLoads = kTR / kRowsPerPass;
+  static_assert(kWLoads * kRowsPerPass == kWR && kTLoads * kRowsPerPass == kTR, "tile / threads");
+  static_assert(kMode == 1 || (kRowsPerPass % 32) == 0 || (32 % kRowsPerPass) == 0, "pass rows");
   constexpr int kStage = (kWR + kTR) * kKB;
 
   __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
@@ -56,8 +63,8 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a, int n_tt, 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int ww = wave & 1;
-  const int wt = wave >> 1;
+  const int ww = wave % kWW;
+  const int wt = wave / kWW;
 
   // ---- XCD-aware tile order ----
   const int total = n_tt * n_ft;
@@ -93,60 +100,52 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a, int n_tt, 
   const int f0 = ft * kFTile;
 
   // ---- per-thread source rows (fixed over the K loop) ----
+  // Rows outside the tile (features >= n_feat, packed rows >= row_hi) are read
+  // from a clamped, valid row instead of being predicated: their products only
+  // reach outputs the epilogue never stores, and the loads stay branch-free.
   const int cchunk = tid & 7;
-  const int rsub = tid >> 3;  // 0..31
-  // weight row of load i: block i of the tile, row rsub inside it
-  const char* wbase0;
-  const char* wbase1;
-  int wfeat0;
-  if constexpr (kMode == 0) {
-    // tile blocks alternate gate (even) / up (odd) for features f0 + 32*(i/2) + rsub
-    wbase0 = a.w0[set];
-    wbase1 = a.w1[set];
-    wfeat0 = f0 + rsub;
-  } else {
-    wbase0 = a.w0[set];
-    wbase1 = a.w0[set];
-    wfeat0 = f0 + rsub;
+  const int rsub = tid >> 3;  // 0 .. kRowsPerPass-1
+  const char* wsrc[kWLoads];
+#pragma unroll
+  for (int i = 0; i < kWLoads; ++i) {
+    const int r = i * kRowsPerPass + rsub;  // tile row
+    int feat;
+    const char* base;
+    if constexpr (kMode == 0) {
+      const int blk = r >> 5;  // even blocks: gate rows, odd blocks: up rows
+      feat = f0 + 32 * (blk >> 1) + (r & 31);
+      base = (blk & 1) ? a.w1[set] : a.w0[set];
+    } else {
+      feat = f0 + r;
+      base = a.w0[set];
+    }
+    feat = feat < n_feat ? feat : n_feat - 1;
+    wsrc[i] = base + (int64_t)feat * a.w_ld + cchunk * 16;
   }
   const char* tsrc[kTLoads];
 #pragma unroll
   for (int i = 0; i < kTLoads; ++i) {
-    const int j = row_lo + i * 32 + rsub;
-    tsrc[i] = (j < row_hi) ? a.tok + (int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + cchunk * 16
-                           : nullptr;
+    int j = row_lo + i * kRowsPerPass + rsub;
+    j = j < row_hi ? j : row_hi - 1;
+    tsrc[i] = a.tok + (int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + cchunk * 16;
   }
 
   u32x4_t wreg[kWLoads], treg[kTLoads];
   auto gload = [&](int kb) {
-    const int koff = kb * kKB + cchunk * 16;
+    const int koff = kb * kKB;
 #pragma unroll
-    for (int i = 0; i < kWLoads; ++i) {
-      int feat;
-      const char* base;
-      if constexpr (kMode == 0) {
-        feat = wfeat0 + 32 * (i >> 1);
-        base = (i & 1) ? wbase1 : wbase0;
-      } else {
-        feat = wfeat0 + 32 * i;
-        base = wbase0;
-      }
-      if (feat < n_feat) wreg[i] = gload16_cached(base + (int64_t)feat * a.w_ld + koff);
-      else wreg[i] = u32x4_t{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < kWLoads; ++i) wreg[i] = gload16_cached(wsrc[i] + koff);
 #pragma unroll
-    for (int i = 0; i < kTLoads; ++i) {
-      if (tsrc[i]) treg[i] = gload16_cached(tsrc[i] + kb * kKB);
-      else treg[i] = u32x4_t{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < kTLoads; ++i) treg[i] = gload16_cached(tsrc[i] + koff);
   };
   auto lstore = [&](int buf) {
     char* s = smem + buf * kStage;
 #pragma unroll
-    for (int i = 0; i < kWLoads; ++i) lds_write16(s, lds_chunk_off(i * 32 + rsub, cchunk), wreg[i]);
+    for (int i = 0; i < kWLoads; ++i)
+      lds_write16(s, lds_chunk_off(i * kRowsPerPass + rsub, cchunk), wreg[i]);
 #pragma unroll
     for (int i = 0; i < kTLoads; ++i)
-      lds_write16(s + kWR * kKB, lds_chunk_off(i * 32 + rsub, cchunk), treg[i]);
+      lds_write16(s + kWR * kKB, lds_chunk_off(i * kRowsPerPass + rsub, cchunk), treg[i]);
   };
 
   f32x16_t acc[kMW][kMT];
@@ -243,7 +242,7 @@ __global__ __launch_bounds__(256) void ffn_gemm_kernel(FfnGemmArgs a, int n_tt, 
   }
 }
 
-template <bool kBF16, int kMode, int kWR, int kTR, int kStages>
+template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT, int kStages>
 hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
   constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
   const int n_tt = (a.cap + kTR - 1) / kTR + (a.n_sets - 1);
@@ -251,31 +250,30 @@ hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
   if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
   const int total = n_tt * n_ft;
   const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
-  hipLaunchKernelGGL((ffn_gemm_kernel<kBF16, kMode, kWR, kTR, kStages>), dim3(grid), dim3(256), 0,
-                     stream, a, n_tt, n_ft);
+  hipLaunchKernelGGL((ffn_gemm_kernel<kBF16, kMode, kWR, kTR, kWW, kWT, kStages>), dim3(grid),
+                     dim3(64 * kWW * kWT), 0, stream, a, n_tt, n_ft);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Tile shapes (weight rows x token rows, LDS stages):
-//   gate/up: 256 x 256, 2 stages (128 output features x 256 tokens per workgroup)
-//   down:    256 x 128, 2 stages (more, smaller tiles: d is only 1536-3584 wide)
+// Tile shapes (weight rows x token rows, wave grid, LDS stages), from a sweep
+// on the five named workloads:
+//   gate/up: 256 x 256, 4 x 2 waves, 2 stages (128 output features x 256 tokens)
+//   down:    256 x 128, 4 x 2 waves, 2 stages when d < 3072 (few output tiles);
+//            128 x 128, 2 x 2 waves, 2 stages for the 7B width
 // fp32 data (tiny workloads) uses 128 x 128 tiles.
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
-#ifdef CE_FFN_GATEUP_CFG
-  return CE_FFN_GATEUP_CFG(a, bf16, stream);
-#endif
-  if (bf16) return launch_cfg<true, 0, 256, 256, 2>(a, stream);
-  return launch_cfg<false, 0, 128, 128, 2>(a, stream);
+  if (bf16) return launch_cfg<true, 0, 256, 256, 4, 2, 2>(a, stream);
+  return launch_cfg<false, 0, 128, 128, 2, 2, 2>(a, stream);
 }
 
 hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
-#ifdef CE_FFN_DOWN_CFG
-  return CE_FFN_DOWN_CFG(a, bf16, stream);
-#endif
-  if (bf16) return launch_cfg<true, 1, 256, 128, 2>(a, stream);
-  return launch_cfg<false, 1, 128, 128, 2>(a, stream);
+  if (bf16) {
+    if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2>(a, stream);
+    return launch_cfg<true, 1, 128, 128, 2, 2, 2>(a, stream);
+  }
+  return launch_cfg<false, 1, 128, 128, 2, 2, 2>(a, stream);
 }
 
 }  // namespace ce
