@@ -73,6 +73,7 @@ FfnGemmArgs gateup_args(const ce_ffn_w* w, const ce_batch* b, const char* tok, c
   a.k_bytes = w->d * elem;
   a.tok = tok;
   a.tok_ld = (int64_t)w->d * elem;
+  a.tok_rows = map2 ? b->T : b->kept_capacity;  // hidden rows, or packed rows
   a.map1 = map1;
   a.map2 = map2;
   a.out = act;
@@ -102,6 +103,7 @@ FfnGemmArgs down_args(const ce_ffn_w* w, const ce_batch* b, const char* act, con
   a.k_bytes = w->d_ff * elem;
   a.tok = act;
   a.tok_ld = (int64_t)w->d_ff * elem;
+  a.tok_rows = b->kept_capacity;
   a.map1 = map1;
   a.map2 = nullptr;
   a.out = out;

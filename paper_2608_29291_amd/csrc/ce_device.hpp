@@ -88,6 +88,17 @@ __device__ __forceinline__ u32x4_t gload16_cached(const char* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
 }
 
+// Raw buffer resource over [base, base + bytes): 16-byte loads through it take
+// a per-lane 32-bit offset plus a wave-uniform offset, and return zeros past
+// `bytes` (the hardware range check).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ u32x4_t bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
+}
+
 // Store 4 consecutive output values (fp32 accumulators) as dtype.
 template <bool kBF16>
 __device__ __forceinline__ void store4(char* p, float a, float b, float c, float d) {

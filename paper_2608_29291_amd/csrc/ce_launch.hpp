@@ -18,6 +18,7 @@ struct FfnGemmArgs {
   // tokens: GEMM row j reads row map2[map1[j]] of `tok`
   const char* tok;
   int64_t tok_ld;
+  int64_t tok_rows;  // rows of `tok` (bounds the 32-bit offsets of the large-tile kernel)
   const int32_t* map1;
   const int32_t* map2;
   // output: row omap2[omap1[j]] of `out` (each level skipped when NULL)
