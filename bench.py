@@ -34,7 +34,7 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0
 MALL_BYTES = 256 << 20
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_gateup_showo2_understanding_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_gateup_showo2_understanding_traffic.txt")
 KERNEL_SOURCES = ["paper_2608_29291_amd/csrc/ce_ffn.hip", "paper_2608_29291_amd/csrc/ce_device.hpp"]
 
 
@@ -51,15 +51,20 @@ def kernel_source_hash() -> str:
 
 
 def load_traffic():
-    """HBM bytes per gate/up launch from the committed counter summary, if current."""
+    """HBM bytes per gate/up launch from the committed counter summary, if it
+    was taken on the current kernel source (else None)."""
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
+            kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith(" "))
+    except OSError:
         return None
-    if t.get("kernel_source_hash") != kernel_source_hash():
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return t.get("hbm_bytes_per_launch")
+    try:
+        return int(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(wl, n_seq: int, min_seconds: float = 10.0, max_reps: int = 50):
