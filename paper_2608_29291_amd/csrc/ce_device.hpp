@@ -35,15 +35,23 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
 }
 
-// float32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two float32 -> packed bf16 (low = a), round to nearest even, one
+// v_cvt_pk_bf16_f32; NaN stays NaN.
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ __forceinline__ float silu_f32(float x) { return x / (1.0f + __expf(-x)); }
+// float32 -> bf16 bits (low 16 bits of the result).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) { return pack_bf16(f, 0.0f) & 0xffffu; }
+
+// SiLU(x) = x * sigmoid(x) with the hardware exp2 and reciprocal (about one
+// ulp each): x * rcp(1 + 2^(-x log2 e)).
+__device__ __forceinline__ float silu_f32(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+}
 
 // LDS byte offset of chunk c of tile row r (XOR swizzle over 8 chunks).
 // The XOR key (r ^ r>>3) & 7 differs for any 8 consecutive rows and also for
@@ -88,6 +96,15 @@ __device__ __forceinline__ u32x4_t gload16_cached(const char* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
 }
 
+// Workgroup barrier for LDS-only hand-offs: waits for this wave's own LDS
+// operations, then s_barrier, with a compiler memory clobber so no memory
+// access moves across it. Unlike __syncthreads() it carries no memory fence,
+// so loads still in flight to LDS (buffer loads with the LDS bit) are not
+// drained here; their consumers wait for them explicitly with vmcnt.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Raw buffer resource over [base, base + bytes): 16-byte loads through it take
 // a per-lane 32-bit offset plus a wave-uniform offset, and return zeros past
 // `bytes` (the hardware range check).
@@ -104,8 +121,8 @@ template <bool kBF16>
 __device__ __forceinline__ void store4(char* p, float a, float b, float c, float d) {
   if constexpr (kBF16) {
     u32x2_t v;
-    v.x = f32_to_bf16(a) | (f32_to_bf16(b) << 16);
-    v.y = f32_to_bf16(c) | (f32_to_bf16(d) << 16);
+    v.x = pack_bf16(a, b);
+    v.y = pack_bf16(c, d);
     *reinterpret_cast<u32x2_t*>(p) = v;
   } else {
     f32x4_t v = {a, b, c, d};

@@ -537,13 +537,255 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
   }
 }
 
-// The big kernel addresses every operand with 32-bit buffer offsets and needs
-// at least two K slabs; callers fall back to ffn_gemm_kernel otherwise.
+// DMA-staged large-tile bf16 kernel (the gate/up workhorse). 4 waves (2 x 2),
+// each owning a 128 x 128 sub-tile (4 x 4 MFMA blocks, 256 fp32 accumulators
+// in AGPRs). K is streamed in 64-byte slabs (32 bf16) fetched straight into a
+// ring of kStages LDS buffers of 32 KB by buffer loads with the LDS bit: each
+// wave instruction fills 1 KB of LDS (16 tile rows), lane i writing bytes
+// [16 i, 16 i + 16), so lane i fetches the logical chunk that the swizzle puts
+// at physical chunk i % 4 of row i / 4. No VGPRs hold slab data, no ds_write
+// is issued, and up to kStages - 1 slabs are in flight (a CU at full MFMA
+// rate consumes a 32 KB slab every ~1000 cycles; a load takes a few thousand
+// to land). Waves 0-1 fetch the weight rows, waves 2-3 the token rows.
+// The slab hand-off uses lds_barrier (no memory fence), so the compiler does
+// not drain the in-flight slabs at every barrier.
+// Rows are 64 bytes = 4 chunks, stored at chunk c ^ key64(r) with
+// key64(r) = ((r >> 1) ^ (r >> 3)) & 3: conflict-free for 8 or 16 consecutive
+// rows, and the same for every 32-row block, so a K step needs one address
+// register per operand. Fragment reads of step s+1 are interleaved with the
+// MFMAs of step s (scheduling groups).
+constexpr int kRB = 64;  // bytes of K per staged row
+
+__device__ __forceinline__ uint32_t key64(uint32_t r) { return ((r >> 1) ^ (r >> 3)) & 3u; }
+
+template <int kMode, int kGroup, int kStages>
+__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void ffn_gemm_ring_kernel(
+    FfnGemmArgs a, int n_tt, int n_ft) {
+  constexpr int kWR = 256, kTR = 256;
+  constexpr int kMW = 4, kMT = 4;
+  constexpr int kStage = (kWR + kTR) * kRB;  // 32 KB
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStage];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ww = wave & 1;
+  const int wt = wave >> 1;
+
+  const int total = n_tt * n_ft;
+  const int per = (total + kXcds - 1) / kXcds;
+  const int w = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
+  if (w >= total) return;
+  const int grp = w / (kGroup * n_tt);
+  const int rem = w - grp * (kGroup * n_tt);
+  const int gsz = min(kGroup, n_ft - grp * kGroup);
+  const int tt = rem / gsz;
+  const int ft = grp * kGroup + (rem - tt * gsz);
+
+  int kt = *a.kt_ptr;
+  kt = kt < 0 ? 0 : (kt > a.cap ? a.cap : kt);
+  int n0 = kt;
+  if (a.n_sets == 2 && a.n0_ptr) {
+    n0 = *a.n0_ptr;
+    n0 = n0 < 0 ? 0 : (n0 > kt ? kt : n0);
+  }
+  const int tiles0 = (n0 + kTR - 1) / kTR;
+  int set, row_lo, row_hi;
+  if (tt < tiles0) {
+    set = 0;
+    row_lo = tt * kTR;
+    row_hi = min(row_lo + kTR, n0);
+  } else {
+    set = 1;
+    row_lo = n0 + (tt - tiles0) * kTR;
+    row_hi = min(row_lo + kTR, kt);
+  }
+  if (row_lo >= row_hi) return;
+
+  const int n_feat = a.n_feat;
+  constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
+  const int f0 = ft * kFTile;
+
+  // ---- DMA plan: waves 0-1 fetch weight rows, waves 2-3 token rows; each
+  //      wave instruction q fills 16 rows x 64 B = 1 KB ----
+  const bool is_w = wave < 2;
+  const int rbase = 128 * (wave & 1);
+  const int r16 = lane >> 2;
+  const int pch = lane & 3;
+  const __amdgpu_buffer_rsrc_t wr0 = make_rsrc(a.w0[set], (uint32_t)(n_feat * a.w_ld));
+  const __amdgpu_buffer_rsrc_t wr1 =
+      (kMode == 0) ? make_rsrc(a.w1[set], (uint32_t)(n_feat * a.w_ld)) : wr0;
+  const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, 0xffffffffu);
+  uint32_t voff[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int r = rbase + 16 * q + r16;
+    const int c = pch ^ (int)key64((uint32_t)r);
+    if (is_w) {
+      int feat;
+      if constexpr (kMode == 0) feat = f0 + 32 * ((r >> 5) >> 1) + (r & 31);
+      else feat = f0 + r;
+      voff[q] = (uint32_t)((int64_t)feat * a.w_ld + c * 16);
+    } else {
+      int j = row_lo + r;
+      j = j < row_hi ? j : row_hi - 1;
+      voff[q] = (uint32_t)((int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + c * 16);
+    }
+  }
+  // row block (rbase + 16q) / 32 has the parity of q / 2: the gate / up choice
+  // is fixed per instruction at compile time
+  auto dma = [&](int kb, int buf) __attribute__((always_inline)) {
+    const int soff = kb * kRB;
+    if (is_w) {
+      char* region = smem + buf * kStage;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        __attribute__((address_space(3))) void* dst =
+            (__attribute__((address_space(3))) void*)(region + (rbase + 16 * q) * kRB);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds((kMode == 0 && ((q >> 1) & 1)) ? wr1 : wr0, dst, 16,
+                                                 (int)voff[q], soff, 0, 0);
+      }
+    } else {
+      char* region = smem + buf * kStage + kWR * kRB;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        __attribute__((address_space(3))) void* dst =
+            (__attribute__((address_space(3))) void*)(region + (rbase + 16 * q) * kRB);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, dst, 16, (int)voff[q], soff, 0, 0);
+      }
+    }
+  };
+
+  f32x16_t acc[kMW][kMT];
+#pragma unroll
+  for (int i = 0; i < kMW; ++i)
+#pragma unroll
+    for (int j = 0; j < kMT; ++j) acc[i][j] = f32x16_t{};
+
+  const int lrow = lane & 31;
+  const int lhalf = lane >> 5;
+  auto opaque = [](uint32_t v) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(v));
+    return v;
+  };
+  const uint32_t rkey = key64((uint32_t)lrow);
+  const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kRB);
+  const uint32_t rowb = (uint32_t)(kWR * kRB + (wt * 128 + lrow) * kRB);
+  u32x4_t fa0[kMW], fb0[kMT], fa1[kMW], fb1[kMT];
+  auto read_frags = [&](u32x4_t (&fa)[kMW], u32x4_t (&fb)[kMT], const char* sw, int step) __attribute__((always_inline)) {
+    const uint32_t off = (((uint32_t)(2 * step + lhalf)) ^ opaque(rkey)) << 4;
+    const char* pa = sw + rowa + off;
+    const char* pb = sw + rowb + off;
+#pragma unroll
+    for (int i = 0; i < kMW; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(pa + 32 * i * kRB);
+#pragma unroll
+    for (int j = 0; j < kMT; ++j) fb[j] = *reinterpret_cast<const u32x4_t*>(pb + 32 * j * kRB);
+  };
+  auto mfmas = [&](const u32x4_t (&fa)[kMW], const u32x4_t (&fb)[kMT]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kMW; ++i)
+#pragma unroll
+      for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[i], fb[j]);
+  };
+
+  const int nk = a.k_bytes / kRB;  // >= kStages (checked by the launcher)
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s) dma(s, s);
+  int buf = 0;
+  for (int kb = 0; kb < nk; ++kb) {
+    // wait for slab kb: the loads of the (up to kStages - 2) later slabs may stay in flight
+    const int ahead = min(nk - 1 - kb, kStages - 2);
+    if (ahead >= 3) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+    else if (ahead == 2) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+    // every wave is past slab kb-1: its buffer now receives slab kb + kStages - 1
+    if (kb + kStages - 1 < nk) {
+      int nb = buf + kStages - 1;
+      nb = nb >= kStages ? nb - kStages : nb;
+      dma(kb + kStages - 1, nb);
+    }
+    const char* sw = smem + buf * kStage;
+    read_frags(fa0, fb0, sw, 0);
+    read_frags(fa1, fb1, sw, 1);
+    mfmas(fa0, fb0);
+    mfmas(fa1, fb1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 24, 0);
+    buf = buf + 1 == kStages ? 0 : buf + 1;
+  }
+
+#pragma unroll
+  for (int j = 0; j < kMT; ++j) {
+    const int jr = row_lo + wt * 128 + 32 * j + lrow;
+    if (jr >= row_hi) continue;
+    const int orow_idx = map_row(jr, a.omap1, a.omap2);
+    char* orow = a.out + (int64_t)orow_idx * a.out_ld;
+    if constexpr (kMode == 0) {
+#pragma unroll
+      for (int p = 0; p < kMW / 2; ++p) {
+        const int fb0_ = f0 + 32 * (ww * (kMW / 2) + p) + 4 * lhalf;
+        if (fb0_ >= n_feat) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16_t& ag = acc[2 * p][j];
+          const f32x16_t& au = acc[2 * p + 1][j];
+          float v0 = silu_f32(ag[4 * g + 0]) * au[4 * g + 0];
+          float v1 = silu_f32(ag[4 * g + 1]) * au[4 * g + 1];
+          float v2 = silu_f32(ag[4 * g + 2]) * au[4 * g + 2];
+          float v3 = silu_f32(ag[4 * g + 3]) * au[4 * g + 3];
+          store4<true>(orow + (int64_t)(fb0_ + 8 * g) * 2, v0, v1, v2, v3);
+        }
+      }
+    } else {
+      const char* rrow = a.res ? a.res + (int64_t)orow_idx * a.res_ld : nullptr;
+#pragma unroll
+      for (int i = 0; i < kMW; ++i) {
+        const int fb0_ = f0 + ww * 128 + 32 * i + 4 * lhalf;
+        if (fb0_ >= n_feat) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int f = fb0_ + 8 * g;
+          float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
+          float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+          if (rrow) {
+            f32x4_t rr = load4<true>(rrow + (int64_t)f * 2);
+            v0 += rr.x; v1 += rr.y; v2 += rr.z; v3 += rr.w;
+          }
+          store4<true>(orow + (int64_t)f * 2, v0, v1, v2, v3);
+        }
+      }
+    }
+  }
+}
+
+template <int kMode, int kGroup, int kStages>
+hipError_t launch_ring(const FfnGemmArgs& a, hipStream_t stream) {
+  constexpr int kFTile = (kMode == 0) ? 128 : 256;
+  const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
+  const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
+  if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
+  const int total = n_tt * n_ft;
+  const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
+  hipLaunchKernelGGL((ffn_gemm_ring_kernel<kMode, kGroup, kStages>), dim3(grid), dim3(256), 0, stream,
+                     a, n_tt, n_ft);
+  return hipGetLastError();
+}
+
+// The large-tile kernels address every operand with 32-bit buffer offsets and
+// need at least a few K slabs; callers fall back to ffn_gemm_kernel otherwise.
 inline bool big_ok(const FfnGemmArgs& a) {
   const int64_t lim = (int64_t)1 << 31;
   return a.k_bytes >= 2 * kKB && (int64_t)a.tok_rows * a.tok_ld < lim &&
          (int64_t)a.n_feat * a.w_ld < lim;
 }
+inline bool ring_ok(const FfnGemmArgs& a, int stages) { return big_ok(a) && a.k_bytes >= stages * kRB; }
 
 template <int kMode, int kGroup>
 hipError_t launch_big(const FfnGemmArgs& a, hipStream_t stream) {
@@ -574,16 +816,19 @@ hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-// Tile shapes, chosen by timing every variant on the five named workloads:
-//   gate/up: 256 x 256 (128 output features x 256 tokens), 4 x 2 waves, one
-//            LDS stage, groups of 4 feature tiles;
+// Kernel and tile choice, from timing every variant on the five named workloads:
+//   gate/up: the DMA ring kernel, 4 stages (128 output features x 256 tokens,
+//            groups of 4 feature tiles); fallback 8-wave 256 x 256 register-staged;
 //   down:    the 4-wave 256 x 256 kernel when it yields >= 200 tiles (enough
 //            to fill the chip), else 256 x 128 (4 x 2 waves) for d < 3072 and
 //            128 x 128 (2 x 2 waves) for the 7B width, token-tile-major order
 //            (every weight tile of a token tile stays in one XCD's L2).
 // fp32 data (tiny workloads) uses 128 x 128 tiles.
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
-  if (bf16) return launch_cfg<true, 0, 256, 256, 4, 2, 1, 1, 4>(a, stream);
+  if (bf16) {
+    if (ring_ok(a, 4)) return launch_ring<0, 4, 4>(a, stream);
+    return launch_cfg<true, 0, 256, 256, 4, 2, 1, 1, 4>(a, stream);
+  }
   return launch_cfg<false, 0, 128, 128, 2, 2, 2>(a, stream);
 }
 

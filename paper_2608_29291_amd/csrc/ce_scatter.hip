@@ -37,7 +37,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(const char* __restrict__ f
       for (int q = 0; q < 4; ++q) {
         const float lo = bf16_to_f32(x[q] & 0xffffu) + bf16_to_f32(y[q] & 0xffffu);
         const float hi = bf16_to_f32(x[q] >> 16) + bf16_to_f32(y[q] >> 16);
-        r[q] = f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+        r[q] = pack_bf16(lo, hi);
       }
     } else {
 #pragma unroll

@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
       }
     }
     a.logits[lo + tid] = l;
-    if (a.probs) a.probs[lo + tid] = is_keep ? 1.0f : 1.0f / (1.0f + __expf(-l));
+    if (a.probs) a.probs[lo + tid] = is_keep ? 1.0f : 1.0f / (1.0f + expf(-l));
   }
 }
 
