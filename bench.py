@@ -231,7 +231,7 @@ def main():
     achieved = gateup_flops / (stages["ffn_gateup"] * 1e-6) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": load_traffic(),
-                "kernel": "ffn_gemm_kernel gate/up + SwiGLU (ce_ffn_gateup)",
+                "kernel": "ffn_gemm_pp2_kernel gate/up + SwiGLU (ce_ffn_gateup)",
                 "flops_per_launch": gateup_flops}
 
     block_flops = (2.0 * cap * d * 3 * F

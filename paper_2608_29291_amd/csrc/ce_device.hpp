@@ -105,6 +105,15 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N vector memory operations of this wave are in flight
+// (vmcnt only; the export and LDS/scalar counters are left alone).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // vmcnt lives in bits [3:0] and [15:14]; expcnt = 7 and lgkmcnt = 15 mean "no wait"
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 // Raw buffer resource over [base, base + bytes): 16-byte loads through it take
 // a per-lane 32-bit offset plus a wave-uniform offset, and return zeros past
 // `bytes` (the hardware range check).

@@ -283,294 +283,44 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
   }
 }
 
-// Large-tile bf16 variant: 4 waves (2 x 2), each owning a 128 x 128 sub-tile
-// (4 x 4 MFMA blocks, 256 fp32 accumulators kept in AGPRs), one wave per SIMD.
-// LDS fragment reads are software-pipelined: the fragments of K step s+1 are
-// read into the second register set while the 16 MFMAs of step s run, so the
-// single wave on each SIMD never waits on LDS between MFMA groups. Per 128-byte
-// K slab a wave reads 32 fragments for 64 MFMAs (half the LDS traffic per
-// MFMA of a 64 x 128 wave tile).
-template <int kMode, int kGroup>
-__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void ffn_gemm_big_kernel(FfnGemmArgs a, int n_tt, int n_ft) {
-  constexpr int kWR = 256, kTR = 256;
-  constexpr int kMW = 4, kMT = 4;
-  constexpr int kLoads = 8;  // per operand per thread per slab
-  constexpr int kStage = (kWR + kTR) * kKB;
-  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int ww = wave & 1;
-  const int wt = wave >> 1;
-
-  const int total = n_tt * n_ft;
-  const int per = (total + kXcds - 1) / kXcds;
-  const int w = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
-  if (w >= total) return;
-  const int grp = w / (kGroup * n_tt);
-  const int rem = w - grp * (kGroup * n_tt);
-  const int gsz = min(kGroup, n_ft - grp * kGroup);
-  const int tt = rem / gsz;
-  const int ft = grp * kGroup + (rem - tt * gsz);
-
-  int kt = *a.kt_ptr;
-  kt = kt < 0 ? 0 : (kt > a.cap ? a.cap : kt);
-  int n0 = kt;
-  if (a.n_sets == 2 && a.n0_ptr) {
-    n0 = *a.n0_ptr;
-    n0 = n0 < 0 ? 0 : (n0 > kt ? kt : n0);
-  }
-  const int tiles0 = (n0 + kTR - 1) / kTR;
-  int set, row_lo, row_hi;
-  if (tt < tiles0) {
-    set = 0;
-    row_lo = tt * kTR;
-    row_hi = min(row_lo + kTR, n0);
-  } else {
-    set = 1;
-    row_lo = n0 + (tt - tiles0) * kTR;
-    row_hi = min(row_lo + kTR, kt);
-  }
-  if (row_lo >= row_hi) return;
-
-  const int n_feat = a.n_feat;
-  constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
-  const int f0 = ft * kFTile;
-  const int cchunk = tid & 7;
-  const int rsub = tid >> 3;  // 0..31
-
-  // Buffer loads: one per-lane offset for all weight rows of this thread
-  // (row blocks differ by a wave-uniform offset); rows past n_feat lie past
-  // the resource's range and read as zero. Token rows are gathered, one
-  // 32-bit offset each; rows past row_hi read a clamped valid row (their
-  // results are never stored).
-  __amdgpu_buffer_rsrc_t wr0, wr1;
-  if constexpr (kMode == 0) {
-    wr0 = make_rsrc(a.w0[set], (uint32_t)(n_feat * a.w_ld));
-    wr1 = make_rsrc(a.w1[set], (uint32_t)(n_feat * a.w_ld));
-  } else {
-    wr0 = make_rsrc(a.w0[set], (uint32_t)(n_feat * a.w_ld));
-    wr1 = wr0;
-  }
-  const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, 0xffffffffu);
-  const uint32_t wvoff = (uint32_t)((int64_t)(f0 + rsub) * a.w_ld + cchunk * 16);
-  uint32_t tvoff[kLoads];
-#pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    int j = row_lo + 32 * i + rsub;
-    j = j < row_hi ? j : row_hi - 1;
-    tvoff[i] = (uint32_t)((int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + cchunk * 16);
-  }
-
-  // two register sets of in-flight global loads: the loads of slab kb+2 are
-  // issued at the start of iteration kb and written to LDS at the end of
-  // iteration kb+1, so each has almost two iterations of MFMA time to land
-  u32x4_t rw0[kLoads], rt0[kLoads], rw1[kLoads], rt1[kLoads];
-  auto gload = [&](u32x4_t (&rw)[kLoads], u32x4_t (&rt)[kLoads], int kb) __attribute__((always_inline)) {
-    const uint32_t koff = (uint32_t)(kb * kKB);
-#pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      // weight tile row block i: gate/up alternate in mode 0
-      const uint32_t blk_off = (uint32_t)((kMode == 0 ? 32 * (i >> 1) : 32 * i) * a.w_ld);
-      rw[i] = bload16((kMode == 0 && (i & 1)) ? wr1 : wr0, wvoff, blk_off + koff);
-      rt[i] = bload16(trs, tvoff[i], koff);
-    }
-  };
-  // LDS addresses are formed from two per-lane values plus immediates. The
-  // swizzle key of tile row r = 32*i + x is (x ^ x>>3 ^ 4*i) & 7, so only the
-  // parity of the row block i changes it. `opaque` hides the per-lane values
-  // from loop-invariant hoisting, which would otherwise keep one address
-  // register per fragment and per buffer alive across the K loop.
-  auto opaque = [](uint32_t v) __attribute__((always_inline)) {
-    asm volatile("" : "+v"(v));
-    return v;
-  };
-  const uint32_t wkey = (uint32_t)((rsub ^ (rsub >> 3)) & 7);
-  auto lstore = [&](const u32x4_t (&rw)[kLoads], const u32x4_t (&rt)[kLoads], int buf) __attribute__((always_inline)) {
-    const uint32_t k = opaque(wkey);
-    const uint32_t base = (uint32_t)(buf * kStage) + (uint32_t)rsub * kKB;
-    const uint32_t even = base + ((cchunk ^ k) << 4);
-    const uint32_t odd = base + ((cchunk ^ k ^ 4u) << 4);
-#pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const uint32_t o = ((i & 1) ? odd : even) + (uint32_t)(32 * i * kKB);
-      *reinterpret_cast<u32x4_t*>(smem + o) = rw[i];
-      *reinterpret_cast<u32x4_t*>(smem + o + kWR * kKB) = rt[i];
-    }
-  };
-
-  f32x16_t acc[kMW][kMT];
-#pragma unroll
-  for (int i = 0; i < kMW; ++i)
-#pragma unroll
-    for (int j = 0; j < kMT; ++j) acc[i][j] = f32x16_t{};
-
-  const int lrow = lane & 31;
-  const int lhalf = lane >> 5;
-  u32x4_t fa0[kMW], fb0[kMT], fa1[kMW], fb1[kMT];
-  const uint32_t rkey = (uint32_t)((lrow ^ (lrow >> 3)) & 7);
-  const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kKB);
-  const uint32_t rowb = (uint32_t)(kWR * kKB + (wt * 128 + lrow) * kKB);
-  auto read_frags = [&](u32x4_t (&fa)[kMW], u32x4_t (&fb)[kMT], const char* sw, int step) __attribute__((always_inline)) {
-    const uint32_t k = opaque(rkey);
-    const uint32_t c = (uint32_t)(2 * step + lhalf);
-    const uint32_t se = (c ^ k) << 4;        // even row blocks
-    const uint32_t so = (c ^ k ^ 4u) << 4;   // odd row blocks
-    const char* pa = sw + rowa;
-    const char* pb = sw + rowb;
-#pragma unroll
-    for (int i = 0; i < kMW; ++i)
-      fa[i] = *reinterpret_cast<const u32x4_t*>(pa + ((i & 1) ? so : se) + 32 * i * kKB);
-#pragma unroll
-    for (int j = 0; j < kMT; ++j)
-      fb[j] = *reinterpret_cast<const u32x4_t*>(pb + ((j & 1) ? so : se) + 32 * j * kKB);
-  };
-  auto mfmas = [&](const u32x4_t (&fa)[kMW], const u32x4_t (&fb)[kMT]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < kMW; ++i)
-#pragma unroll
-      for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[i], fb[j]);
-  };
-
-  // One K slab: fragments of step s+1 are read while the 16 MFMAs of step s
-  // run; the next slab's LDS tile is written during the last step. The
-  // scheduling groups pin that interleave (mask 0x008 MFMA, 0x100 LDS read,
-  // 0x200 LDS write, 0x020 global read).
-  auto slab = [&](auto load_tag, auto write_tag, const char* sw, int next_buf,
-                  u32x4_t (&lw)[kLoads], u32x4_t (&lt)[kLoads], const u32x4_t (&sw_w)[kLoads],
-                  const u32x4_t (&sw_t)[kLoads], int load_kb) __attribute__((always_inline)) {
-    constexpr bool kLoad = decltype(load_tag)::value;
-    constexpr bool kWrite = decltype(write_tag)::value;
-    if constexpr (kLoad) gload(lw, lt, load_kb);
-    read_frags(fa0, fb0, sw, 0);
-    read_frags(fa1, fb1, sw, 1);
-    mfmas(fa0, fb0);
-    read_frags(fa0, fb0, sw, 2);
-    mfmas(fa1, fb1);
-    read_frags(fa1, fb1, sw, 3);
-    mfmas(fa0, fb0);
-    if constexpr (kWrite) lstore(sw_w, sw_t, next_buf);
-    mfmas(fa1, fb1);
-    if constexpr (kLoad) __builtin_amdgcn_sched_group_barrier(0x020, 2 * kLoads, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-#pragma unroll
-    for (int st = 0; st < 3; ++st) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    }
-    if constexpr (kWrite) {
-#pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-      }
-    } else {
-      __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-    }
-    __syncthreads();
-  };
-  using T = std::true_type;
-  using F = std::false_type;
-
-  const int nk = a.k_bytes / kKB;  // >= 2 (checked by the launcher)
-  gload(rw0, rt0, 0);
-  gload(rw1, rt1, 1);
-  lstore(rw0, rt0, 0);
-  __syncthreads();
-  // Pairs of slabs (even slab in buffer 0, odd slab in buffer 1). The loads
-  // two slabs ahead clamp the slab index to the last one: near the end they
-  // re-read a slab from L2 and write it to a buffer that is never read again,
-  // which keeps one branch-free loop body.
-  int kb = 0;
-  for (; kb + 1 < nk; kb += 2) {
-    slab(T{}, T{}, smem, 1, rw0, rt0, rw1, rt1, min(kb + 2, nk - 1));
-    slab(T{}, T{}, smem + kStage, 0, rw1, rt1, rw0, rt0, min(kb + 3, nk - 1));
-  }
-  if (kb < nk) slab(F{}, F{}, smem, 1, rw0, rt0, rw1, rt1, 0);  // odd slab count: last slab
-
-#pragma unroll
-  for (int j = 0; j < kMT; ++j) {
-    const int jr = row_lo + wt * 128 + 32 * j + lrow;
-    if (jr >= row_hi) continue;
-    const int orow_idx = map_row(jr, a.omap1, a.omap2);
-    char* orow = a.out + (int64_t)orow_idx * a.out_ld;
-    if constexpr (kMode == 0) {
-#pragma unroll
-      for (int p = 0; p < kMW / 2; ++p) {
-        const int fb0 = f0 + 32 * (ww * (kMW / 2) + p) + 4 * lhalf;
-        if (fb0 >= n_feat) continue;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x16_t& ag = acc[2 * p][j];
-          const f32x16_t& au = acc[2 * p + 1][j];
-          float v0 = silu_f32(ag[4 * g + 0]) * au[4 * g + 0];
-          float v1 = silu_f32(ag[4 * g + 1]) * au[4 * g + 1];
-          float v2 = silu_f32(ag[4 * g + 2]) * au[4 * g + 2];
-          float v3 = silu_f32(ag[4 * g + 3]) * au[4 * g + 3];
-          store4<true>(orow + (int64_t)(fb0 + 8 * g) * 2, v0, v1, v2, v3);
-        }
-      }
-    } else {
-      const char* rrow = a.res ? a.res + (int64_t)orow_idx * a.res_ld : nullptr;
-#pragma unroll
-      for (int i = 0; i < kMW; ++i) {
-        const int fb0 = f0 + ww * 128 + 32 * i + 4 * lhalf;
-        if (fb0 >= n_feat) continue;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int f = fb0 + 8 * g;
-          float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
-          float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-          if (rrow) {
-            f32x4_t r = load4<true>(rrow + (int64_t)f * 2);
-            v0 += r.x; v1 += r.y; v2 += r.z; v3 += r.w;
-          }
-          store4<true>(orow + (int64_t)f * 2, v0, v1, v2, v3);
-        }
-      }
-    }
-  }
-}
-
-// DMA-staged large-tile bf16 kernel (the gate/up workhorse). 4 waves (2 x 2),
-// each owning a 128 x 128 sub-tile (4 x 4 MFMA blocks, 256 fp32 accumulators
-// in AGPRs). K is streamed in 64-byte slabs (32 bf16) fetched straight into a
-// ring of kStages LDS buffers of 32 KB by buffer loads with the LDS bit: each
-// wave instruction fills 1 KB of LDS (16 tile rows), lane i writing bytes
-// [16 i, 16 i + 16), so lane i fetches the logical chunk that the swizzle puts
-// at physical chunk i % 4 of row i / 4. No VGPRs hold slab data, no ds_write
-// is issued, and up to kStages - 1 slabs are in flight (a CU at full MFMA
-// rate consumes a 32 KB slab every ~1000 cycles; a load takes a few thousand
-// to land). Waves 0-1 fetch the weight rows, waves 2-3 the token rows.
-// The slab hand-off uses lds_barrier (no memory fence), so the compiler does
-// not drain the in-flight slabs at every barrier.
-// Rows are 64 bytes = 4 chunks, stored at chunk c ^ key64(r) with
-// key64(r) = ((r >> 1) ^ (r >> 3)) & 3: conflict-free for 8 or 16 consecutive
-// rows, and the same for every 32-row block, so a K step needs one address
-// register per operand. Fragment reads of step s+1 are interleaved with the
-// MFMAs of step s (scheduling groups).
-constexpr int kRB = 64;  // bytes of K per staged row
-
-__device__ __forceinline__ uint32_t key64(uint32_t r) { return ((r >> 1) ^ (r >> 3)) & 3u; }
-
-template <int kMode, int kGroup, int kStages>
-__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void ffn_gemm_ring_kernel(
+// Ping-pong bf16 kernel (the gate/up workhorse, and the down GEMM on large
+// grids): 8 waves, two per SIMD, over a 256 x 256 tile. Wave w owns weight
+// rows 128 (w & 1) .. +128 and token rows 64 (w >> 1) .. +64 (4 x 2 MFMA
+// blocks, 128 fp32 accumulators). Waves 0-3 (group A) and 4-7 (group B) share
+// the four SIMDs (wave w on SIMD w % 4) and run half a phase apart: while one
+// group issues its 16 MFMAs for 64 bytes of K, the other reads its fragments
+// of the next 64 bytes from LDS and issues DMA. Every phase ends at a
+// workgroup barrier; group B starts one barrier late and group A ends with one
+// extra barrier, so both execute the same number.
+//
+// Operands reach LDS through buffer loads with the LDS bit, each wave
+// instruction fetching 8 rows x 128 bytes: whole cache lines (16 rows x 64
+// bytes, i.e. half lines, move about half as many bytes per clock from L2).
+// A "superslab" is 128 bytes of K: 32 KB per operand. LDS holds 3 token
+// superslabs and 2 weight superslabs (160 KB); tokens, which mostly miss L2,
+// are fetched two superslabs ahead, weights one ahead. Waves 0-3 fetch weight
+// rows, waves 4-7 token rows, half of their rows in each of the two memory
+// phases of a superslab so the DMA writes into LDS do not bunch up. Rows are
+// 128 bytes, chunk c of row r stored at chunk c ^ (r & 7), which keeps the
+// 32-row fragment reads free of bank conflicts.
+template <int kMode, int kGroup, bool kPrio>
+__global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) void ffn_gemm_pp2_kernel(
     FfnGemmArgs a, int n_tt, int n_ft) {
   constexpr int kWR = 256, kTR = 256;
-  constexpr int kMW = 4, kMT = 4;
-  constexpr int kStage = (kWR + kTR) * kRB;  // 32 KB
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStage];
+  constexpr int kMW = 4, kMT = 2;
+  constexpr int kRow = 128;                  // bytes of K per staged row
+  constexpr int kSlab = 256 * kRow;          // one operand's superslab: 32 KB
+  constexpr int kWBufs = 2, kTBufs = 3;
+  __shared__ __attribute__((aligned(1024))) char smem[(kWBufs + kTBufs) * kSlab];
+  char* const wsm = smem;                    // weight ring
+  char* const tsm = smem + kWBufs * kSlab;   // token ring
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ww = wave & 1;
   const int wt = wave >> 1;
+  const bool late = wave >= 4;  // group B
 
   const int total = n_tt * n_ft;
   const int per = (total + kXcds - 1) / kXcds;
@@ -606,12 +356,11 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
   constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
   const int f0 = ft * kFTile;
 
-  // ---- DMA plan: waves 0-1 fetch weight rows, waves 2-3 token rows; each
-  //      wave instruction q fills 16 rows x 64 B = 1 KB ----
-  const bool is_w = wave < 2;
-  const int rbase = 128 * (wave & 1);
-  const int r16 = lane >> 2;
-  const int pch = lane & 3;
+  // ---- DMA plan: waves 0-3 fetch weight rows 64 (w & 3) .. +63, waves 4-7
+  //      the same token rows; instruction q covers 8 rows x 128 B ----
+  const bool is_w = wave < 4;
+  const int r8 = lane >> 3;
+  const int pch = lane & 7;
   const __amdgpu_buffer_rsrc_t wr0 = make_rsrc(a.w0[set], (uint32_t)(n_feat * a.w_ld));
   const __amdgpu_buffer_rsrc_t wr1 =
       (kMode == 0) ? make_rsrc(a.w1[set], (uint32_t)(n_feat * a.w_ld)) : wr0;
@@ -619,8 +368,8 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
   uint32_t voff[8];
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
-    const int r = rbase + 16 * q + r16;
-    const int c = pch ^ (int)key64((uint32_t)r);
+    const int r = 64 * (wave & 3) + 8 * q + r8;
+    const int c = pch ^ (r & 7);
     if (is_w) {
       int feat;
       if constexpr (kMode == 0) feat = f0 + 32 * ((r >> 5) >> 1) + (r & 31);
@@ -632,29 +381,30 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
       voff[q] = (uint32_t)((int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + c * 16);
     }
   }
-  // row block (rbase + 16q) / 32 has the parity of q / 2: the gate / up choice
-  // is fixed per instruction at compile time
-  auto dma = [&](int kb, int buf) __attribute__((always_inline)) {
-    const int soff = kb * kRB;
+  // weight row block (64 w + 8 q) / 32 has the parity of q / 4: the gate / up
+  // choice is fixed per instruction at compile time. kPart 0 issues all 8
+  // instructions, 1 the first four (rows 0-31 of the wave's 64), 2 the rest.
+  auto dma = [&](int s, int buf, auto part) __attribute__((always_inline)) {
+    constexpr int kPart = decltype(part)::value;
+    const int soff = s * kRow;
+    char* region = (is_w ? wsm : tsm) + buf * kSlab + 64 * (wave & 3) * kRow;
     if (is_w) {
-      char* region = smem + buf * kStage;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        __attribute__((address_space(3))) void* dst =
-            (__attribute__((address_space(3))) void*)(region + (rbase + 16 * q) * kRB);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds((kMode == 0 && ((q >> 1) & 1)) ? wr1 : wr0, dst, 16,
-                                                 (int)voff[q], soff, 0, 0);
-      }
+      for (int q = 0; q < 8; ++q)
+        if (kPart == 0 || (kPart == 1) == (q < 4))
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              (kMode == 0 && ((q >> 2) & 1)) ? wr1 : wr0,
+              (__attribute__((address_space(3))) void*)(region + 8 * q * kRow), 16, (int)voff[q], soff, 0, 0);
     } else {
-      char* region = smem + buf * kStage + kWR * kRB;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        __attribute__((address_space(3))) void* dst =
-            (__attribute__((address_space(3))) void*)(region + (rbase + 16 * q) * kRB);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, dst, 16, (int)voff[q], soff, 0, 0);
-      }
+      for (int q = 0; q < 8; ++q)
+        if (kPart == 0 || (kPart == 1) == (q < 4))
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              trs, (__attribute__((address_space(3))) void*)(region + 8 * q * kRow), 16, (int)voff[q], soff, 0, 0);
     }
   };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
 
   f32x16_t acc[kMW][kMT];
 #pragma unroll
@@ -668,62 +418,80 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
     asm volatile("" : "+v"(v));
     return v;
   };
-  const uint32_t rkey = key64((uint32_t)lrow);
-  const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kRB);
-  const uint32_t rowb = (uint32_t)(kWR * kRB + (wt * 128 + lrow) * kRB);
-  u32x4_t fa0[kMW], fb0[kMT], fa1[kMW], fb1[kMT];
-  auto read_frags = [&](u32x4_t (&fa)[kMW], u32x4_t (&fb)[kMT], const char* sw, int step) __attribute__((always_inline)) {
-    const uint32_t off = (((uint32_t)(2 * step + lhalf)) ^ opaque(rkey)) << 4;
-    const char* pa = sw + rowa + off;
-    const char* pb = sw + rowb + off;
-#pragma unroll
-    for (int i = 0; i < kMW; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(pa + 32 * i * kRB);
-#pragma unroll
-    for (int j = 0; j < kMT; ++j) fb[j] = *reinterpret_cast<const u32x4_t*>(pb + 32 * j * kRB);
-  };
-  auto mfmas = [&](const u32x4_t (&fa)[kMW], const u32x4_t (&fb)[kMT]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < kMW; ++i)
-#pragma unroll
-      for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[i], fb[j]);
-  };
+  const uint32_t rkey = (uint32_t)(lrow & 7);
+  const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kRow);
+  const uint32_t rowb = (uint32_t)((wt * 64 + lrow) * kRow);
+  u32x4_t fa[2][kMW], fb[2][kMT];
 
-  const int nk = a.k_bytes / kRB;  // >= kStages (checked by the launcher)
+  const int ns = a.k_bytes / kRow;  // superslabs (>= 3, checked by the launcher)
+  if (is_w) {
+    dma(0, 0, I0{});  // weights: superslab 0
+    wait_vmcnt<0>();
+  } else {
+    dma(0, 0, I0{});  // tokens: superslabs 0 and 1
+    dma(1, 1, I0{});
+    wait_vmcnt<8>();
+  }
+  lds_barrier();  // superslab 0 is in LDS
+  if (late) lds_barrier();
+  int wb = 0, tb = 0;  // ring slots of superslab s
+  // one memory phase and one compute phase over K half H of superslab s
+  auto half = [&](int s, auto hc) __attribute__((always_inline)) {
+    constexpr int H = decltype(hc)::value;
+    // ---- memory phase: fragments of K half H of superslab s ----
+    const char* sa = wsm + wb * kSlab;
+    const char* sb = tsm + tb * kSlab;
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s) dma(s, s);
-  int buf = 0;
-  for (int kb = 0; kb < nk; ++kb) {
-    // wait for slab kb: the loads of the (up to kStages - 2) later slabs may stay in flight
-    const int ahead = min(nk - 1 - kb, kStages - 2);
-    if (ahead >= 3) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
-    else if (ahead == 2) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    else if (ahead == 1) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    for (int step = 0; step < 2; ++step) {
+      const uint32_t off = (((uint32_t)(4 * H + 2 * step + lhalf)) ^ opaque(rkey)) << 4;
+#pragma unroll
+      for (int i = 0; i < kMW; ++i) fa[step][i] = *reinterpret_cast<const u32x4_t*>(sa + rowa + off + 32 * i * kRow);
+#pragma unroll
+      for (int j = 0; j < kMT; ++j) fb[step][j] = *reinterpret_cast<const u32x4_t*>(sb + rowb + off + 32 * j * kRow);
+    }
+    // superslab s - 1 is consumed by both groups: refill its slots, half of
+    // this wave's rows in each phase (weights one superslab ahead, tokens two)
+    using Part = std::integral_constant<int, H + 1>;
+    if (is_w) {
+      if (s + 1 < ns) dma(s + 1, wb ^ 1, Part{});
+    } else {
+      if (s + 2 < ns) dma(s + 2, tb == 0 ? 2 : tb - 1, Part{});
+      // token superslab s + 1 is read next and must have landed; the 8
+      // instructions of superslab s + 2 may stay in flight
+      if (H == 1 && s + 1 < ns) {
+        if (s + 2 >= ns) wait_vmcnt<0>();
+        else wait_vmcnt<8>();
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
-    // every wave is past slab kb-1: its buffer now receives slab kb + kStages - 1
-    if (kb + kStages - 1 < nk) {
-      int nb = buf + kStages - 1;
-      nb = nb >= kStages ? nb - kStages : nb;
-      dma(kb + kStages - 1, nb);
-    }
-    const char* sw = smem + buf * kStage;
-    read_frags(fa0, fb0, sw, 0);
-    read_frags(fa1, fb1, sw, 1);
-    mfmas(fa0, fb0);
-    mfmas(fa1, fb1);
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- compute phase ----
+    if constexpr (kPrio) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 24, 0);
-    buf = buf + 1 == kStages ? 0 : buf + 1;
+    for (int step = 0; step < 2; ++step)
+#pragma unroll
+      for (int i = 0; i < kMW; ++i)
+#pragma unroll
+        for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[step][i], fb[step][j]);
+    if constexpr (kPrio) __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_sched_barrier(0);
+    // weight superslab s + 1 (second half issued in this memory phase) must
+    // have landed before the next barrier; the wait sits behind the MFMAs
+    if (H == 1 && is_w && s + 1 < ns) wait_vmcnt<0>();
+    lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int s = 0; s < ns; ++s) {
+    half(s, I0{});
+    half(s, I1{});
+    wb ^= 1;
+    tb = tb == 2 ? 0 : tb + 1;
   }
 
 #pragma unroll
   for (int j = 0; j < kMT; ++j) {
-    const int jr = row_lo + wt * 128 + 32 * j + lrow;
+    const int jr = row_lo + wt * 64 + 32 * j + lrow;
     if (jr >= row_hi) continue;
     const int orow_idx = map_row(jr, a.omap1, a.omap2);
     char* orow = a.out + (int64_t)orow_idx * a.out_ld;
@@ -763,18 +531,19 @@ __global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) 
       }
     }
   }
+  if (!late) lds_barrier();  // matches group B's extra barrier at the start
 }
 
-template <int kMode, int kGroup, int kStages>
-hipError_t launch_ring(const FfnGemmArgs& a, hipStream_t stream) {
+template <int kMode, int kGroup, bool kPrio>
+hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream) {
   constexpr int kFTile = (kMode == 0) ? 128 : 256;
   const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
   const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
   if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
   const int total = n_tt * n_ft;
   const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
-  hipLaunchKernelGGL((ffn_gemm_ring_kernel<kMode, kGroup, kStages>), dim3(grid), dim3(256), 0, stream,
-                     a, n_tt, n_ft);
+  hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio>), dim3(grid), dim3(512), 0, stream, a,
+                     n_tt, n_ft);
   return hipGetLastError();
 }
 
@@ -785,20 +554,7 @@ inline bool big_ok(const FfnGemmArgs& a) {
   return a.k_bytes >= 2 * kKB && (int64_t)a.tok_rows * a.tok_ld < lim &&
          (int64_t)a.n_feat * a.w_ld < lim;
 }
-inline bool ring_ok(const FfnGemmArgs& a, int stages) { return big_ok(a) && a.k_bytes >= stages * kRB; }
-
-template <int kMode, int kGroup>
-hipError_t launch_big(const FfnGemmArgs& a, hipStream_t stream) {
-  constexpr int kFTile = (kMode == 0) ? 128 : 256;
-  const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
-  const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
-  if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
-  const int total = n_tt * n_ft;
-  const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
-  hipLaunchKernelGGL((ffn_gemm_big_kernel<kMode, kGroup>), dim3(grid), dim3(256), 0, stream, a, n_tt,
-                     n_ft);
-  return hipGetLastError();
-}
+inline bool pp2_ok(const FfnGemmArgs& a) { return big_ok(a) && a.k_bytes % 128 == 0 && a.k_bytes >= 3 * 128; }
 
 template <bool kBF16, int kMode, int kWR, int kTR, int kWW, int kWT, int kStages, int kPf = 1,
           int kGroup = 1>
@@ -817,16 +573,17 @@ hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
 }  // namespace
 
 // Kernel and tile choice, from timing every variant on the five named workloads:
-//   gate/up: the DMA ring kernel, 4 stages (128 output features x 256 tokens,
+//   gate/up: the full-line ping-pong kernel (128 output features x 256 tokens,
 //            groups of 4 feature tiles); fallback 8-wave 256 x 256 register-staged;
-//   down:    the 4-wave 256 x 256 kernel when it yields >= 200 tiles (enough
-//            to fill the chip), else 256 x 128 (4 x 2 waves) for d < 3072 and
-//            128 x 128 (2 x 2 waves) for the 7B width, token-tile-major order
-//            (every weight tile of a token tile stays in one XCD's L2).
+//   down:    the full-line ping-pong kernel when its 256 x 256 tiles number
+//            >= 200 (enough to fill the chip), else 256 x 128 (4 x 2 waves)
+//            for d < 3072 and 128 x 128 (2 x 2 waves) for the 7B width,
+//            token-tile-major order (every weight tile of a token tile stays in
+//            one XCD's L2).
 // fp32 data (tiny workloads) uses 128 x 128 tiles.
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
   if (bf16) {
-    if (ring_ok(a, 4)) return launch_ring<0, 4, 4>(a, stream);
+    if (pp2_ok(a)) return launch_pp2<0, 4, true>(a, stream);
     return launch_cfg<true, 0, 256, 256, 4, 2, 1, 1, 4>(a, stream);
   }
   return launch_cfg<false, 0, 128, 128, 2, 2, 2>(a, stream);
@@ -835,7 +592,7 @@ hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream
 hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
   if (bf16) {
     const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
-    if (a.n_feat < 3072 && big_tiles >= 200 && big_ok(a)) return launch_big<1, 64>(a, stream);
+    if (big_tiles >= 200 && pp2_ok(a)) return launch_pp2<1, 1, true>(a, stream);
     if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2, 1, 64>(a, stream);
     return launch_cfg<true, 1, 128, 128, 2, 2, 2, 1, 64>(a, stream);
   }

@@ -39,13 +39,6 @@ constexpr int kRowB = 64;  // bytes of K per staged row
 
 __device__ __forceinline__ uint32_t skey(uint32_t r) { return ((r >> 1) ^ (r >> 3)) & 3u; }
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  // vmcnt in bits [3:0] and [15:14]; expcnt (7) and lgkmcnt (15) not waited on
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
 // wait until at most `ahead` slabs of kPer instructions each remain in flight
 template <int kPer, int kMaxAhead>
 __device__ __forceinline__ void wait_slabs(int ahead) {
