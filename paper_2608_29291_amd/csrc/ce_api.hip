@@ -119,6 +119,12 @@ FfnGemmArgs down_args(const ce_ffn_w* w, const ce_batch* b, const char* act, con
   return a;
 }
 
+// Split-K scratch of the down GEMM (present when the layout reserved it).
+void set_down_split(FfnGemmArgs& a, void* ws, const WsLayout& L) {
+  a.part = L.down_part ? at<float>(ws, L.down_part) : nullptr;
+  a.tile_cnt = L.down_cnt ? at<int32_t>(ws, L.down_cnt) : nullptr;
+}
+
 // Shared argument checks of the staged FFN calls; on success fills the
 // MoT grouping (launching the group kernel when there are two weight sets).
 int ffn_prologue(const ce_batch* batch, const void* in, const int32_t* kept_idx,
@@ -128,7 +134,7 @@ int ffn_prologue(const ce_batch* batch, const void* in, const int32_t* kept_idx,
   CE_CHECK(check_ffn(w));
   if (!kept_offsets) return CE_ERR_INVALID_ARG;
   if (batch->kept_capacity > 0 && (!in || !kept_idx || !out)) return CE_ERR_INVALID_ARG;
-  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d_ff,
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d, w->d_ff,
                                elem_size(w->dtype));
   CE_CHECK(check_ws(ws, ws_bytes, L.total));
   *grp = nullptr;
@@ -160,7 +166,7 @@ int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w, fl
   CE_CHECK(check_batch(batch, w != nullptr && w->r_exp > 0));
   CE_CHECK(check_scorer(w));
   if (batch->T > 0 && (!hidden || !logits)) return CE_ERR_INVALID_ARG;
-  const WsLayout L = ws_layout(CE_WS_SCORE, batch->B, batch->T, batch->kept_capacity, 0, 4);
+  const WsLayout L = ws_layout(CE_WS_SCORE, batch->B, batch->T, batch->kept_capacity, 0, 0, 4);
   CE_CHECK(check_ws(ws, ws_bytes, L.total));
   if (batch->T == 0) return CE_OK;
   const ScoreArgs a = make_score_args(batch, hidden, w, logits, probs);
@@ -180,7 +186,7 @@ int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidd
     if (batch->T > 0 && !hidden) return CE_ERR_INVALID_ARG;
   }
   const int elem = compact ? elem_size(dtype) : 4;
-  const WsLayout L = ws_layout(CE_WS_TOPK, batch->B, batch->T, batch->kept_capacity, 0, elem);
+  const WsLayout L = ws_layout(CE_WS_TOPK, batch->B, batch->T, batch->kept_capacity, 0, 0, elem);
   CE_CHECK(check_ws(ws, ws_bytes, L.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* info = at<int32_t>(ws, L.seq_info);
@@ -223,9 +229,12 @@ int ce_ffn_down(const ce_batch* batch, const void* act, const int32_t* kept_idx,
   int32_t *grp, *n0;
   CE_CHECK(ffn_prologue(batch, act, kept_idx, kept_offsets, w, ffn_out, ws, ws_bytes, s, &grp, &n0));
   if (batch->kept_capacity == 0) return CE_OK;
-  const FfnGemmArgs dn = down_args(w, batch, static_cast<const char*>(act), grp,
-                                   static_cast<char*>(ffn_out), grp, nullptr, nullptr,
-                                   kept_offsets + batch->B, n0);
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d, w->d_ff,
+                               elem_size(w->dtype));
+  FfnGemmArgs dn = down_args(w, batch, static_cast<const char*>(act), grp,
+                             static_cast<char*>(ffn_out), grp, nullptr, nullptr,
+                             kept_offsets + batch->B, n0);
+  set_down_split(dn, ws, L);
   CE_TRY(launch_ffn_down(dn, w->dtype == CE_BF16, s));
   return CE_OK;
 }
@@ -238,7 +247,7 @@ int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kep
   CE_CHECK(ffn_prologue(batch, compact, kept_idx, kept_offsets, w, ffn_out, ws, ws_bytes, s, &grp,
                         &n0));
   if (batch->kept_capacity == 0) return CE_OK;
-  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d_ff,
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d, w->d_ff,
                                elem_size(w->dtype));
   const bool bf16 = w->dtype == CE_BF16;
   const int32_t* kt = kept_offsets + batch->B;
@@ -247,8 +256,9 @@ int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kep
   const FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr, act,
                                     nullptr, kt, n0);
   CE_TRY(launch_ffn_gateup(g, bf16, s));
-  const FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr,
-                                   nullptr, kt, n0);
+  FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr,
+                             nullptr, kt, n0);
+  set_down_split(dn, ws, L);
   CE_TRY(launch_ffn_down(dn, bf16, s));
   return CE_OK;
 }
@@ -282,7 +292,7 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   if (scorer->d != ffn->d || scorer->dtype != ffn->dtype) return CE_ERR_INVALID_ARG;
   if (batch->T > 0 && (!hidden_in || !hidden_out)) return CE_ERR_INVALID_ARG;
   const int elem = elem_size(ffn->dtype);
-  const WsLayout L = ws_layout(CE_WS_BLOCK, batch->B, batch->T, batch->kept_capacity, ffn->d_ff, elem);
+  const WsLayout L = ws_layout(CE_WS_BLOCK, batch->B, batch->T, batch->kept_capacity, ffn->d, ffn->d_ff, elem);
   CE_CHECK(check_ws(ws, ws_bytes, L.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool bf16 = ffn->dtype == CE_BF16;
@@ -331,8 +341,9 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                                     act, nullptr, kt, n0);
   CE_TRY(launch_ffn_gateup(g, bf16, s));
   // 5. down projection + residual, scattered straight into the token rows
-  const FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
-                                   kept_idx, static_cast<const char*>(hidden_in), kt, n0);
+  FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
+                             kept_idx, static_cast<const char*>(hidden_in), kt, n0);
+  set_down_split(dn, ws, L);
   CE_TRY(launch_ffn_down(dn, bf16, s));
   return CE_OK;
 }

@@ -29,6 +29,7 @@
 
 #include "ce_device.hpp"
 #include "ce_launch.hpp"
+#include "ce_host.hpp"
 
 namespace ce {
 
@@ -303,7 +304,7 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
 // phases of a superslab so the DMA writes into LDS do not bunch up. Rows are
 // 128 bytes, chunk c of row r stored at chunk c ^ (r & 7), which keeps the
 // 32-row fragment reads free of bank conflicts.
-template <int kMode, int kGroup, bool kPrio>
+template <int kMode, int kGroup, bool kPrio, int kSplit>
 __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) void ffn_gemm_pp2_kernel(
     FfnGemmArgs a, int n_tt, int n_ft) {
   constexpr int kWR = 256, kTR = 256;
@@ -322,10 +323,13 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int wt = wave >> 1;
   const bool late = wave >= 4;  // group B
 
-  const int total = n_tt * n_ft;
+  static_assert(kSplit == 1 || kSplit == 2, "two K halves at most (their sum is order-free)");
+  const int total = n_tt * n_ft * kSplit;
   const int per = (total + kXcds - 1) / kXcds;
-  const int w = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
-  if (w >= total) return;
+  const int wk = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
+  if (wk >= total) return;
+  const int w = wk / kSplit;   // tile; both K halves of a tile are adjacent in the XCD order
+  const int kz = wk - w * kSplit;
   const int grp = w / (kGroup * n_tt);
   const int rem = w - grp * (kGroup * n_tt);
   const int gsz = min(kGroup, n_ft - grp * kGroup);
@@ -423,13 +427,17 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const uint32_t rowb = (uint32_t)((wt * 64 + lrow) * kRow);
   u32x4_t fa[2][kMW], fb[2][kMT];
 
-  const int ns = a.k_bytes / kRow;  // superslabs (>= 3, checked by the launcher)
+  // superslabs [s0, ns) of K: all of them, or one half when K is split
+  // (>= 3 per range, checked by the launcher)
+  const int ns_all = a.k_bytes / kRow;
+  const int s0 = ns_all * kz / kSplit;
+  const int ns = ns_all * (kz + 1) / kSplit;
   if (is_w) {
-    dma(0, 0, I0{});  // weights: superslab 0
+    dma(s0, 0, I0{});  // weights: first superslab
     wait_vmcnt<0>();
   } else {
-    dma(0, 0, I0{});  // tokens: superslabs 0 and 1
-    dma(1, 1, I0{});
+    dma(s0, 0, I0{});  // tokens: first two superslabs
+    dma(s0 + 1, 1, I0{});
     wait_vmcnt<8>();
   }
   lds_barrier();  // superslab 0 is in LDS
@@ -482,11 +490,59 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  for (int s = 0; s < ns; ++s) {
+  for (int s = s0; s < ns; ++s) {
     half(s, I0{});
     half(s, I1{});
     wb ^= 1;
     tb = tb == 2 ? 0 : tb + 1;
+  }
+
+  if constexpr (kSplit == 2) {
+    if (!late) lds_barrier();  // both groups in step from here on
+    // The two K halves of a tile meet through the workspace: each writes its
+    // sums, then bumps the tile's arrival counter; the second to arrive adds
+    // the other's sums and finishes the tile. Nobody waits on anybody. The
+    // sums move with device-coherent (sc1) stores and loads, so no L2
+    // write-back or invalidation is needed; the counter is an agent-scope
+    // atomic issued after this workgroup's stores have completed.
+    constexpr int kSC1 = 16;  // cache-policy operand: sc1
+    const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.part + (int64_t)w * 2 * (256 * 256), 2 * 256 * 256 * 4);
+    const uint32_t mine = (uint32_t)kz * (256 * 256 * 4);
+    const uint32_t other = (uint32_t)(kz ^ 1) * (256 * 256 * 4);
+    // register order: per lane 32 float4, one store instruction = 1 KB contiguous
+#pragma unroll
+    for (int i = 0; i < kMW; ++i)
+#pragma unroll
+      for (int j = 0; j < kMT; ++j)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+          const uint32_t o = (uint32_t)((((wave * 32 + (i * kMT + j) * 4 + v4) * 64) + lane) * 16);
+          const u32x4_t x = {__float_as_uint(acc[i][j][4 * v4]), __float_as_uint(acc[i][j][4 * v4 + 1]),
+                             __float_as_uint(acc[i][j][4 * v4 + 2]), __float_as_uint(acc[i][j][4 * v4 + 3])};
+          __builtin_amdgcn_raw_buffer_store_b128(x, prs, (int)(mine + o), 0, kSC1);
+        }
+    wait_vmcnt<0>();  // this wave's sums have reached the coherence point
+    __syncthreads();
+    int* const arrived = reinterpret_cast<int*>(smem);  // the rings are no longer read
+    if (tid == 0)
+      arrived[0] = __hip_atomic_fetch_add(a.tile_cnt + w, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (arrived[0] == 0) return;  // first half done: the other finishes the tile
+#pragma unroll
+    for (int i = 0; i < kMW; ++i)
+#pragma unroll
+      for (int j = 0; j < kMT; ++j)
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+          const uint32_t o = (uint32_t)((((wave * 32 + (i * kMT + j) * 4 + v4) * 64) + lane) * 16);
+          const u32x4_t y = __builtin_bit_cast(
+              u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, (int)(other + o), 0, kSC1));
+          // two addends: the sum does not depend on which half came last
+          acc[i][j][4 * v4] += __uint_as_float(y.x);
+          acc[i][j][4 * v4 + 1] += __uint_as_float(y.y);
+          acc[i][j][4 * v4 + 2] += __uint_as_float(y.z);
+          acc[i][j][4 * v4 + 3] += __uint_as_float(y.w);
+        }
   }
 
 #pragma unroll
@@ -531,19 +587,31 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       }
     }
   }
-  if (!late) lds_barrier();  // matches group B's extra barrier at the start
+  if (kSplit == 1 && !late) lds_barrier();  // matches group B's extra barrier at the start
 }
 
-template <int kMode, int kGroup, bool kPrio>
+__global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
+}
+
+template <int kMode, int kGroup, bool kPrio, int kSplit = 1>
 hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream) {
   constexpr int kFTile = (kMode == 0) ? 128 : 256;
   const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
   const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
   if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
-  const int total = n_tt * n_ft;
+  if (kSplit > 1) {
+    if (!a.part || !a.tile_cnt) return hipErrorInvalidValue;
+    // arrival counters start at zero (a fill kernel: no memset nodes in a
+    // captured stream)
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(256), 0, stream, a.tile_cnt, n_tt * n_ft);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int total = n_tt * n_ft * kSplit;
   const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
-  hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio>), dim3(grid), dim3(512), 0, stream, a,
-                     n_tt, n_ft);
+  hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, kSplit>), dim3(grid), dim3(512), 0,
+                     stream, a, n_tt, n_ft);
   return hipGetLastError();
 }
 
@@ -593,6 +661,11 @@ hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream) 
   if (bf16) {
     const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
     if (big_tiles >= 200 && pp2_ok(a)) return launch_pp2<1, 1, true>(a, stream);
+    // too few tiles to fill the chip: two K halves per tile, when the
+    // workspace holds their partial sums
+    if (a.part && a.tile_cnt && pp2_ok(a) &&
+        down_split_tiles(a.cap, a.n_feat, a.k_bytes / 2, a.n_sets, 2) == big_tiles)
+      return launch_pp2<1, 1, true, 2>(a, stream);
     if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2, 1, 64>(a, stream);
     return launch_cfg<true, 1, 128, 128, 2, 2, 2, 1, 64>(a, stream);
   }

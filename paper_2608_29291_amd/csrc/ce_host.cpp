@@ -15,7 +15,19 @@ int elem_size(int dtype) {
   return 0;
 }
 
-WsLayout ws_layout(int which, int B, int T, int cap, int d_ff, int elem) {
+int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem) {
+  if (elem != 2 || cap <= 0 || d <= 0 || d_ff <= 0 || n_sets < 1) return 0;
+  const int64_t k_bytes = (int64_t)d_ff * 2;
+  const int64_t lim = (int64_t)1 << 31;
+  // the ping-pong kernel's limits: whole 128-byte K superslabs, at least 3 of
+  // them per K half, 32-bit buffer offsets
+  if (k_bytes % 128 != 0 || k_bytes < 6 * 128) return 0;
+  if ((int64_t)cap * k_bytes >= lim || (int64_t)d * k_bytes >= lim) return 0;
+  const int64_t tiles = (int64_t)((cap + 255) / 256 + n_sets - 1) * ((d + 255) / 256);
+  return tiles <= kSplitMaxTiles ? (int)tiles : 0;
+}
+
+WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) {
   WsLayout L;
   memset(&L, 0, sizeof(L));
   size_t off = 0;
@@ -41,6 +53,15 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d_ff, int elem) {
     L.grp_rows = take(sC * 4);
     L.grp_n0 = take(4);
     L.act = take(sC * sF * (size_t)elem);
+    int tiles = 0;
+    for (int n_sets = 1; n_sets <= 2; ++n_sets) {
+      const int t = down_split_tiles(cap, d, d_ff, n_sets, elem);
+      tiles = t > tiles ? t : tiles;
+    }
+    if (tiles > 0) {
+      L.down_part = take((size_t)tiles * 2 * 256 * 256 * 4);
+      L.down_cnt = take((size_t)tiles * 4);
+    }
   }
   L.total = off;
   return L;
@@ -152,13 +173,12 @@ int64_t ce_kept_count_host(int32_t B, int32_t T, const int32_t* offs, const uint
 }
 
 size_t ce_workspace_size(int which, const ce_batch* batch, int32_t d, int32_t d_ff, int dtype) {
-  (void)d;
   if (!batch || (which != CE_WS_TOPK && which != CE_WS_FFN && which != CE_WS_BLOCK &&
                  which != CE_WS_SCORE))
     return 0;
   const int elem = ce::elem_size(dtype);
   if (!elem) return 0;
-  return ce::ws_layout(which, batch->B, batch->T, batch->kept_capacity, d_ff, elem).total;
+  return ce::ws_layout(which, batch->B, batch->T, batch->kept_capacity, d, d_ff, elem).total;
 }
 
 }  // extern "C"

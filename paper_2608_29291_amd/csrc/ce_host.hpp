@@ -26,10 +26,19 @@ struct WsLayout {
   size_t grp_rows;   // int32 [cap]    (MoT grouping)
   size_t grp_n0;     // int32          (MoT group size)
   size_t act;        // dtype [cap * d_ff] SwiGLU activations
+  size_t down_part;  // float [2 x tiles x 256 x 256] split-K partial sums of the down GEMM
+  size_t down_cnt;   // int32 [tiles] arrival counters of the split-K down GEMM
   size_t total;
 };
 
-WsLayout ws_layout(int which, int B, int T, int cap, int d_ff, int elem);
+WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem);
+
+// The down GEMM (d outputs, contraction d_ff) runs as two K halves when its
+// 256 x 256 tiles are too few to fill the chip; returns that tile count, or 0
+// when the down GEMM is not split. Shared by the launcher and the workspace
+// layout so both agree.
+constexpr int kSplitMaxTiles = 128;
+int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem);
 
 int elem_size(int dtype);  // 2 for bf16, 4 for f32, 0 if unknown
 

@@ -33,6 +33,10 @@ struct FfnGemmArgs {
   int cap;
   const int32_t* n0_ptr;  // rows in the first weight set (MoT), or NULL
   int n_sets;
+  // down GEMM split over two K halves (both NULL: no split): fp32 partial sums
+  // [2 x tiles x 256 x 256] and per-tile arrival counters [tiles]
+  float* part;
+  int32_t* tile_cnt;
 };
 
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream);
