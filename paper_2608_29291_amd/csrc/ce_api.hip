@@ -253,13 +253,15 @@ int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kep
   const int32_t* kt = kept_offsets + batch->B;
   // activations stay in grouped GEMM order inside the workspace
   char* act = at<char>(ws, L.act);
-  const FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr, act,
-                                    nullptr, kt, n0);
-  CE_TRY(launch_ffn_gateup(g, bf16, s));
   FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr,
                              nullptr, kt, n0);
   set_down_split(dn, ws, L);
-  CE_TRY(launch_ffn_down(dn, bf16, s));
+  FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr, act,
+                              nullptr, kt, n0);
+  g.clear_n = ffn_down_split_tiles(dn, bf16);
+  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
+  CE_TRY(launch_ffn_gateup(g, bf16, s));
+  CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
   return CE_OK;
 }
 
@@ -337,14 +339,16 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                         grp, n0, s));
   }
   char* act = at<char>(ws, L.act);
-  const FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx,
-                                    act, nullptr, kt, n0);
-  CE_TRY(launch_ffn_gateup(g, bf16, s));
-  // 5. down projection + residual, scattered straight into the token rows
   FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
                              kept_idx, static_cast<const char*>(hidden_in), kt, n0);
   set_down_split(dn, ws, L);
-  CE_TRY(launch_ffn_down(dn, bf16, s));
+  FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx, act,
+                              nullptr, kt, n0);
+  g.clear_n = ffn_down_split_tiles(dn, bf16);
+  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
+  CE_TRY(launch_ffn_gateup(g, bf16, s));
+  // 5. down projection + residual, scattered straight into the token rows
+  CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
   return CE_OK;
 }
 

@@ -62,6 +62,8 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
   constexpr int kTLoads = kTR / kRowsPerPass;
   static_assert(kWLoads * kRowsPerPass == kWR && kTLoads * kRowsPerPass == kTR, "tile / threads");
   static_assert(kMode == 1 || (kRowsPerPass % 32) == 0 || (32 % kRowsPerPass) == 0, "pass rows");
+  if (a.clear_cnt && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < a.clear_n; i += kThreads) a.clear_cnt[i] = 0;
   constexpr int kStage = (kWR + kTR) * kKB;
 
   __shared__ __attribute__((aligned(16))) char smem[kStages * kStage];
@@ -317,6 +319,8 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   char* const tsm = smem + kWBufs * kSlab;   // token ring
 
   const int tid = threadIdx.x;
+  if (a.clear_cnt && blockIdx.x == 0)
+    for (int i = tid; i < a.clear_n; i += 512) a.clear_cnt[i] = 0;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ww = wave & 1;
@@ -595,18 +599,20 @@ __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, 
 }
 
 template <int kMode, int kGroup, bool kPrio, int kSplit = 1>
-hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream) {
+hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream, bool counters_clear = false) {
   constexpr int kFTile = (kMode == 0) ? 128 : 256;
   const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
   const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
   if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
   if (kSplit > 1) {
     if (!a.part || !a.tile_cnt) return hipErrorInvalidValue;
-    // arrival counters start at zero (a fill kernel: no memset nodes in a
-    // captured stream)
-    hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(256), 0, stream, a.tile_cnt, n_tt * n_ft);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    // arrival counters start at zero: cleared by the preceding gate/up launch,
+    // else by a fill kernel (no memset nodes in a captured stream)
+    if (!counters_clear) {
+      hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(256), 0, stream, a.tile_cnt, n_tt * n_ft);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
   }
   const int total = n_tt * n_ft * kSplit;
   const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
@@ -657,15 +663,21 @@ hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream
   return launch_cfg<false, 0, 128, 128, 2, 2, 2>(a, stream);
 }
 
-hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
+int ffn_down_split_tiles(const FfnGemmArgs& a, bool bf16) {
+  if (!bf16 || !a.part || !a.tile_cnt || !pp2_ok(a)) return 0;
+  const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
+  if (big_tiles >= 200) return 0;
+  const int t = down_split_tiles(a.cap, a.n_feat, a.k_bytes / 2, a.n_sets, 2);
+  return t == big_tiles ? t : 0;
+}
+
+hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear) {
   if (bf16) {
     const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
     if (big_tiles >= 200 && pp2_ok(a)) return launch_pp2<1, 1, true>(a, stream);
     // too few tiles to fill the chip: two K halves per tile, when the
     // workspace holds their partial sums
-    if (a.part && a.tile_cnt && pp2_ok(a) &&
-        down_split_tiles(a.cap, a.n_feat, a.k_bytes / 2, a.n_sets, 2) == big_tiles)
-      return launch_pp2<1, 1, true, 2>(a, stream);
+    if (ffn_down_split_tiles(a, bf16) > 0) return launch_pp2<1, 1, true, 2>(a, stream, counters_clear);
     if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2, 1, 64>(a, stream);
     return launch_cfg<true, 1, 128, 128, 2, 2, 2, 1, 64>(a, stream);
   }

@@ -37,10 +37,19 @@ struct FfnGemmArgs {
   // [2 x tiles x 256 x 256] and per-tile arrival counters [tiles]
   float* part;
   int32_t* tile_cnt;
+  // gate/up only: the following down GEMM's arrival counters, cleared by the
+  // first workgroup (NULL: none), so the down launch needs no fill kernel
+  int32_t* clear_cnt;
+  int clear_n;
 };
 
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream);
-hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream);
+// counters_clear: the arrival counters of a split down GEMM were already
+// cleared on this stream (by the gate/up launch through clear_cnt).
+hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream,
+                           bool counters_clear = false);
+// Number of arrival counters the down GEMM with these arguments uses (0: no split).
+int ffn_down_split_tiles(const FfnGemmArgs& a, bool bf16);
 
 struct ScoreArgs {
   const char* hidden;
