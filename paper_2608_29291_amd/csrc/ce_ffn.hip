@@ -306,14 +306,16 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
 // phases of a superslab so the DMA writes into LDS do not bunch up. Rows are
 // 128 bytes, chunk c of row r stored at chunk c ^ (r & 7), which keeps the
 // 32-row fragment reads free of bank conflicts.
-template <int kMode, int kGroup, bool kPrio, int kSplit>
+template <int kMode, int kGroup, bool kPrio, int kSplit, int kWBufs = 2, bool kSpreadW = true,
+          bool kSpreadT = true>
 __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) void ffn_gemm_pp2_kernel(
     FfnGemmArgs a, int n_tt, int n_ft) {
   constexpr int kWR = 256, kTR = 256;
   constexpr int kMW = 4, kMT = 2;
   constexpr int kRow = 128;                  // bytes of K per staged row
   constexpr int kSlab = 256 * kRow;          // one operand's superslab: 32 KB
-  constexpr int kWBufs = 2, kTBufs = 3;
+  constexpr int kTBufs = 5 - kWBufs;         // 160 KB of LDS in all
+  static_assert(kWBufs >= 2 && kTBufs >= 2, "each ring holds two superslabs at least");
   __shared__ __attribute__((aligned(1024))) char smem[(kWBufs + kTBufs) * kSlab];
   char* const wsm = smem;                    // weight ring
   char* const tsm = smem + kWBufs * kSlab;   // token ring
@@ -436,13 +438,18 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int ns_all = a.k_bytes / kRow;
   const int s0 = ns_all * kz / kSplit;
   const int ns = ns_all * (kz + 1) / kSplit;
+  // each ring starts with all but one of its slots in flight; the first
+  // superslab must have landed
+  constexpr int kBufs0 = kWBufs;  // waves 0-3 (weights)
+  constexpr int kBufs1 = kTBufs;  // waves 4-7 (tokens)
   if (is_w) {
-    dma(s0, 0, I0{});  // weights: first superslab
-    wait_vmcnt<0>();
+#pragma unroll
+    for (int q = 0; q < kBufs0 - 1; ++q) dma(s0 + q, q, I0{});
+    wait_vmcnt<8 * (kBufs0 - 2)>();
   } else {
-    dma(s0, 0, I0{});  // tokens: first two superslabs
-    dma(s0 + 1, 1, I0{});
-    wait_vmcnt<8>();
+#pragma unroll
+    for (int q = 0; q < kBufs1 - 1; ++q) dma(s0 + q, q, I0{});
+    wait_vmcnt<8 * (kBufs1 - 2)>();
   }
   lds_barrier();  // superslab 0 is in LDS
   if (late) lds_barrier();
@@ -461,19 +468,29 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 #pragma unroll
       for (int j = 0; j < kMT; ++j) fb[step][j] = *reinterpret_cast<const u32x4_t*>(sb + rowb + off + 32 * j * kRow);
     }
-    // superslab s - 1 is consumed by both groups: refill its slots, half of
-    // this wave's rows in each phase (weights one superslab ahead, tokens two)
-    using Part = std::integral_constant<int, H + 1>;
-    if (is_w) {
-      if (s + 1 < ns) dma(s + 1, wb ^ 1, Part{});
-    } else {
-      if (s + 2 < ns) dma(s + 2, tb == 0 ? 2 : tb - 1, Part{});
-      // token superslab s + 1 is read next and must have landed; the 8
-      // instructions of superslab s + 2 may stay in flight
-      if (H == 1 && s + 1 < ns) {
-        if (s + 2 >= ns) wait_vmcnt<0>();
-        else wait_vmcnt<8>();
+    // superslab s - 1 is consumed by both groups: its slot receives superslab
+    // s + kBufs - 1, either half of this wave's rows in each phase (spread) or
+    // all of them in the first
+    const int nb = is_w ? kBufs0 : kBufs1;
+    const int slot = is_w ? wb : tb;
+    const int fill = s + nb - 1;
+    const int fslot = slot == 0 ? nb - 1 : slot - 1;
+    if (fill < ns) {
+      if (is_w) {
+        if constexpr (kSpreadW) dma(fill, fslot, std::integral_constant<int, H + 1>{});
+        else if constexpr (H == 0) dma(fill, fslot, I0{});
+      } else {
+        if constexpr (kSpreadT) dma(fill, fslot, std::integral_constant<int, H + 1>{});
+        else if constexpr (H == 0) dma(fill, fslot, I0{});
       }
+    }
+    // superslab s + 1 is read right after the barrier that ends group A's
+    // second compute phase and group B's second memory phase: each wave
+    // waits for its part of it there, leaving the later superslabs in flight
+    const bool more = H == 1 && s + 1 < ns && (min(ns - 1, fill) - (s + 1)) >= 1;
+    if (H == 1 && late && s + 1 < ns) {
+      if (more) wait_vmcnt<8>();
+      else wait_vmcnt<0>();
     }
     __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
@@ -488,17 +505,18 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[step][i], fb[step][j]);
     if constexpr (kPrio) __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_sched_barrier(0);
-    // weight superslab s + 1 (second half issued in this memory phase) must
-    // have landed before the next barrier; the wait sits behind the MFMAs
-    if (H == 1 && is_w && s + 1 < ns) wait_vmcnt<0>();
+    if (H == 1 && !late && s + 1 < ns) {
+      if (more) wait_vmcnt<8>();
+      else wait_vmcnt<0>();
+    }
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
   for (int s = s0; s < ns; ++s) {
     half(s, I0{});
     half(s, I1{});
-    wb ^= 1;
-    tb = tb == 2 ? 0 : tb + 1;
+    wb = wb + 1 == kBufs0 ? 0 : wb + 1;
+    tb = tb + 1 == kBufs1 ? 0 : tb + 1;
   }
 
   if constexpr (kSplit == 2) {
@@ -598,7 +616,8 @@ __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, 
   for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
 }
 
-template <int kMode, int kGroup, bool kPrio, int kSplit = 1>
+template <int kMode, int kGroup, bool kPrio, int kSplit = 1, int kWBufs = 2, bool kSpreadW = true,
+          bool kSpreadT = true>
 hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream, bool counters_clear = false) {
   constexpr int kFTile = (kMode == 0) ? 128 : 256;
   const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
@@ -616,8 +635,8 @@ hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream, bool counters_cl
   }
   const int total = n_tt * n_ft * kSplit;
   const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
-  hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, kSplit>), dim3(grid), dim3(512), 0,
-                     stream, a, n_tt, n_ft);
+  hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, kSplit, kWBufs, kSpreadW, kSpreadT>),
+                     dim3(grid), dim3(512), 0, stream, a, n_tt, n_ft);
   return hipGetLastError();
 }
 
