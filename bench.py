@@ -193,11 +193,10 @@ def main():
     compact = torch.empty((cap, d), dtype=dt, device=dev)
     act = torch.empty((cap, F), dtype=dt, device=dev)
     ffn_out = torch.empty((cap, d), dtype=dt, device=dev)
-    ws_score = ce.alloc_workspace(ce.CE_WS_SCORE, batch, d, F, dtc, device=dev)
     ws_topk = ce.alloc_workspace(ce.CE_WS_TOPK, batch, d, F, dtc, device=dev)
     ws_ffn = ce.alloc_workspace(ce.CE_WS_FFN, batch, d, F, dtc, device=dev)
     h0, sc0, ff0 = sets[0]
-    ce.ce_score(batch, h0, sc0, logits, ws_score, stream=stream)
+    ce.ce_score(batch, h0, sc0, logits, stream=stream)
     ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk, hidden=h0, compact=compact,
                        stream=stream)
     torch.cuda.synchronize()
@@ -215,7 +214,7 @@ def main():
     reps = max(args.steps, 10)
     stages = {
         "score": timed(lambda i: ce.ce_score(batch, sets[i % n_sets][0], sets[i % n_sets][1], logits,
-                                             ws_score, stream=stream), reps),
+                                             stream=stream), reps),
         "topk_compact": timed(lambda i: ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk,
                                                            stream=stream), reps),
         "ffn_gateup": timed(lambda i: ce.ce_ffn_gateup(batch, compact, kept_idx, kept_off,

@@ -75,7 +75,7 @@ enum {
 };
 
 /* ---- workspace kinds ---------------------------------------------------- */
-enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2, CE_WS_SCORE = 3 };
+enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2 };
 
 /*
  * A ragged batch of B sequences packed back to back: sequence b owns tokens
@@ -184,14 +184,13 @@ int ce_workspace_status(const void* ws, uint32_t* status_out, void* stream);
  * Step 1 -- routing logits (section 3.2, Eq. 4) and scores (Eq. 6).
  *   hidden  device dtype [T x d]
  *   logits  device float32 [T] out: Eq. 4 logit; +inf for KEEP tokens
- *   probs   device float32 [T] out or NULL: sigmoid(logit) (Eq. 6)
- *   ws      device workspace of ce_workspace_size(CE_WS_SCORE, ...) bytes
- *           (per-rank-group partial logits, summed in a fixed order)
+ *   probs   device float32 [T] out or NULL: sigmoid(logit) (Eq. 6); 1 for KEEP
+ * Deterministic: every logit is summed in a fixed order.
  * Errors: CE_ERR_INVALID_ARG for null pointers / sizes, CE_ERR_UNSUPPORTED
- * for shapes outside the limits, CE_ERR_WORKSPACE, CE_ERR_HIP on a failed launch.
+ * for shapes outside the limits, CE_ERR_HIP on a failed launch.
  */
 int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w,
-             float* logits, float* probs, void* ws, size_t ws_bytes, void* stream);
+             float* logits, float* probs, void* stream);
 
 /*
  * Steps 2-3 -- per-sequence TopK and packing (section 3.4, Eq. 6).

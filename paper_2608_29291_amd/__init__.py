@@ -26,7 +26,7 @@ CE_OK, CE_ERR_INVALID_ARG, CE_ERR_UNSUPPORTED, CE_ERR_WORKSPACE, CE_ERR_HIP = 0,
 CE_F32, CE_BF16 = 0, 1
 CE_TOK_GEN, CE_TOK_KEEP = 1, 2
 CE_DEV_BAD_OFFSETS, CE_DEV_OVERFLOW = 1, 2
-CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK, CE_WS_SCORE = 0, 1, 2, 3
+CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK = 0, 1, 2
 
 EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
@@ -86,8 +86,7 @@ _sig("ce_num_keep", _i32, [ctypes.c_float, _i32])
 _sig("ce_kept_count_host", ctypes.c_int64, [_i32, _i32, _p, _p, ctypes.c_float])
 _sig("ce_workspace_size", ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(CEBatch), _i32, _i32, ctypes.c_int])
 _sig("ce_workspace_status", ctypes.c_int, [_p, ctypes.POINTER(ctypes.c_uint32), _p])
-_sig("ce_score", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, ctypes.POINTER(CEScorerW), _p, _p, _p,
-                                ctypes.c_size_t, _p])
+_sig("ce_score", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, ctypes.POINTER(CEScorerW), _p, _p, _p])
 _sig("ce_topk_compact", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p,
                                        _p, _p, ctypes.c_size_t, _p])
 _sig("ce_routed_ffn", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
@@ -244,10 +243,10 @@ def ce_workspace_status(ws, stream=None) -> int:
     return int(out.value)
 
 
-def ce_score(batch: Batch, hidden, scorer: Scorer, logits, ws, probs=None, stream=None):
+def ce_score(batch: Batch, hidden, scorer: Scorer, logits, probs=None, stream=None):
     cb, sw = batch.c(), scorer.c()
     _check(lib.ce_score(ctypes.byref(cb), _dev_ptr(hidden), ctypes.byref(sw), _dev_ptr(logits),
-                        _dev_ptr(probs), _dev_ptr(ws), ws.numel(), _stream(stream)), "ce_score")
+                        _dev_ptr(probs), _stream(stream)), "ce_score")
 
 
 def ce_topk_compact(batch: Batch, logits, kept_idx, kept_offsets, ws, token_pos=None,
@@ -306,6 +305,5 @@ __all__ = [
     "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block",
     "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK",
-    "CE_WS_SCORE",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -162,16 +162,13 @@ int ce_workspace_status(const void* ws, uint32_t* status_out, void* stream) {
 }
 
 int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w, float* logits,
-             float* probs, void* ws, size_t ws_bytes, void* stream) {
+             float* probs, void* stream) {
   CE_CHECK(check_batch(batch, w != nullptr && w->r_exp > 0));
   CE_CHECK(check_scorer(w));
   if (batch->T > 0 && (!hidden || !logits)) return CE_ERR_INVALID_ARG;
-  const WsLayout L = ws_layout(CE_WS_SCORE, batch->B, batch->T, batch->kept_capacity, 0, 0, 4);
-  CE_CHECK(check_ws(ws, ws_bytes, L.total));
   if (batch->T == 0) return CE_OK;
   const ScoreArgs a = make_score_args(batch, hidden, w, logits, probs);
-  return hip_status(launch_score(a, w->dtype == CE_BF16, at<float>(ws, L.score_part),
-                                 static_cast<hipStream_t>(stream)));
+  return hip_status(launch_score(a, w->dtype == CE_BF16, static_cast<hipStream_t>(stream)));
 }
 
 int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidden, int dtype,
@@ -307,7 +304,7 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   // 1. routing logits (Eq. 4)
   if (batch->T > 0) {
     const ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
-    CE_TRY(launch_score(sa, bf16, at<float>(ws, L.score_part), s));
+    CE_TRY(launch_score(sa, bf16, s));
   }
   // 2-3. per-sequence TopK + packed index maps (Eq. 6)
   CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));

@@ -17,7 +17,6 @@ constexpr int kMaxSeg = 16;
 // Byte offsets of each workspace region (0 = region absent for that kind).
 struct WsLayout {
   size_t status;     // uint32 status word (+ padding)
-  size_t score_part; // float [16 x T] per-rank-group partial logits
   size_t seq_info;   // int32 [3 * B]
   size_t kept_off;   // int32 [B + 1]  (block path, when the caller passes none)
   size_t kept_idx;   // int32 [cap]    (block path)

@@ -71,8 +71,7 @@ struct ScoreArgs {
   float* logits;
   float* probs;
 };
-// part: device float [(ceil(r_core/64) + ceil(r_exp/64)) x T] partial logits (<= 16 x T)
-hipError_t launch_score(const ScoreArgs& a, bool bf16, float* part, hipStream_t stream);
+hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream);
 
 // Per-sequence summary written by the count kernel: {lo, len, keep_count | bad<<31}.
 hipError_t launch_seq_info(const int32_t* seq_offsets, const uint8_t* flags, int B, int T,

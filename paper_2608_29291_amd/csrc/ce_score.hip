@@ -5,273 +5,314 @@
 //   generation token:     l = c(h) + e_m(h)   e_m(h) = w2e[m] . SiLU(W1e[m] h + b1e[m]) + b2e[m]
 //   m = min(floor(n_seg * t_b), n_seg - 1), t_b the timestep of the token's sequence.
 //
-// Two launches:
-//   score_tile_kernel   grid = token tiles x rank groups. A token tile holds
-//                       kTR consecutive tokens of one sequence (tiles never
-//                       straddle sequences, so the segment m is uniform); a
-//                       rank group holds kRG ranks of the core scorer or of the
-//                       active expansion. The first layer is an MFMA GEMM of the
-//                       group's W1 rows (A operand) against the token rows (B
-//                       operand); its epilogue applies b1, SiLU and the w2 dot
-//                       over the group's ranks in fp32 and writes one partial
-//                       logit per (group, token). Group 0 of the core adds b2c,
-//                       group 0 of the expansion adds b2e[m].
-//   score_finish_kernel sums a token's partials in a fixed order (core groups,
-//                       then expansion groups for generation tokens), writes
-//                       +inf for always-kept tokens, and the sigmoid score.
-// Everything is deterministic (no atomics).
+// One launch. A workgroup scores a tile of up to 32 consecutive tokens of one
+// sequence (tiles never straddle sequences, so the segment m is uniform). The
+// first layer is an MFMA GEMM of the W1 rows (A operand, blocks of 32 ranks:
+// all core blocks, then the active expansion's blocks when the tile holds a
+// generation token) against the 32 token rows (B operand). Wave w owns the
+// rank blocks w, w + 4, ...; its epilogue applies b1, SiLU and the w2 dot in
+// fp32 over its blocks, the four waves' partial sums meet in LDS in a fixed
+// order, and the tile's logits and scores are written directly. Always-kept
+// tokens get +inf / 1 and their hidden rows are never read.
 //
-// K is streamed in 64-byte slabs fetched straight into a ring of LDS buffers
-// by buffer loads with the LDS bit (one 1 KB wave instruction = 16 rows of 64
-// bytes), so kStages - 1 slabs are in flight: the kernel is bound by memory
-// latency and bandwidth, not by math. Rows are stored at chunk c ^ skey(r).
-// Always-kept and out-of-tile token rows are fetched from past the end of the
-// buffer resource, which returns zeros without touching memory, so their
-// hidden states are never read.
+// K is streamed in 128-byte slabs (64 bf16 or 32 fp32 values per row) by
+// buffer loads with the LDS bit: one wave instruction fetches 8 rows x 128
+// bytes, whole cache lines, into LDS. A slab holds the 32 token rows and the
+// tile's weight rows; the ring holds as many slabs as fit in 160 KB (at most
+// 8). Chunk c of row r is stored at chunk c ^ (r & 7), so the 32-row fragment
+// reads are free of bank conflicts.
+#include <type_traits>
+
 #include "ce_device.hpp"
 #include "ce_launch.hpp"
+#include "ce_router.h"
 
 namespace ce {
 
 namespace {
 
-constexpr int kRowB = 64;  // bytes of K per staged row
+constexpr int kTok = 32;         // tokens per tile
+constexpr int kSlabRow = 128;    // bytes of K per staged row
+constexpr int kLds = 152 * 1024;  // ring bytes (the rest of the 160 KB holds the small arrays)
+constexpr int kMaxBlocks = 16;   // (r_core + r_exp) / 32 <= 512 / 32
 
-__device__ __forceinline__ uint32_t skey(uint32_t r) { return ((r >> 1) ^ (r >> 3)) & 3u; }
-
-// wait until at most `ahead` slabs of kPer instructions each remain in flight
-template <int kPer, int kMaxAhead>
-__device__ __forceinline__ void wait_slabs(int ahead) {
-  if (ahead >= 6 && kMaxAhead >= 6) wait_vmcnt<6 * kPer>();
-  else if (ahead == 5 && kMaxAhead >= 5) wait_vmcnt<5 * kPer>();
-  else if (ahead == 4 && kMaxAhead >= 4) wait_vmcnt<4 * kPer>();
-  else if (ahead == 3 && kMaxAhead >= 3) wait_vmcnt<3 * kPer>();
-  else if (ahead == 2 && kMaxAhead >= 2) wait_vmcnt<2 * kPer>();
-  else if (ahead == 1 && kMaxAhead >= 1) wait_vmcnt<1 * kPer>();
-  else wait_vmcnt<0>();
+// s_waitcnt with a run-time vmcnt (0..63): the immediate is chosen by a switch.
+template <int N>
+__device__ __forceinline__ void wait_vm_upto(int n) {
+  if constexpr (N < 63) {
+    if (n > N) {
+      wait_vm_upto<N + 1>(n);
+      return;
+    }
+  }
+  wait_vmcnt<N>();
+}
+__device__ __forceinline__ void wait_vm(int n) {
+  n = n < 0 ? 0 : (n > 63 ? 63 : n);
+  // split first so the chain of compares stays short
+  if (n < 16) wait_vm_upto<0>(n);
+  else if (n < 32) wait_vm_upto<16>(n);
+  else if (n < 48) wait_vm_upto<32>(n);
+  else wait_vm_upto<48>(n);
 }
 
-template <bool kBF16, int kRG, int kTR, int kStages>
-__global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a, int ncg, float* __restrict__ part) {
-  constexpr int kMW = kRG / 64;  // rank blocks per wave (2 x 2 waves)
-  constexpr int kMT = kTR / 64;  // token blocks per wave
-  constexpr int kStage = (kRG + kTR) * kRowB;
-  constexpr int kWPer = kRG / 32;  // DMA instructions per slab, weight waves (0-1)
-  constexpr int kTPer = kTR / 32;  // DMA instructions per slab, token waves (2-3)
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * kStage];
-  __shared__ float red[2][kTR];
+// Locate tile `tile` among the per-sequence tilings: sequence b, tokens [lo, hi).
+// The offsets are read into LDS 256 sequences at a time (one load per thread),
+// then every thread walks them: one memory latency plus a few LDS reads per
+// sequence.
+__device__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo, int& hi) {
+  const int tid = threadIdx.x;
+  int base = 0;  // tiles before the current chunk of sequences
+  b = -1;
+  lo = hi = 0;
+  for (int s0 = 0; s0 < a.B; s0 += 256) {
+    const int cnt = min(256, a.B - s0);
+    if (tid <= cnt) {
+      int o = a.seq_offsets[s0 + tid];
+      sh[tid] = o < 0 ? 0 : (o > a.T ? a.T : o);
+    }
+    __syncthreads();
+    int prev = sh[0];
+    for (int j = 0; j < cnt; ++j) {
+      int se = sh[j + 1];
+      se = se < prev ? prev : se;
+      const int nt = (se - prev + kTok - 1) / kTok;
+      if (b < 0 && tile < base + nt) {
+        b = s0 + j;
+        lo = prev + (tile - base) * kTok;
+        hi = min(lo + kTok, se);
+      }
+      base += nt;
+      prev = se;
+    }
+    __syncthreads();  // sh is refilled by the next chunk
+    if (b >= 0) return;
+  }
+}
+
+template <bool kBF16>
+__global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kLds];
+  __shared__ int sh[260];
+  __shared__ float red[4][2][kTok];
+  __shared__ float ep[4][kMaxBlocks / 4][64];  // per wave and block: b1 (32 ranks), w2 (32 ranks)
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int ww = wave & 1;
-  const int wt = wave >> 1;
 
-  // ---- locate the token tile: sequence b, tokens [lo, hi) ----
-  int tile = blockIdx.x;
-  int b = -1, lo = 0, hi = 0;
-  for (int s = 0; s < a.B; ++s) {
-    int s0 = a.seq_offsets[s], s1 = a.seq_offsets[s + 1];
-    s0 = s0 < 0 ? 0 : (s0 > a.T ? a.T : s0);
-    s1 = s1 < s0 ? s0 : (s1 > a.T ? a.T : s1);
-    const int nt = (s1 - s0 + kTR - 1) / kTR;
-    if (tile < nt) {
-      b = s;
-      lo = s0 + tile * kTR;
-      hi = min(lo + kTR, s1);
-      break;
-    }
-    tile -= nt;
-  }
-  if (b < 0) return;
+  int b, lo, hi;
+  find_tile(a, blockIdx.x, sh, b, lo, hi);
+  // the same for every lane (read from LDS after a barrier): keep them scalar
+  b = __builtin_amdgcn_readfirstlane(b);
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  hi = __builtin_amdgcn_readfirstlane(hi);
+  if (b < 0) return;  // past the last tile
   const int n = hi - lo;
 
-  // ---- token kinds in the tile, rank group ----
+  // ---- token kinds ----
   bool kp = true, gen = false;
   if (tid < n) {
     const uint8_t f = a.flags[lo + tid];
-    kp = (f & 2) != 0;
-    gen = ((f & 1) != 0) && !kp;
+    kp = (f & CE_TOK_KEEP) != 0;
+    gen = ((f & CE_TOK_GEN) != 0) && !kp;
   }
   const int any_scored = __syncthreads_or(!kp);
-  const int any_gen = __syncthreads_or(gen);
-  const int g = blockIdx.y;
-  const bool core = g < ncg;
-  if (!any_scored || (!core && !any_gen)) return;
+  const bool any_gen = __syncthreads_or(gen) && a.r_exp > 0;
+  if (!any_scored) {
+    if (tid < n) {
+      a.logits[lo + tid] = __builtin_inff();
+      if (a.probs) a.probs[lo + tid] = 1.0f;
+    }
+    return;
+  }
   int m = 0;
-  if (!core) {
+  if (any_gen) {
     // exact product in double: floor(n_seg * t) never rounds across a bin edge
     const double mf = floor((double)a.n_seg * (double)a.t[b]);
     m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
+    m = __builtin_amdgcn_readfirstlane(m);  // uniform (one t per sequence): keep it scalar
   }
-  const int r_tot = core ? a.r_core : a.r_exp;
-  const int rank_lo = (core ? g : g - ncg) * kRG;
-  const int nr = min(kRG, r_tot - rank_lo);
-  const char* wbase = core ? a.w1c + (int64_t)rank_lo * a.h_ld
-                           : a.w1e + ((int64_t)m * a.r_exp + rank_lo) * a.h_ld;
+  const int nbc = a.r_core / 32;
+  const int nb = nbc + (any_gen ? a.r_exp / 32 : 0);  // weight blocks of this tile (<= 16)
+  const int stage = (kTok + 32 * nb) * kSlabRow;
+  // two slabs in flight: deeper rings measured slower (the extra LDS DMA in
+  // flight only adds queueing)
+  int nstage = kLds / stage;         // >= 2: a stage is at most (32 + 512) x 128 B = 68 KB
+  nstage = nstage > 3 ? 3 : nstage;
+  const int per_slab = 1 + nb;       // DMA instructions per wave per slab
 
-  // ---- DMA plan: waves 0-1 fetch the group's weight rows, waves 2-3 the token rows ----
-  const bool is_w = wave < 2;
-  const int r16 = lane >> 2;
-  const int pch = lane & 3;
-  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(wbase, (uint32_t)(nr * a.h_ld));
+  // ---- DMA plan: instruction i of a slab covers stage rows 8i .. 8i + 7 and
+  //      belongs to wave i % 4: wave w fetches token rows 8w .. 8w + 7 and rows
+  //      8w .. 8w + 7 of every weight block ----
+  const int r8 = lane >> 3;
+  const int pch = lane & 7;
+  const int trow = 8 * wave + r8;  // this lane's row inside a 32-row block
+  const bool tlive = trow < n && !(a.flags[lo + (trow < n ? trow : 0)] & CE_TOK_KEEP);
+  const uint32_t chunk_off = (uint32_t)((pch ^ (trow & 7)) << 4);
+  // rows that are never scored read past the resource end: zeros, no traffic
+  const uint32_t t_voff = tlive ? (uint32_t)(trow * a.h_ld) + chunk_off : 0x7ffffff0u;
+  const uint32_t w_voff = (uint32_t)(trow * a.h_ld) + chunk_off;
   const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.hidden + (int64_t)lo * a.h_ld, (uint32_t)(n * a.h_ld));
-  constexpr int kPerMax = kWPer > kTPer ? kWPer : kTPer;
-  uint32_t voff[kPerMax];
-#pragma unroll
-  for (int q = 0; q < kPerMax; ++q) {
-    if (is_w) {
-      const int r = (wave & 1) * (kRG / 2) + 16 * q + r16;
-      voff[q] = (uint32_t)(r * a.h_ld) + ((uint32_t)(pch ^ (int)skey((uint32_t)r)) << 4);
-    } else {
-      const int r = (wave & 1) * (kTR / 2) + 16 * q + r16;
-      const bool live = r < n && !(a.flags[lo + (r < n ? r : 0)] & 2);
-      // rows that are never scored read past the resource end: zeros, no traffic
-      voff[q] = live ? (uint32_t)(r * a.h_ld) + ((uint32_t)(pch ^ (int)skey((uint32_t)r)) << 4)
-                     : 0x7ffffff0u;
-    }
-  }
+  const __amdgpu_buffer_rsrc_t crs = make_rsrc(a.w1c, (uint32_t)(a.r_core * a.h_ld));
+  const __amdgpu_buffer_rsrc_t ers =
+      make_rsrc(any_gen ? a.w1e + (int64_t)m * a.r_exp * a.h_ld : a.w1c,
+                (uint32_t)((any_gen ? a.r_exp : a.r_core) * a.h_ld));
+  // The ring base passes through an empty asm: the compiler then cannot tie the
+  // DMA writes to the fragment reads and leaves their ordering to the explicit
+  // vmcnt waits and barriers of the loop, instead of draining every load in
+  // flight before each slab's first LDS read (which would serialize the ring).
+  typedef __attribute__((address_space(3))) char lds_char;
+  lds_char* ring = (lds_char*)smem;
+  asm volatile("" : "+s"(ring));
+  // Each tile walks K starting from its own slab, so the workgroups running
+  // at the same time fetch different weight lines instead of all hitting the
+  // same L2 lines (the sum order is fixed per tile).
+  const int nk_all = a.k_bytes / kSlabRow;
+  const int rot = (int)(blockIdx.x % (unsigned)nk_all);
   auto dma = [&](int kb, int buf) __attribute__((always_inline)) {
-    const int soff = kb * kRowB;
-    if (is_w) {
-      char* region = smem + buf * kStage + (wave & 1) * (kRG / 2) * kRowB;
-#pragma unroll
-      for (int q = 0; q < kWPer; ++q)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            wrs, (__attribute__((address_space(3))) void*)(region + 16 * q * kRowB), 16, (int)voff[q],
-            soff, 0, 0);
-    } else {
-      char* region = smem + buf * kStage + kRG * kRowB + (wave & 1) * (kTR / 2) * kRowB;
-#pragma unroll
-      for (int q = 0; q < kTPer; ++q)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            trs, (__attribute__((address_space(3))) void*)(region + 16 * q * kRowB), 16, (int)voff[q],
-            soff, 0, 0);
-    }
+    lds_char* st = ring + buf * stage;
+    int ks = kb + rot;
+    ks = ks >= nk_all ? ks - nk_all : ks;
+    const int soff = ks * kSlabRow;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, st + 8 * wave * kSlabRow, 16, (int)t_voff, soff, 0, 0);
+    // one loop per weight matrix: each instruction's resource is fixed
+    for (int blk = 0; blk < nbc; ++blk)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(crs, st + (kTok + 32 * blk + 8 * wave) * kSlabRow, 16,
+                                               (int)w_voff, soff + (int)(32 * blk * a.h_ld), 0, 0);
+    for (int blk = nbc; blk < nb; ++blk)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ers, st + (kTok + 32 * blk + 8 * wave) * kSlabRow, 16,
+                                               (int)w_voff, soff + (int)(32 * (blk - nbc) * a.h_ld), 0, 0);
   };
 
-  f32x16_t acc[kMW][kMT];
-#pragma unroll
-  for (int i = 0; i < kMW; ++i)
-#pragma unroll
-    for (int j = 0; j < kMT; ++j) acc[i][j] = f32x16_t{};
+  // ---- main loop: wave w accumulates its blocks w, w + 4, w + 8, w + 12;
+  //      the block count is a compile-time constant of each variant, so a
+  //      slab's fragments are all read before its MFMAs are issued ----
   const int lrow = lane & 31;
   const int lhalf = lane >> 5;
-  const uint32_t rkey = skey((uint32_t)lrow);
-  const uint32_t rowa = (uint32_t)((ww * (kRG / 2) + lrow) * kRowB);
-  const uint32_t rowb = (uint32_t)(kRG * kRowB + (wt * (kTR / 2) + lrow) * kRowB);
-
-  const int nk = a.k_bytes / kRowB;
-  const int pre = min(nk, kStages - 1);
-  for (int s = 0; s < pre; ++s) dma(s, s);
-  int buf = 0;
-  for (int kb = 0; kb < nk; ++kb) {
-    const int ahead = min(nk - 1 - kb, kStages - 2);
-    if (is_w) wait_slabs<kWPer, kStages - 2>(ahead);
-    else wait_slabs<kTPer, kStages - 2>(ahead);
-    lds_barrier();
-    if (kb + kStages - 1 < nk) {
-      int nb = buf + kStages - 1;
-      nb = nb >= kStages ? nb - kStages : nb;
-      dma(kb + kStages - 1, nb);
+  const uint32_t rkey = (uint32_t)(lrow & 7);
+  const int nk = a.k_bytes / kSlabRow;
+  const int nbw = (nb - wave + 3) / 4;  // blocks of this wave (0..4)
+  // the epilogue's b1 / w2 values (lane l < 32: b1 of rank l of the block,
+  // l >= 32: w2 of rank l - 32), loaded now and parked in LDS after the loop
+  float epv[kMaxBlocks / 4];
+#pragma unroll
+  for (int i = 0; i < kMaxBlocks / 4; ++i) {
+    epv[i] = 0.0f;
+    const int blk = wave + 4 * i;
+    if (blk < nb) {
+      const bool core = blk < nbc;
+      const int r = (core ? 32 * blk : 32 * (blk - nbc)) + lrow;
+      const float* b1 = core ? a.b1c : (a.b1e ? a.b1e + m * a.r_exp : nullptr);
+      const float* w2 = core ? a.w2c : a.w2e + m * a.r_exp;
+      epv[i] = lhalf ? w2[r] : (b1 ? b1[r] : 0.0f);
     }
-    const char* sw = smem + buf * kStage;
-#pragma unroll
-    for (int step = 0; step < 2; ++step) {
-      const uint32_t off = (((uint32_t)(2 * step + lhalf)) ^ rkey) << 4;
-      u32x4_t fa[kMW], fb[kMT];
-#pragma unroll
-      for (int i = 0; i < kMW; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(sw + rowa + off + 32 * i * kRowB);
-#pragma unroll
-      for (int j = 0; j < kMT; ++j) fb[j] = *reinterpret_cast<const u32x4_t*>(sw + rowb + off + 32 * j * kRowB);
-#pragma unroll
-      for (int i = 0; i < kMW; ++i)
-#pragma unroll
-        for (int j = 0; j < kMT; ++j) mfma_step<kBF16>(acc[i][j], fa[i], fb[j]);
-    }
-    buf = buf + 1 == kStages ? 0 : buf + 1;
   }
-
-  // ---- epilogue: b1, SiLU, w2 dot over this wave's ranks ----
-  const float* b1 = core ? a.b1c : (a.b1e ? a.b1e + m * a.r_exp : nullptr);
-  const float* w2 = core ? a.w2c : a.w2e + m * a.r_exp;
+  const int pre = min(nk, nstage - 1);
+  for (int s = 0; s < pre; ++s) dma(s, s);
+  float pc = 0.0f, pe = 0.0f;
+  auto run = [&](auto nbw_c) __attribute__((always_inline)) {
+    constexpr int NBW = decltype(nbw_c)::value;
+    // two accumulators per block (even and odd K steps) halve the chain of
+    // dependent MFMAs; they are added before the epilogue
+    f32x16_t acc[NBW > 0 ? NBW : 1][2];
 #pragma unroll
-  for (int j = 0; j < kMT; ++j) {
-    float pj = 0.0f;
+    for (int i = 0; i < NBW; ++i) acc[i][0] = acc[i][1] = f32x16_t{};
+    int buf = 0;
+    for (int kb = 0; kb < nk; ++kb) {
+      // slab kb must have landed; the later slabs already issued may stay in flight
+      const int ahead = min(nk - 1 - kb, nstage - 2);
+      wait_vm(ahead * per_slab);
+      lds_barrier();
+      if constexpr (NBW > 0) {
+        const char* st = smem + buf * stage;
+        u32x4_t fb[4], fa[4][NBW];
 #pragma unroll
-    for (int i = 0; i < kMW; ++i) {
-      const int rb = ww * (kRG / 2) + 32 * i;  // rank block offset inside the group
-      if (rb >= nr) continue;
+        for (int step = 0; step < 4; ++step) {
+          const uint32_t off = (((uint32_t)(2 * step + lhalf)) ^ rkey) << 4;
+          fb[step] = *reinterpret_cast<const u32x4_t*>(st + lrow * kSlabRow + off);
+#pragma unroll
+          for (int i = 0; i < NBW; ++i)
+            fa[step][i] = *reinterpret_cast<const u32x4_t*>(
+                st + (kTok + 32 * (wave + 4 * i) + lrow) * kSlabRow + off);
+        }
+#pragma unroll
+        for (int step = 0; step < 4; ++step)
+#pragma unroll
+          for (int i = 0; i < NBW; ++i) mfma_step<kBF16>(acc[i][step & 1], fa[step][i], fb[step]);
+      }
+      // every wave is past slab kb - 1 (the barrier above): its buffer receives
+      // slab kb + nstage - 1. Issued after this slab's fragment reads, so no
+      // LDS read follows a DMA without a barrier in between.
+      if (kb + nstage - 1 < nk) {
+        int nbuf = buf + nstage - 1;
+        nbuf = nbuf >= nstage ? nbuf - nstage : nbuf;
+        dma(kb + nstage - 1, nbuf);
+      }
+      buf = buf + 1 == nstage ? 0 : buf + 1;
+    }
+    // ---- epilogue: b1, SiLU, w2 over this wave's blocks; core and expansion kept apart ----
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) ep[wave][i][lane] = epv[i];
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) {
+      const int blk = wave + 4 * i;
+      const bool hb = (blk >= nbc ? a.b1e : a.b1c) != nullptr;
+      float p = 0.0f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int r = rank_lo + rb + 8 * (v >> 2) + 4 * lhalf + (v & 3);
-        float z = acc[i][j][v];
-        if (b1) z += b1[r];
-        pj += w2[r] * silu_f32(z);
+        const int r = 8 * (v >> 2) + 4 * lhalf + (v & 3);  // rank inside the block
+        float z = acc[i][0][v] + acc[i][1][v];
+        if (hb) z += ep[wave][i][r];
+        p += ep[wave][i][32 + r] * silu_f32(z);
       }
+      if (blk < nbc) pc += p;
+      else pe += p;
     }
-    pj += __shfl_xor(pj, 32);
-    if (lhalf == 0) red[ww][wt * (kTR / 2) + 32 * j + lrow] = pj;
+  };
+  switch (nbw) {
+    case 0: run(std::integral_constant<int, 0>{}); break;
+    case 1: run(std::integral_constant<int, 1>{}); break;
+    case 2: run(std::integral_constant<int, 2>{}); break;
+    case 3: run(std::integral_constant<int, 3>{}); break;
+    default: run(std::integral_constant<int, 4>{}); break;
+  }
+  pc += __shfl_xor(pc, 32);
+  pe += __shfl_xor(pe, 32);
+  if (lhalf == 0) {
+    red[wave][0][lrow] = pc;
+    red[wave][1][lrow] = pe;
   }
   __syncthreads();
   if (tid < n) {
-    float p = red[0][tid] + red[1][tid];
-    if (rank_lo == 0) {
-      if (core) p += a.b2c;
-      else if (a.b2e) p += a.b2e[m];
+    const int i = lo + tid;
+    const uint8_t f = a.flags[i];
+    float l;
+    if (f & CE_TOK_KEEP) {
+      l = __builtin_inff();
+    } else {
+      l = ((red[0][0][tid] + red[1][0][tid]) + (red[2][0][tid] + red[3][0][tid])) + a.b2c;
+      if ((f & CE_TOK_GEN) && a.r_exp > 0) {
+        float e = (red[0][1][tid] + red[1][1][tid]) + (red[2][1][tid] + red[3][1][tid]);
+        if (a.b2e) e += a.b2e[m];
+        l += e;
+      }
     }
-    part[(int64_t)g * a.T + lo + tid] = p;
+    a.logits[i] = l;
+    if (a.probs) a.probs[i] = (f & CE_TOK_KEEP) ? 1.0f : 1.0f / (1.0f + expf(-l));
   }
-}
-
-__global__ __launch_bounds__(256) void score_finish_kernel(ScoreArgs a, int ncg, int neg,
-                                                           const float* __restrict__ part) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= a.T) return;
-  const uint8_t f = a.flags[i];
-  float l;
-  if (f & 2) {
-    l = __builtin_inff();
-  } else {
-    l = 0.0f;
-    for (int g = 0; g < ncg; ++g) l += part[(int64_t)g * a.T + i];
-    if ((f & 1) && a.r_exp > 0) {
-      float e = 0.0f;
-      for (int g = 0; g < neg; ++g) e += part[(int64_t)(ncg + g) * a.T + i];
-      l += e;
-    }
-  }
-  a.logits[i] = l;
-  if (a.probs) a.probs[i] = (f & 2) ? 1.0f : 1.0f / (1.0f + expf(-l));
-}
-
-template <bool kBF16, int kRG, int kTR, int kStages>
-hipError_t launch_tiles(const ScoreArgs& a, float* part, hipStream_t stream) {
-  const int ncg = (a.r_core + kRG - 1) / kRG;
-  const int neg = (a.r_exp + kRG - 1) / kRG;
-  const int tiles = (a.T + kTR - 1) / kTR + a.B;
-  hipLaunchKernelGGL((score_tile_kernel<kBF16, kRG, kTR, kStages>), dim3(tiles, ncg + neg), dim3(256), 0,
-                     stream, a, ncg, part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(score_finish_kernel, dim3((a.T + 255) / 256), dim3(256), 0, stream, a, ncg, neg,
-                     (const float*)part);
-  return hipGetLastError();
 }
 
 }  // namespace
 
-// Tile choice: 64 ranks x 64 tokens keeps ~270+ workgroups busy on the
-// narrow (d <= 2048) workloads; 128 x 128 halves the weight and token re-reads
-// for wide ones (re-read traffic = T*d*(R/kRG) + R*d*(T/kTR)).
-hipError_t launch_score(const ScoreArgs& a, bool bf16, float* part, hipStream_t stream) {
+hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;
-  const bool wide = a.k_bytes >= 4096;
-  if (bf16) {
-    if (wide) return launch_tiles<true, 128, 128, 6>(a, part, stream);
-    return launch_tiles<true, 64, 64, 8>(a, part, stream);
-  }
-  return launch_tiles<false, 64, 64, 8>(a, part, stream);
+  const int tiles = (a.T + kTok - 1) / kTok + a.B;  // >= the per-sequence tile count
+  if (bf16)
+    hipLaunchKernelGGL(score_kernel<true>, dim3(tiles), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(score_kernel<false>, dim3(tiles), dim3(256), 0, stream, a);
+  return hipGetLastError();
 }
 
 }  // namespace ce

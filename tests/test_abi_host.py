@@ -19,7 +19,6 @@ HEADER = os.path.join(ROOT, "include", "ce_router.h")
 ce = pytest.importorskip("paper_2608_29291_amd")
 
 FAKE = 0x10000  # never dereferenced: validation fails first
-WS_FAKE = 0x20000  # 256-byte aligned fake workspace address
 
 
 def declared_functions():
@@ -89,10 +88,9 @@ def _ffn(d=256, F=512, n_sets=1, dtype=ce.CE_BF16):
     return w
 
 
-def score(b, w, hidden=FAKE, logits=FAKE, ws=WS_FAKE, ws_bytes=1 << 30):
+def score(b, w, hidden=FAKE, logits=FAKE):
     return ce.lib.ce_score(ctypes.byref(b) if b is not None else None, hidden,
-                           ctypes.byref(w) if w is not None else None, logits, None, ws, ws_bytes,
-                           None)
+                           ctypes.byref(w) if w is not None else None, logits, None, None)
 
 
 @pytest.mark.parametrize("mut,code", [
@@ -125,15 +123,6 @@ def test_score_null_buffers():
     w = _scorer()
     w.w1_exp = None
     assert score(_batch(), w) == ce.CE_ERR_INVALID_ARG
-
-
-def test_score_workspace():
-    b = _batch()
-    need = ce.lib.ce_workspace_size(ce.CE_WS_SCORE, ctypes.byref(b), 256, 512, ce.CE_BF16)
-    assert need >= 16 * b.T * 4
-    assert score(b, _scorer(), ws=None) == ce.CE_ERR_WORKSPACE
-    assert score(b, _scorer(), ws_bytes=need - 1) == ce.CE_ERR_WORKSPACE
-    assert score(b, _scorer(), ws=WS_FAKE + 4) == ce.CE_ERR_WORKSPACE
 
 
 def test_topk_validation_and_workspace():

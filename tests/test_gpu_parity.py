@@ -44,7 +44,7 @@ def test_score(G, kind, dtype):
     logits = torch.full((wl.T,), float("nan"), device="cuda")
     probs = torch.full((wl.T,), float("nan"), device="cuda")
     import paper_2608_29291_amd as ce
-    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits, dw.ws(ce.CE_WS_SCORE), probs)
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits, probs)
     torch.cuda.synchronize()
     l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
     err = G.logit_err(G.host(logits), l64)
@@ -72,7 +72,7 @@ def test_score_rank_shapes(G, rank):
     if r_e == 0:
         dw.scorer.b2_exp = None
     logits = torch.empty(wl.T, device="cuda")
-    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits, dw.ws(ce.CE_WS_SCORE))
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits)
     torch.cuda.synchronize()
     l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
     assert G.logit_err(G.host(logits), l64) <= 1e-4
@@ -87,7 +87,7 @@ def test_score_segments_follow_t(G):
                        dtype="bf16", seed=5, t_values=ts, biases=True)
     dw = G.DevWorkload(wl)
     logits = torch.empty(wl.T, device="cuda")
-    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits, dw.ws(ce.CE_WS_SCORE))
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits)
     torch.cuda.synchronize()
     l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
     assert G.logit_err(G.host(logits), l64) <= 1e-4
