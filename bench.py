@@ -92,6 +92,32 @@ def cpu_baseline(wl, n_seq: int, min_seconds: float = 10.0, max_reps: int = 50):
                       f"({os.cpu_count()} logical CPUs visible, BLAS threads {threads})"}
 
 
+def time_drop_stability(ce, stream, reps: int) -> dict:
+    """Drop-set Jaccard / RDA between two timesteps (section 3.4, Eq. 10-11) on
+    the Show-o2 generation workload's shape: 4 x [4096 latent, 128 text]."""
+    import torch
+    from ce_workloads import TOK_GEN, TOK_KEEP, make_drop_pair
+    offs, flags, tp_t, tp_r = make_drop_pair([[(4096, TOK_GEN), (128, TOK_KEEP)]] * 4, 0.5, 0.5, 0.05, 1)
+    up = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to("cuda")
+    B, T = len(offs) - 1, int(offs[-1])
+    batch = ce.Batch(up(offs), up(flags), up(np.zeros(B, np.float32)), 0.5, 0)
+    a, b = up(tp_t), up(tp_r)
+    jac, jr, rda = (torch.empty(B, device="cuda") for _ in range(3))
+    for _ in range(3):
+        ce.ce_drop_stability(batch, a, b, jac, jr, rda, stream=stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        ce.ce_drop_stability(batch, a, b, jac, jr, rda, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    return {"drop_stability": {"us_per_call": round(us, 2), "sequences": B, "tokens": T,
+                               "bytes_per_call": 9 * T, "bound": "latency",
+                               "workload": "showo2-generation shape, adjacent steps"}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -258,6 +284,7 @@ def main():
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
         "roofline": roofline,
     }
+    result["ucs_signals"] = time_drop_stability(ce, stream, max(args.steps, 10))
     if not args.no_cpu_baseline:
         n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
         log(f"oracle CPU baseline on {n_seq} sequence(s)...")

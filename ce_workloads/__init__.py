@@ -356,3 +356,38 @@ def small_workload(kind: str, seed: int = 0, dtype: str = "bf16", **kw) -> Workl
 def kept_capacity_upper(flags: np.ndarray, seq_offsets: np.ndarray) -> int:
     """A capacity that always suffices: every token of every sequence."""
     return int(seq_offsets[-1])
+
+
+def make_drop_pair(segments, keep_t: float, keep_ref: float, noise: float, seed: int):
+    """Two timesteps' packed positions over one batch layout, for the drop-set
+    stability signals: each routable token draws a random score u; timestep t
+    keeps the ceil(keep_t * R) highest u of its sequence, the reference keeps
+    the ceil(keep_ref * R) highest of u + noise * v (v another draw), so the two
+    drop sets overlap more the smaller the noise. The kept counts are
+    round(keep * R) (a generator choice, not the method's rule). Always-kept
+    tokens get a position at both timesteps. Returns (seq_offsets, flags, token_pos_t,
+    token_pos_ref); positions are plain running counters (only their sign is
+    read downstream).
+    """
+    offs, flags = build_layout(segments)
+    rng = np.random.default_rng(seed)
+    T = int(offs[-1])
+    u = rng.random(T)
+    v = rng.random(T)
+    tps = []
+    for keep, score in ((keep_t, u), (keep_ref, u + noise * v)):
+        tp = np.full(T, -1, np.int32)
+        pos = 0
+        for b in range(len(offs) - 1):
+            lo, hi = int(offs[b]), int(offs[b + 1])
+            idx = np.arange(lo, hi)
+            keep_tok = (flags[lo:hi] & TOK_KEEP) != 0
+            routable = idx[~keep_tok]
+            n_keep = int(round(keep * len(routable)))  # any count will do for these signals
+            chosen = set(routable[np.argsort(-score[routable], kind="stable")[:n_keep]].tolist())
+            for i in idx:
+                if keep_tok[i - lo] or i in chosen:
+                    tp[i] = pos
+                    pos += 1
+        tps.append(tp)
+    return offs, flags, tps[0], tps[1]

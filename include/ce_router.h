@@ -268,6 +268,30 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                     int32_t* kept_idx_out, int32_t* kept_offsets_out, void* ws,
                     size_t ws_bytes, void* stream);
 
+/*
+ * Drop-set stability between two timesteps (section 3.4, UCS operators (3)
+ * diffusion-head cache reuse and (4) denoising-step early exit; Eq. 10-11).
+ * For each sequence b the drop set D of a timestep is its routable tokens
+ * (CE_TOK_KEEP clear) whose packed position is negative (dropped):
+ *   jaccard[b] = |D_t n D_ref| / |D_t u D_ref|            (1 when both are empty)
+ *   j_rand[b]  = expected Jaccard of two independent, uniformly random subsets
+ *                of the sequence's routable tokens with the same two sizes
+ *                (hypergeometric overlap, evaluated in fp64)
+ *   rda[b]     = (jaccard - j_rand) / (1 - j_rand)       (1 when j_rand = 1)
+ * The early-exit signal is the pair (t, t - 1); cache reuse compares with the
+ * timestep of the last refresh. Thresholds and the decisions they drive stay
+ * with the caller.
+ *   token_pos_t, token_pos_ref  device int32 [T]: ce_topk_compact's token_pos
+ *                               at the two timesteps (same batch layout)
+ *   jaccard                     device float32 [B] out
+ *   j_rand, rda                 device float32 [B] out, or NULL
+ * Deterministic. Errors: CE_ERR_INVALID_ARG for null pointers / sizes,
+ * CE_ERR_HIP on a failed launch.
+ */
+int ce_drop_stability(const ce_batch* batch, const int32_t* token_pos_t,
+                      const int32_t* token_pos_ref, float* jaccard, float* j_rand, float* rda,
+                      void* stream);
+
 #ifdef __cplusplus
 }
 #endif

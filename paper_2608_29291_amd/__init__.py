@@ -11,6 +11,7 @@ this package fails loudly when the library has not been built.
     ce_routed_ffn        SwiGLU FFN on the packed rows
     ce_scatter_residual  residual merge; dropped rows bypass
     ce_routed_block      all of the above, fused
+    ce_drop_stability    drop-set Jaccard / RDA between two timesteps (Eq. 10-11)
 """
 from __future__ import annotations
 
@@ -31,7 +32,7 @@ CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK = 0, 1, 2
 EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
-    "ce_ffn_down", "ce_scatter_residual", "ce_routed_block",
+    "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
 ]
 
 
@@ -99,6 +100,7 @@ _sig("ce_scatter_residual", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, 
                                            _p, _p])
 _sig("ce_routed_block", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.POINTER(CEScorerW),
                                        ctypes.POINTER(CEFFNW), _p, _p, _p, _p, ctypes.c_size_t, _p])
+_sig("ce_drop_stability", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, _p, _p, _p])
 
 
 # ----------------------------------------------------------------------------
@@ -299,11 +301,19 @@ def ce_routed_block(batch: Batch, hidden_in, hidden_out, scorer: Scorer, ffn: FF
                                ws.numel(), _stream(stream)), "ce_routed_block")
 
 
+def ce_drop_stability(batch: Batch, token_pos_t, token_pos_ref, jaccard, j_rand=None, rda=None,
+                      stream=None):
+    cb = batch.c()
+    _check(lib.ce_drop_stability(ctypes.byref(cb), _dev_ptr(token_pos_t), _dev_ptr(token_pos_ref),
+                                 _dev_ptr(jaccard), _dev_ptr(j_rand), _dev_ptr(rda), _stream(stream)),
+           "ce_drop_stability")
+
+
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
     "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
-    "ce_scatter_residual", "ce_routed_block",
+    "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

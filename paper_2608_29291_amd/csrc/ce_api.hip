@@ -349,4 +349,15 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   return CE_OK;
 }
 
+int ce_drop_stability(const ce_batch* batch, const int32_t* token_pos_t,
+                      const int32_t* token_pos_ref, float* jaccard, float* j_rand, float* rda,
+                      void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  if (!jaccard) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && (!token_pos_t || !token_pos_ref)) return CE_ERR_INVALID_ARG;
+  return hip_status(launch_stability(batch->seq_offsets, batch->flags, batch->B, batch->T, token_pos_t,
+                                     token_pos_ref, jaccard, j_rand, rda,
+                                     static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -111,4 +111,9 @@ hipError_t launch_scatter(const char* ffn_out, const int32_t* kept_idx, const in
 hipError_t launch_copy_rows(const char* h_in, char* h_out, int64_t row_bytes, int T,
                             const int32_t* token_pos, hipStream_t stream);
 
+// Drop-set Jaccard / random baseline / RDA per sequence (see ce_stability.hip).
+hipError_t launch_stability(const int32_t* seq_offsets, const uint8_t* flags, int B, int T,
+                            const int32_t* tp_t, const int32_t* tp_ref, float* jaccard, float* j_rand,
+                            float* rda, hipStream_t stream);
+
 }  // namespace ce

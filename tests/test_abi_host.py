@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -217,3 +217,14 @@ int main(void) {
         assert r.returncode == 0, r.stderr
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0 and r.stdout.startswith("OK"), r.stdout + r.stderr
+
+
+def test_drop_stability_validation():
+    b = _batch()
+    st = lambda bb, tpt=FAKE, tpr=FAKE, jac=FAKE: ce.lib.ce_drop_stability(
+        ctypes.byref(bb) if bb is not None else None, tpt, tpr, jac, None, None, None)
+    assert st(None) == ce.CE_ERR_INVALID_ARG
+    assert st(_batch(B=0)) == ce.CE_ERR_INVALID_ARG
+    assert st(b, jac=None) == ce.CE_ERR_INVALID_ARG
+    assert st(b, tpt=None) == ce.CE_ERR_INVALID_ARG
+    assert st(b, tpr=None) == ce.CE_ERR_INVALID_ARG
