@@ -12,6 +12,7 @@ Modules:
   select  -- per-sequence TopK (Eq. 6) with a total order, packed index maps
   block   -- gather, SwiGLU FFN on the kept rows, residual scatter; dense block
   stability -- drop-set Jaccard and random-drop-adjusted agreement (Eq. 10-11)
+  ucs_ffn -- FFN-pruning saliency and leakage on the retained rows (Eq. 8-9)
 
 Readings of points the paper leaves open (scorer MLP form, segment boundaries,
 rounding of K, tie-break, packed order, no score scaling) are stated in the
@@ -21,12 +22,12 @@ function docstrings that use them. Every function here is pinned by the
 
 from .score import segment_of, silu, sigmoid, score, score_rows
 from .select import num_keep, order_key, select
-from .block import ffn, routed_block, dense_block, routed_rows
-from . import stability
+from .block import activations, ffn, routed_block, dense_block, routed_rows
+from . import stability, ucs_ffn
 
 __all__ = [
     "segment_of", "silu", "sigmoid", "score", "score_rows",
     "num_keep", "order_key", "select",
-    "ffn", "routed_block", "dense_block", "routed_rows",
-    "stability",
+    "activations", "ffn", "routed_block", "dense_block", "routed_rows",
+    "stability", "ucs_ffn",
 ]

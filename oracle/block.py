@@ -22,13 +22,17 @@ from .select import select
 GEN = 1
 
 
-def ffn(x, w):
-    """SwiGLU FFN on rows x [n, d]: W_d (SiLU(W_g x) * (W_u x)), float64."""
+def activations(x, w):
+    """SwiGLU activations on rows x [n, d]: SiLU(W_g x) * (W_u x), float64 [n, d_ff]."""
     x = np.asarray(x, dtype=np.float64)
     g = x @ np.asarray(w.w_gate, dtype=np.float64).T
     u = x @ np.asarray(w.w_up, dtype=np.float64).T
-    s = silu(g) * u
-    return s @ np.asarray(w.w_down, dtype=np.float64).T
+    return silu(g) * u
+
+
+def ffn(x, w):
+    """SwiGLU FFN on rows x [n, d]: W_d (SiLU(W_g x) * (W_u x)), float64."""
+    return activations(x, w) @ np.asarray(w.w_down, dtype=np.float64).T
 
 
 def routed_rows(hidden, flags, rows, ffn_sets):
