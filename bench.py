@@ -107,6 +107,7 @@ def time_drop_stability(ce, stream, reps: int) -> dict:
         ce.ce_drop_stability(batch, a, b, jac, jr, rda, stream=stream)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(20_000_000)  # let the host enqueue every call before the first starts
     e0.record(stream)
     for _ in range(reps):
         ce.ce_drop_stability(batch, a, b, jac, jr, rda, stream=stream)
@@ -228,8 +229,12 @@ def main():
     torch.cuda.synchronize()
 
     def timed(fn, reps):
+        """Mean GPU time per call. A short device-side delay is queued first so
+        that the host has enqueued every call before the first one starts: the
+        events then time the kernels back to back, not the host's launch rate."""
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(reps)]
+        torch.cuda._sleep(20_000_000)
         for i in range(reps):
             evs[i][0].record(stream)
             fn(i)
@@ -250,6 +255,24 @@ def main():
                                                    ffn_out, ws_ffn, stream=stream), reps),
     }
     log("stages (us): " + ", ".join(f"{k}={v:.1f}" for k, v in stages.items()))
+
+    # FFN-pruning signal (section 3.4, Eq. 8-9) on this step's activations: one
+    # read of act plus the per-sequence saliency rows; a 30% static mask
+    ffn0 = sets[0][2]
+    n_fs = len(wl.ffn)
+    norms = torch.empty(n_fs * F, device=dev)
+    ce.ce_ffn_down_colnorms(ffn0, norms, stream=stream)
+    pmask = torch.from_numpy((np.random.default_rng(3).random(F) < 0.3).astype(np.uint8)).to(dev)
+    sal = torch.empty(wl.B * F, device=dev)
+    lam = torch.empty(wl.B, device=dev)
+    use = torch.empty(wl.B, dtype=torch.uint8, device=dev)
+    sal_us = timed(lambda i: ce.ce_ffn_saliency(batch, act, kept_idx, kept_off, ffn0, norms, pmask, 0.150,
+                                                sal, lam, ws_ffn, use, stream=stream), reps)
+    sal_bytes = cap * F * (2 if bf16 else 4) + wl.B * F * 4 + F  # activations, saliency rows, mask
+    ucs_ffn = {"us_per_call": round(sal_us, 2), "bytes_per_call": sal_bytes, "bound": "hbm",
+               "achieved_GBps": round(sal_bytes / (sal_us * 1e-6) / 1e9, 1), "peak_GBps": PEAK_HBM_GBS,
+               "frac": round(sal_bytes / (sal_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    log(f"ffn saliency + leakage: {sal_us:.1f} us")
 
     gateup_flops = 4.0 * cap * d * F  # gate and up: 2 GEMMs of Kt x d x F, 2 flops per MAC
     peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
@@ -285,6 +308,7 @@ def main():
         "roofline": roofline,
     }
     result["ucs_signals"] = time_drop_stability(ce, stream, max(args.steps, 10))
+    result["ucs_signals"]["ffn_saliency_leakage"] = ucs_ffn
     if not args.no_cpu_baseline:
         n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
         log(f"oracle CPU baseline on {n_seq} sequence(s)...")

@@ -292,6 +292,50 @@ int ce_drop_stability(const ce_batch* batch, const int32_t* token_pos_t,
                       const int32_t* token_pos_ref, float* jaccard, float* j_rand, float* rda,
                       void* stream);
 
+/*
+ * FFN pruning on the retained rows (section 3.4, UCS operator (2); Eq. 8-9).
+ * The pruned FFN is the FFN without the channels of a static mask P; it runs
+ * for a sequence when the saliency leakage of P on that sequence's retained
+ * tokens is at most delta (the paper's delta_FFN is 0.150).
+ *
+ * ce_ffn_down_colnorms: norms[s * d_ff + c] = ||W_down[s][:, c]||_2 in fp32 for
+ *   each weight set s of w (W_down is [d x d_ff]); computed once per layer.
+ *   norms  device float32 [n_sets x d_ff] out
+ *
+ * ce_ffn_saliency: for each sequence b, over its packed rows j (kept_offsets),
+ *   saliency[b * d_ff + c] = mean_j |act[j][c]| * norms[set(j) * d_ff + c]   (Eq. 8)
+ *   leakage[b] = sum_{c: prune_mask[c]} saliency[b][c] / sum_c saliency[b][c]  (Eq. 9)
+ *   use_pruned[b] = leakage[b] <= delta
+ *   act         device dtype [kept_capacity x d_ff]: SwiGLU activations in packed
+ *               row order (the output of ce_ffn_gateup)
+ *   kept_idx    device int32 [kept_capacity] (the MoT set of row j is the GEN
+ *               bit of token kept_idx[j] when w->n_sets == 2)
+ *   prune_mask  device uint8 [d_ff], nonzero = channel in P
+ *   saliency    device float32 [B x d_ff] out; leakage device float32 [B] out
+ *   use_pruned  device uint8 [B] out, or NULL
+ *   ws          the FFN workspace (ce_workspace_size(CE_WS_FFN, ...)); holds the
+ *               per-row-split partial sums (each sequence's rows are split over
+ *               up to 16 workgroups), summed in a fixed order
+ *   A sequence with no retained rows (or zero total saliency) has leakage 0.
+ *
+ * ce_ffn_mask_channels: act[j][c] = 0 for every c in P on the rows j of the
+ *   sequences with use_pruned[b] != 0, in place; ce_ffn_down on the result is
+ *   the pruned FFN for those sequences and the full FFN for the others.
+ *
+ * All three are deterministic (fixed summation order). Errors:
+ * CE_ERR_INVALID_ARG for null pointers / sizes / a non-finite delta,
+ * CE_ERR_UNSUPPORTED for dtypes or widths outside the limits, CE_ERR_WORKSPACE
+ * (ce_ffn_saliency), CE_ERR_HIP.
+ */
+int ce_ffn_down_colnorms(const ce_ffn_w* w, float* norms, void* stream);
+int ce_ffn_saliency(const ce_batch* batch, const void* act, const int32_t* kept_idx,
+                    const int32_t* kept_offsets, const ce_ffn_w* w, const float* norms,
+                    const uint8_t* prune_mask, float delta, float* saliency, float* leakage,
+                    uint8_t* use_pruned, void* ws, size_t ws_bytes, void* stream);
+int ce_ffn_mask_channels(const ce_batch* batch, void* act, const int32_t* kept_offsets, int dtype,
+                         int32_t d_ff, const uint8_t* prune_mask, const uint8_t* use_pruned,
+                         void* stream);
+
 #ifdef __cplusplus
 }
 #endif

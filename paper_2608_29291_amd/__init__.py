@@ -12,6 +12,8 @@ this package fails loudly when the library has not been built.
     ce_scatter_residual  residual merge; dropped rows bypass
     ce_routed_block      all of the above, fused
     ce_drop_stability    drop-set Jaccard / RDA between two timesteps (Eq. 10-11)
+    ce_ffn_down_colnorms, ce_ffn_saliency, ce_ffn_mask_channels
+                         FFN-pruning saliency / leakage on the retained rows (Eq. 8-9)
 """
 from __future__ import annotations
 
@@ -33,6 +35,7 @@ EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
+    "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels",
 ]
 
 
@@ -101,6 +104,10 @@ _sig("ce_scatter_residual", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, 
 _sig("ce_routed_block", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.POINTER(CEScorerW),
                                        ctypes.POINTER(CEFFNW), _p, _p, _p, _p, ctypes.c_size_t, _p])
 _sig("ce_drop_stability", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, _p, _p, _p])
+_sig("ce_ffn_down_colnorms", ctypes.c_int, [ctypes.POINTER(CEFFNW), _p, _p])
+_sig("ce_ffn_saliency", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
+                                       ctypes.c_float, _p, _p, _p, _p, ctypes.c_size_t, _p])
+_sig("ce_ffn_mask_channels", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p])
 
 
 # ----------------------------------------------------------------------------
@@ -309,11 +316,33 @@ def ce_drop_stability(batch: Batch, token_pos_t, token_pos_ref, jaccard, j_rand=
            "ce_drop_stability")
 
 
+def ce_ffn_down_colnorms(ffn: FFN, norms, stream=None):
+    fw = ffn.c()
+    _check(lib.ce_ffn_down_colnorms(ctypes.byref(fw), _dev_ptr(norms), _stream(stream)), "ce_ffn_down_colnorms")
+
+
+def ce_ffn_saliency(batch: Batch, act, kept_idx, kept_offsets, ffn: FFN, norms, prune_mask, delta,
+                    saliency, leakage, ws, use_pruned=None, stream=None):
+    cb, fw = batch.c(), ffn.c()
+    _check(lib.ce_ffn_saliency(ctypes.byref(cb), _dev_ptr(act), _dev_ptr(kept_idx), _dev_ptr(kept_offsets),
+                               ctypes.byref(fw), _dev_ptr(norms), _dev_ptr(prune_mask), float(delta),
+                               _dev_ptr(saliency), _dev_ptr(leakage), _dev_ptr(use_pruned), _dev_ptr(ws),
+                               ws.numel(), _stream(stream)), "ce_ffn_saliency")
+
+
+def ce_ffn_mask_channels(batch: Batch, act, kept_offsets, prune_mask, use_pruned, stream=None):
+    cb = batch.c()
+    _check(lib.ce_ffn_mask_channels(ctypes.byref(cb), _dev_ptr(act), _dev_ptr(kept_offsets), _dtype_code(act),
+                                    int(act.shape[1]), _dev_ptr(prune_mask), _dev_ptr(use_pruned),
+                                    _stream(stream)), "ce_ffn_mask_channels")
+
+
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
     "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
+    "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels",
     "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include "ce_host.hpp"
+#include <math.h>
+
 #include "ce_launch.hpp"
 
 using namespace ce;
@@ -358,6 +360,46 @@ int ce_drop_stability(const ce_batch* batch, const int32_t* token_pos_t,
   return hip_status(launch_stability(batch->seq_offsets, batch->flags, batch->B, batch->T, token_pos_t,
                                      token_pos_ref, jaccard, j_rand, rda,
                                      static_cast<hipStream_t>(stream)));
+}
+
+int ce_ffn_down_colnorms(const ce_ffn_w* w, float* norms, void* stream) {
+  CE_CHECK(check_ffn(w));
+  if (!norms) return CE_ERR_INVALID_ARG;
+  return hip_status(launch_colnorms(static_cast<const char*>(w->w_down[0]),
+                                    static_cast<const char*>(w->n_sets == 2 ? w->w_down[1] : w->w_down[0]),
+                                    w->n_sets, w->d, w->d_ff, w->dtype == CE_BF16, norms,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+int ce_ffn_saliency(const ce_batch* batch, const void* act, const int32_t* kept_idx,
+                    const int32_t* kept_offsets, const ce_ffn_w* w, const float* norms,
+                    const uint8_t* prune_mask, float delta, float* saliency, float* leakage,
+                    uint8_t* use_pruned, void* ws, size_t ws_bytes, void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  CE_CHECK(check_ffn(w));
+  if (!kept_offsets || !norms || !prune_mask || !saliency || !leakage) return CE_ERR_INVALID_ARG;
+  if (!isfinite(delta)) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && (!act || !kept_idx)) return CE_ERR_INVALID_ARG;
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d, w->d_ff,
+                               elem_size(w->dtype));
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  return hip_status(launch_saliency(static_cast<const char*>(act), kept_idx, kept_offsets, batch->flags,
+                                    norms, batch->B, batch->T, batch->kept_capacity, w->d_ff, w->n_sets,
+                                    w->dtype == CE_BF16, prune_mask, delta, at<float>(ws, L.sal_part),
+                                    saliency, leakage, use_pruned, static_cast<hipStream_t>(stream)));
+}
+
+int ce_ffn_mask_channels(const ce_batch* batch, void* act, const int32_t* kept_offsets, int dtype,
+                         int32_t d_ff, const uint8_t* prune_mask, const uint8_t* use_pruned,
+                         void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  if (dtype != CE_F32 && dtype != CE_BF16) return CE_ERR_UNSUPPORTED;
+  if (d_ff <= 0 || (d_ff % 64) != 0) return CE_ERR_UNSUPPORTED;
+  if (!kept_offsets || !prune_mask || !use_pruned) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && !act) return CE_ERR_INVALID_ARG;
+  return hip_status(launch_mask_channels(static_cast<char*>(act), kept_offsets, batch->B,
+                                         batch->kept_capacity, d_ff, dtype == CE_BF16, prune_mask, use_pruned,
+                                         static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

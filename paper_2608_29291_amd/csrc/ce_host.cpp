@@ -61,6 +61,7 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
       L.down_part = take((size_t)tiles * 2 * 256 * 256 * 4);
       L.down_cnt = take((size_t)tiles * 4);
     }
+    L.sal_part = take(((size_t)kSalSplits * sB * sF + sB * ((sF + 255) / 256) * 2) * 4);
   }
   L.total = off;
   return L;

@@ -27,6 +27,8 @@ struct WsLayout {
   size_t act;        // dtype [cap * d_ff] SwiGLU activations
   size_t down_part;  // float [2 x tiles x 256 x 256] split-K partial sums of the down GEMM
   size_t down_cnt;   // int32 [tiles] arrival counters of the split-K down GEMM
+  size_t sal_part;   // float [kSalSplits x B x d_ff] FFN-saliency partial sums, then
+                     // float [B x ceil(d_ff / 256) x 2] per-chunk totals
   size_t total;
 };
 
@@ -37,6 +39,9 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem);
 // when the down GEMM is not split. Shared by the launcher and the workspace
 // layout so both agree.
 constexpr int kSplitMaxTiles = 128;
+// The FFN-saliency reduction splits each sequence's rows over at most this
+// many workgroups (partial sums in the workspace, summed in a fixed order).
+constexpr int kSalSplits = 16;
 int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem);
 
 int elem_size(int dtype);  // 2 for bf16, 4 for f32, 0 if unknown

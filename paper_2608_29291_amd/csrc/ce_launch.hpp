@@ -116,4 +116,15 @@ hipError_t launch_stability(const int32_t* seq_offsets, const uint8_t* flags, in
                             const int32_t* tp_t, const int32_t* tp_ref, float* jaccard, float* j_rand,
                             float* rda, hipStream_t stream);
 
+// FFN-pruning signal: down-projection column norms, per-sequence saliency +
+// leakage, channel masking (see ce_ucs_ffn.hip).
+hipError_t launch_colnorms(const char* w0, const char* w1, int n_sets, int d, int d_ff, bool bf16,
+                           float* norms, hipStream_t stream);
+hipError_t launch_saliency(const char* act, const int32_t* kept_idx, const int32_t* kept_offsets,
+                           const uint8_t* flags, const float* norms, int B, int T, int cap, int d_ff,
+                           int n_sets, bool bf16, const uint8_t* mask, float delta, float* part,
+                           float* saliency, float* lambda, uint8_t* use_pruned, hipStream_t stream);
+hipError_t launch_mask_channels(char* act, const int32_t* kept_offsets, int B, int cap, int d_ff, bool bf16,
+                                const uint8_t* mask, const uint8_t* use_pruned, hipStream_t stream);
+
 }  // namespace ce

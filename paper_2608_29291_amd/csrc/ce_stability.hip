@@ -9,11 +9,16 @@
 //   RDA  = (J - J_rd) / (1 - J_rd)                 (Eq. 11; 1 when J_rd = 1)
 //
 // One workgroup per sequence: the four counts (routable, dropped at t, dropped
-// at t_ref, dropped at both) are reduced over the block; thread 0 forms J from
-// the integers and J_rd in fp64. The hypergeometric probabilities are
-// unimodal: the one at the mode comes from lgamma, its neighbours from the
-// exact ratio of consecutive terms, walking outwards until a term drops below
-// 1e-20 of the peak (the rest of the tail is below fp64 resolution).
+// at t_ref, dropped at both) are reduced over the block, J is formed from the
+// integers and J_rd in fp64 by the whole block. The overlap X of the two random
+// sets is hypergeometric with mean E = a b / n; by Hoeffding's inequality for
+// sampling without replacement, P(|X - E| >= s) <= 2 exp(-2 s^2 / m) with
+// m = min(a, b), so the window E +- sqrt(48 m) misses less than 1e-41 of the
+// mass. Each thread takes a contiguous run of that window: the probability at
+// the run's point nearest the mode comes from lgamma, the others from the
+// exact ratio of consecutive terms walking away from it (so the terms only
+// shrink and an underflow to zero is harmless). The per-thread sums are then
+// added in a fixed order.
 #include "ce_device.hpp"
 #include "ce_launch.hpp"
 #include "ce_router.h"
@@ -31,28 +36,35 @@ __device__ double jaccard_of(int64_t x, int64_t a, int64_t b) {
   return u == 0 ? 1.0 : (double)x / (double)u;
 }
 
-__device__ double expected_random_jaccard(int64_t n, int64_t a, int64_t b) {
-  const int64_t xlo = a + b - n > 0 ? a + b - n : 0;
-  const int64_t xhi = a < b ? a : b;
-  if (xlo >= xhi) return jaccard_of(xlo, a, b);  // a single possible overlap
+// this thread's share of E[J] over the window (see above); every thread calls it
+__device__ double expected_random_jaccard_part(int64_t n, int64_t a, int64_t b, int tid) {
+  int64_t xlo = a + b - n > 0 ? a + b - n : 0;
+  int64_t xhi = a < b ? a : b;
+  const double mean = (double)a * (double)b / (double)(n > 0 ? n : 1);
+  const double half = sqrt(48.0 * (double)xhi) + 2.0;
+  const int64_t wlo = (int64_t)floor(mean - half), whi = (int64_t)ceil(mean + half);
+  xlo = wlo > xlo ? wlo : xlo;
+  xhi = whi < xhi ? whi : xhi;
+  const int64_t per = (xhi - xlo + 256) / 256;
+  const int64_t c0 = xlo + (int64_t)tid * per;
+  const int64_t c1 = c0 + per - 1 < xhi ? c0 + per - 1 : xhi;
+  if (c0 > c1) return 0.0;
   int64_t xm = (int64_t)(((double)(a + 1) * (double)(b + 1)) / (double)(n + 2));
-  xm = xm < xlo ? xlo : (xm > xhi ? xhi : xm);
-  const double pm = exp(log_choose((double)a, (double)xm) + log_choose((double)(n - a), (double)(b - xm)) -
+  const int64_t x0 = xm < c0 ? c0 : (xm > c1 ? c1 : xm);
+  const double p0 = exp(log_choose((double)a, (double)x0) + log_choose((double)(n - a), (double)(b - x0)) -
                         log_choose((double)n, (double)b));
-  const double tiny = pm * 1e-20;
-  double sum = pm * jaccard_of(xm, a, b);
+  if (p0 == 0.0) return 0.0;
+  double sum = p0 * jaccard_of(x0, a, b);
   const double c = (double)(n - a - b);
-  double q = pm;
-  for (int64_t x = xm; x < xhi; ++x) {  // P(x + 1) / P(x) = (a - x)(b - x) / ((x + 1)(n - a - b + x + 1))
+  double q = p0;
+  for (int64_t x = x0; x < c1; ++x) {  // P(x + 1) / P(x) = (a - x)(b - x) / ((x + 1)(n - a - b + x + 1))
     q *= ((double)(a - x) * (double)(b - x)) / ((double)(x + 1) * (c + (double)(x + 1)));
     sum += q * jaccard_of(x + 1, a, b);
-    if (q < tiny) break;
   }
-  q = pm;
-  for (int64_t x = xm; x > xlo; --x) {  // P(x - 1) / P(x) = x (n - a - b + x) / ((a - x + 1)(b - x + 1))
+  q = p0;
+  for (int64_t x = x0; x > c0; --x) {  // P(x - 1) / P(x) = x (n - a - b + x) / ((a - x + 1)(b - x + 1))
     q *= ((double)x * (c + (double)x)) / ((double)(a - x + 1) * (double)(b - x + 1));
     sum += q * jaccard_of(x - 1, a, b);
-    if (q < tiny) break;
   }
   return sum;
 }
@@ -65,6 +77,7 @@ __global__ __launch_bounds__(256) void stability_kernel(const int32_t* __restric
                                                         float* __restrict__ jrand,
                                                         float* __restrict__ rda) {
   __shared__ int cnt[4][4];
+  __shared__ double part[4];
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   int o0 = offs[b], o1 = offs[b + 1];
@@ -92,11 +105,23 @@ __global__ __launch_bounds__(256) void stability_kernel(const int32_t* __restric
     cnt[tid >> 6][3] = nx;
   }
   __syncthreads();
-  if (tid != 0) return;
   int64_t c[4];
   for (int k = 0; k < 4; ++k) c[k] = (int64_t)cnt[0][k] + cnt[1][k] + cnt[2][k] + cnt[3][k];
+  // c[0] = routable tokens, c[1] / c[2] = dropped at t / t_ref, c[3] = dropped at both
+  double jr;
+  const int64_t xlo = c[1] + c[2] - c[0] > 0 ? c[1] + c[2] - c[0] : 0;
+  const int64_t xhi = c[1] < c[2] ? c[1] : c[2];
+  if (xlo >= xhi) {
+    jr = jaccard_of(xlo, c[1], c[2]);  // a single possible overlap
+  } else {
+    double v = expected_random_jaccard_part(c[0], c[1], c[2], tid);
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if ((tid & 63) == 0) part[tid >> 6] = v;
+    __syncthreads();
+    jr = (part[0] + part[1]) + (part[2] + part[3]);
+  }
+  if (tid != 0) return;
   const double j = jaccard_of(c[3], c[1], c[2]);
-  const double jr = expected_random_jaccard(c[0], c[1], c[2]);
   jac[b] = (float)j;
   if (jrand) jrand[b] = (float)jr;
   if (rda) rda[b] = (float)(jr >= 1.0 ? 1.0 : (j - jr) / (1.0 - jr));

@@ -66,3 +66,19 @@ def test_stability_generation_50step_shape(noise):
     # Show-o2 generation workload shape: 4 x [4096 latent (G), then 128 text (KEEP)], keep 0.5
     segs = [[(4096, TOK_GEN), (128, TOK_KEEP)]] * 4
     run_case(segs, 0.5, 0.5, noise, 11)
+
+
+def test_stability_many_sequences():
+    rng = np.random.default_rng(21)
+    segs = []
+    for _ in range(300):
+        n = int(rng.integers(0, 200))
+        segs.append([(n, TOK_GEN), (int(rng.integers(0, 4)), TOK_KEEP)])
+    run_case(segs, 0.37, 0.61, 0.3, 21)
+
+
+@pytest.mark.parametrize("keep_t,keep_ref", [(0.99, 0.02), (0.005, 0.004), (0.5, 0.5), (0.999, 0.998)])
+def test_stability_long_sequence(keep_t, keep_ref):
+    # 60000 routable tokens: J_rand is summed over a window of the overlap's support
+    segs = [[(60000, TOK_GEN), (64, TOK_KEEP)], [(2000, TOK_GEN)]]
+    run_case(segs, keep_t, keep_ref, 0.4, 23)
