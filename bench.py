@@ -274,6 +274,23 @@ def main():
                "frac": round(sal_bytes / (sal_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     log(f"ffn saliency + leakage: {sal_us:.1f} us")
 
+    # layer-skipping gap (section 3.4, Eq. 7) over this workload's hidden
+    # states: two [T x d] reads, the per-token cosines written and re-read
+    kt = int(kept_off[-1].item())
+    tok_pos = torch.full((T,), -1, dtype=torch.int32, device=dev)
+    tok_pos[kept_idx[:kt].long()] = torch.arange(kt, dtype=torch.int32, device=dev)
+    cos_tok = torch.empty(T, device=dev)
+    rho_a, rho_r, gap_b = (torch.empty(wl.B, device=dev) for _ in range(3))
+    skip_b = torch.empty(wl.B, dtype=torch.uint8, device=dev)
+    x_out = sets[1 % n_sets][0]
+    gap_us = timed(lambda i: ce.ce_layer_gap(batch, h0, x_out, tok_pos, 0.0040, cos_tok, rho_a, rho_r, gap_b,
+                                             skip_b, stream=stream), reps)
+    gap_bytes = 2 * T * d * (2 if bf16 else 4) + 12 * T
+    ucs_gap = {"us_per_call": round(gap_us, 2), "bytes_per_call": gap_bytes, "bound": "hbm",
+               "achieved_GBps": round(gap_bytes / (gap_us * 1e-6) / 1e9, 1), "peak_GBps": PEAK_HBM_GBS,
+               "frac": round(gap_bytes / (gap_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    log(f"layer gap: {gap_us:.1f} us")
+
     gateup_flops = 4.0 * cap * d * F  # gate and up: 2 GEMMs of Kt x d x F, 2 flops per MAC
     peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
     achieved = gateup_flops / (stages["ffn_gateup"] * 1e-6) / 1e12
@@ -309,6 +326,7 @@ def main():
     }
     result["ucs_signals"] = time_drop_stability(ce, stream, max(args.steps, 10))
     result["ucs_signals"]["ffn_saliency_leakage"] = ucs_ffn
+    result["ucs_signals"]["layer_gap"] = ucs_gap
     if not args.no_cpu_baseline:
         n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
         log(f"oracle CPU baseline on {n_seq} sequence(s)...")

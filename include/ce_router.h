@@ -336,6 +336,29 @@ int ce_ffn_mask_channels(const ce_batch* batch, void* act, const int32_t* kept_o
                          int32_t d_ff, const uint8_t* prune_mask, const uint8_t* use_pruned,
                          void* stream);
 
+/*
+ * Layer-skipping redundancy gap (section 3.4, UCS operator (1); Eq. 7). For a
+ * candidate layer with input x_in and output x_out (the same batch layout),
+ * per token i and sequence b:
+ *   cos[i]     = <x_in[i], x_out[i]> / (||x_in[i]|| ||x_out[i]||)
+ *                (1 when both rows are zero, 0 when exactly one is)
+ *   rho_all[b] = mean cos over the sequence's tokens          (1 for an empty sequence)
+ *   rho_ret[b] = mean cos over its retained tokens, token_pos >= 0
+ *                (rho_all[b] when none is retained)
+ *   gap[b]     = rho_all[b] - rho_ret[b]                       (Eq. 7)
+ *   skip[b]    = gap[b] <= delta (the paper's delta_LS is 0.0040)
+ *   x_in, x_out  device dtype [T x d] row-major (CE_BF16 or CE_F32; d % 64 == 0)
+ *   token_pos    device int32 [T]: ce_topk_compact's token_pos for this layer
+ *   cos          device float32 [T] out (also the per-token stage's result)
+ *   rho_all, rho_ret, gap  device float32 [B] out; skip device uint8 [B] out, or NULL
+ * Sums run in fp64 in a fixed order (deterministic). Errors: CE_ERR_INVALID_ARG
+ * for null pointers / sizes / a non-finite delta, CE_ERR_UNSUPPORTED for the
+ * dtype or d, CE_ERR_HIP.
+ */
+int ce_layer_gap(const ce_batch* batch, const void* x_in, const void* x_out, int dtype, int32_t d,
+                 const int32_t* token_pos, float delta, float* cos, float* rho_all, float* rho_ret,
+                 float* gap, uint8_t* skip, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

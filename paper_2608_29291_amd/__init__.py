@@ -14,6 +14,7 @@ this package fails loudly when the library has not been built.
     ce_drop_stability    drop-set Jaccard / RDA between two timesteps (Eq. 10-11)
     ce_ffn_down_colnorms, ce_ffn_saliency, ce_ffn_mask_channels
                          FFN-pruning saliency / leakage on the retained rows (Eq. 8-9)
+    ce_layer_gap         layer-skipping redundancy gap of input/output cosines (Eq. 7)
 """
 from __future__ import annotations
 
@@ -35,7 +36,7 @@ EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
-    "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels",
+    "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
 ]
 
 
@@ -108,6 +109,8 @@ _sig("ce_ffn_down_colnorms", ctypes.c_int, [ctypes.POINTER(CEFFNW), _p, _p])
 _sig("ce_ffn_saliency", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
                                        ctypes.c_float, _p, _p, _p, _p, ctypes.c_size_t, _p])
 _sig("ce_ffn_mask_channels", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p])
+_sig("ce_layer_gap", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, ctypes.c_float,
+                                    _p, _p, _p, _p, _p, _p])
 
 
 # ----------------------------------------------------------------------------
@@ -337,12 +340,22 @@ def ce_ffn_mask_channels(batch: Batch, act, kept_offsets, prune_mask, use_pruned
                                     _stream(stream)), "ce_ffn_mask_channels")
 
 
+
+def ce_layer_gap(batch: Batch, x_in, x_out, token_pos, delta, cos, rho_all, rho_ret, gap, skip=None,
+                 stream=None):
+    cb = batch.c()
+    _check(lib.ce_layer_gap(ctypes.byref(cb), _dev_ptr(x_in), _dev_ptr(x_out), _dtype_code(x_in),
+                            int(x_in.shape[1]), _dev_ptr(token_pos), float(delta), _dev_ptr(cos),
+                            _dev_ptr(rho_all), _dev_ptr(rho_ret), _dev_ptr(gap), _dev_ptr(skip),
+                            _stream(stream)), "ce_layer_gap")
+
+
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
     "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
-    "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels",
+    "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -402,4 +402,17 @@ int ce_ffn_mask_channels(const ce_batch* batch, void* act, const int32_t* kept_o
                                          static_cast<hipStream_t>(stream)));
 }
 
+int ce_layer_gap(const ce_batch* batch, const void* x_in, const void* x_out, int dtype, int32_t d,
+                 const int32_t* token_pos, float delta, float* cos, float* rho_all, float* rho_ret,
+                 float* gap, uint8_t* skip, void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  CE_CHECK(check_dtype_d(dtype, d));
+  if (!rho_all || !rho_ret || !gap) return CE_ERR_INVALID_ARG;
+  if (!isfinite(delta)) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && (!x_in || !x_out || !token_pos || !cos)) return CE_ERR_INVALID_ARG;
+  return hip_status(launch_layer_gap(static_cast<const char*>(x_in), static_cast<const char*>(x_out),
+                                     batch->seq_offsets, batch->B, batch->T, d, dtype == CE_BF16, token_pos,
+                                     delta, cos, rho_all, rho_ret, gap, skip, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

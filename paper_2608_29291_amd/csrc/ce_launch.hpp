@@ -127,4 +127,8 @@ hipError_t launch_saliency(const char* act, const int32_t* kept_idx, const int32
 hipError_t launch_mask_channels(char* act, const int32_t* kept_offsets, int B, int cap, int d_ff, bool bf16,
                                 const uint8_t* mask, const uint8_t* use_pruned, hipStream_t stream);
 
+hipError_t launch_layer_gap(const char* x_in, const char* x_out, const int32_t* seq_offsets, int B, int T, int d,
+                            bool bf16, const int32_t* token_pos, float delta, float* cos_tok, float* rho_all,
+                            float* rho_ret, float* gap, uint8_t* skip, hipStream_t stream);
+
 }  // namespace ce

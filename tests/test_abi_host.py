@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 17
+    assert len(names) == 18
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -228,3 +228,53 @@ def test_drop_stability_validation():
     assert st(b, jac=None) == ce.CE_ERR_INVALID_ARG
     assert st(b, tpt=None) == ce.CE_ERR_INVALID_ARG
     assert st(b, tpr=None) == ce.CE_ERR_INVALID_ARG
+
+
+def test_ffn_pruning_validation():
+    b, w = _batch(), _ffn()
+    assert ce.lib.ce_ffn_down_colnorms(None, FAKE, None) == ce.CE_ERR_INVALID_ARG
+    assert ce.lib.ce_ffn_down_colnorms(ctypes.byref(w), None, None) == ce.CE_ERR_INVALID_ARG
+    assert ce.lib.ce_ffn_down_colnorms(ctypes.byref(_ffn(F=100)), FAKE, None) == ce.CE_ERR_UNSUPPORTED
+    need = ce.lib.ce_workspace_size(ce.CE_WS_FFN, ctypes.byref(b), 256, 512, ce.CE_BF16)
+
+    def sal(bb=b, ww=w, act=FAKE, idx=FAKE, off=FAKE, norms=FAKE, mask=FAKE, delta=0.15, s=FAKE, lam=FAKE,
+            ws=FAKE, ws_bytes=need):
+        return ce.lib.ce_ffn_saliency(ctypes.byref(bb), act, idx, off, ctypes.byref(ww), norms, mask, delta,
+                                      s, lam, None, ws, ws_bytes, None)
+    assert sal(off=None) == ce.CE_ERR_INVALID_ARG
+    assert sal(norms=None) == ce.CE_ERR_INVALID_ARG
+    assert sal(mask=None) == ce.CE_ERR_INVALID_ARG
+    assert sal(s=None) == ce.CE_ERR_INVALID_ARG
+    assert sal(lam=None) == ce.CE_ERR_INVALID_ARG
+    assert sal(act=None) == ce.CE_ERR_INVALID_ARG
+    assert sal(delta=float("nan")) == ce.CE_ERR_INVALID_ARG
+    assert sal(delta=float("inf")) == ce.CE_ERR_INVALID_ARG
+    assert sal(ws=None) == ce.CE_ERR_WORKSPACE
+    assert sal(ws_bytes=need - 1) == ce.CE_ERR_WORKSPACE
+    assert sal(ww=_ffn(dtype=5)) == ce.CE_ERR_UNSUPPORTED
+
+    def msk(bb=b, act=FAKE, off=FAKE, dtype=ce.CE_BF16, F=512, mask=FAKE, use=FAKE):
+        return ce.lib.ce_ffn_mask_channels(ctypes.byref(bb), act, off, dtype, F, mask, use, None)
+    assert msk(act=None) == ce.CE_ERR_INVALID_ARG
+    assert msk(off=None) == ce.CE_ERR_INVALID_ARG
+    assert msk(mask=None) == ce.CE_ERR_INVALID_ARG
+    assert msk(use=None) == ce.CE_ERR_INVALID_ARG
+    assert msk(F=100) == ce.CE_ERR_UNSUPPORTED
+    assert msk(dtype=3) == ce.CE_ERR_UNSUPPORTED
+
+
+def test_layer_gap_validation():
+    b = _batch()
+
+    def gap(bb=b, xi=FAKE, xo=FAKE, dtype=ce.CE_BF16, d=256, tp=FAKE, delta=0.004, cos=FAKE, ra=FAKE,
+            rr=FAKE, g=FAKE):
+        return ce.lib.ce_layer_gap(ctypes.byref(bb) if bb is not None else None, xi, xo, dtype, d, tp, delta,
+                                   cos, ra, rr, g, None, None)
+    assert gap(None) == ce.CE_ERR_INVALID_ARG
+    assert gap(_batch(B=0)) == ce.CE_ERR_INVALID_ARG
+    for k in ("xi", "xo", "tp", "cos", "ra", "rr", "g"):
+        assert gap(**{k: None}) == ce.CE_ERR_INVALID_ARG, k
+    assert gap(delta=float("nan")) == ce.CE_ERR_INVALID_ARG
+    assert gap(d=100) == ce.CE_ERR_UNSUPPORTED
+    assert gap(d=0) == ce.CE_ERR_UNSUPPORTED
+    assert gap(dtype=9) == ce.CE_ERR_UNSUPPORTED
