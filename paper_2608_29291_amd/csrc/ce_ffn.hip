@@ -304,8 +304,12 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
 // are fetched two superslabs ahead, weights one ahead. Waves 0-3 fetch weight
 // rows, waves 4-7 token rows, half of their rows in each of the two memory
 // phases of a superslab so the DMA writes into LDS do not bunch up. Rows are
-// 128 bytes, chunk c of row r stored at chunk c ^ (r & 7), which keeps the
-// 32-row fragment reads free of bank conflicts.
+// 128 bytes, chunk c of row r stored at chunk c ^ ((r >> 1) & 7). The LDS
+// (64 banks of 4 bytes) serves a 16-byte read for 16 lanes per clock, here 16
+// consecutive rows; consecutive rows start in alternate halves of the 256-byte
+// bank line, so the 8 rows of each parity need 8 distinct keys for the 16
+// lanes to cover all 64 banks (a key of r & 7 repeats every 8 rows: 2-way
+// conflicts, measured as half of the LDS busy time).
 template <int kMode, int kGroup, bool kPrio, int kSplit, int kWBufs = 2, bool kSpreadW = true,
           bool kSpreadT = true>
 __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) void ffn_gemm_pp2_kernel(
@@ -379,7 +383,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
     const int r = 64 * (wave & 3) + 8 * q + r8;
-    const int c = pch ^ (r & 7);
+    const int c = pch ^ ((r >> 1) & 7);
     if (is_w) {
       int feat;
       if constexpr (kMode == 0) feat = f0 + 32 * ((r >> 5) >> 1) + (r & 31);
@@ -428,7 +432,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     asm volatile("" : "+v"(v));
     return v;
   };
-  const uint32_t rkey = (uint32_t)(lrow & 7);
+  const uint32_t rkey = (uint32_t)((lrow >> 1) & 7);  // fragment rows start at multiples of 32
   const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kRow);
   const uint32_t rowb = (uint32_t)((wt * 64 + lrow) * kRow);
   u32x4_t fa[2][kMW], fb[2][kMT];

@@ -19,8 +19,9 @@
 // buffer loads with the LDS bit: one wave instruction fetches 8 rows x 128
 // bytes, whole cache lines, into LDS. A slab holds the 32 token rows and the
 // tile's weight rows; the ring holds as many slabs as fit in 160 KB (at most
-// 8). Chunk c of row r is stored at chunk c ^ (r & 7), so the 32-row fragment
-// reads are free of bank conflicts.
+// 8). Chunk c of row r is stored at chunk c ^ ((r >> 1) & 7): each group of 16
+// consecutive rows read by a 16-byte fragment load (16 lanes per LDS clock)
+// then covers all 64 banks, so the reads are free of bank conflicts.
 #include <type_traits>
 
 #include "ce_device.hpp"
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int pch = lane & 7;
   const int trow = 8 * wave + r8;  // this lane's row inside a 32-row block
   const bool tlive = trow < n && !(a.flags[lo + (trow < n ? trow : 0)] & CE_TOK_KEEP);
-  const uint32_t chunk_off = (uint32_t)((pch ^ (trow & 7)) << 4);
+  const uint32_t chunk_off = (uint32_t)((pch ^ ((trow >> 1) & 7)) << 4);
   // rows that are never scored read past the resource end: zeros, no traffic
   const uint32_t t_voff = tlive ? (uint32_t)(trow * a.h_ld) + chunk_off : 0x7ffffff0u;
   const uint32_t w_voff = (uint32_t)(trow * a.h_ld) + chunk_off;
@@ -190,7 +191,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   //      slab's fragments are all read before its MFMAs are issued ----
   const int lrow = lane & 31;
   const int lhalf = lane >> 5;
-  const uint32_t rkey = (uint32_t)(lrow & 7);
+  const uint32_t rkey = (uint32_t)((lrow >> 1) & 7);
   const int nk = a.k_bytes / kSlabRow;
   const int nbw = (nb - wave + 3) / 4;  // blocks of this wave (0..4)
   // the epilogue's b1 / w2 values (lane l < 32: b1 of rank l of the block,
