@@ -14,6 +14,7 @@ Modules:
   stability -- drop-set Jaccard and random-drop-adjusted agreement (Eq. 10-11)
   ucs_ffn -- FFN-pruning saliency and leakage on the retained rows (Eq. 8-9)
   layer_gap -- layer-skipping redundancy gap of input/output cosines (Eq. 7)
+  attention -- attention over the packed retained tokens (compressed KV cache)
 
 Readings of points the paper leaves open (scorer MLP form, segment boundaries,
 rounding of K, tie-break, packed order, no score scaling) are stated in the
@@ -24,11 +25,11 @@ function docstrings that use them. Every function here is pinned by the
 from .score import segment_of, silu, sigmoid, score, score_rows
 from .select import num_keep, order_key, select
 from .block import activations, ffn, routed_block, dense_block, routed_rows
-from . import stability, ucs_ffn, layer_gap
+from . import stability, ucs_ffn, layer_gap, attention
 
 __all__ = [
     "segment_of", "silu", "sigmoid", "score", "score_rows",
     "num_keep", "order_key", "select",
     "activations", "ffn", "routed_block", "dense_block", "routed_rows",
-    "stability", "ucs_ffn", "layer_gap",
+    "stability", "ucs_ffn", "layer_gap", "attention",
 ]
