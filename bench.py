@@ -119,6 +119,45 @@ def time_drop_stability(ce, stream, reps: int) -> dict:
                                "workload": "showo2-generation shape, adjacent steps"}}
 
 
+def time_attention(ce, stream, reps: int) -> dict:
+    """Routed attention over the packed retained tokens (section 3.4 token
+    compaction), at the Show-o2 shapes (12 query heads, 2 key/value heads,
+    head_dim 128): understanding prefill over the retained rows of the
+    understanding workload (8 x 551, causal, the compressed KV cache's
+    prefill) and generation over 4 x [2048 latent + 128 text] retained rows
+    (full attention)."""
+    import torch
+    from ce_workloads import make_attention_inputs
+    out = {}
+    for name, lens, causal in (("understanding_prefill", [551] * 8, True),
+                               ("generation", [2176] * 4, False)):
+        q, k, v, qo, ko = make_attention_inputs(lens, lens, 12, 2, 128, seed=3)
+        up = lambda x, dt=None: (torch.from_numpy(np.ascontiguousarray(x)).to(dt) if dt is not None
+                                 else torch.from_numpy(np.ascontiguousarray(x))).to("cuda")
+        dq, dk, dv = up(q, torch.bfloat16), up(k, torch.bfloat16), up(v, torch.bfloat16)
+        o = torch.empty_like(dq)
+        dqo, dko = up(qo), up(ko)
+        for _ in range(3):
+            ce.ce_routed_attention(dq, dk, dv, o, dqo, dko, causal, 128 ** -0.5, stream=stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20_000_000)
+        e0.record(stream)
+        for _ in range(reps):
+            ce.ce_routed_attention(dq, dk, dv, o, dqo, dko, causal, 128 ** -0.5, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        pairs = sum(n * (n + 1) // 2 if causal else n * n for n in lens)
+        flops = 4.0 * 128 * 12 * pairs
+        tf = flops / (us * 1e-6) / 1e12
+        out[name] = {"us_per_call": round(us, 2), "sequences": len(lens), "rows_per_sequence": lens[0],
+                     "causal": causal, "flops_per_call": flops, "bound": "mfma", "achieved_TFLOPs": round(tf, 1),
+                     "peak_TFLOPs": PEAK_BF16_TFLOPS, "frac": round(tf / PEAK_BF16_TFLOPS, 4)}
+        log(f"attention {name}: {us:.1f} us, {tf:.0f} TFLOP/s")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -327,6 +366,7 @@ def main():
     result["ucs_signals"] = time_drop_stability(ce, stream, max(args.steps, 10))
     result["ucs_signals"]["ffn_saliency_leakage"] = ucs_ffn
     result["ucs_signals"]["layer_gap"] = ucs_gap
+    result["routed_attention"] = time_attention(ce, stream, max(args.steps, 10))
     if not args.no_cpu_baseline:
         n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
         log(f"oracle CPU baseline on {n_seq} sequence(s)...")

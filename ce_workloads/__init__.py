@@ -391,3 +391,18 @@ def make_drop_pair(segments, keep_t: float, keep_ref: float, noise: float, seed:
                     pos += 1
         tps.append(tp)
     return offs, flags, tps[0], tps[1]
+
+
+def make_attention_inputs(q_lens, kv_lens, n_heads: int, n_kv_heads: int, head_dim: int, seed: int,
+                          q_scale: float = 1.0):
+    """Packed queries / keys / values for the routed attention: per sequence b,
+    q_lens[b] query rows and kv_lens[b] key/value rows, entries N(0,1) (queries
+    times q_scale), rounded to bf16. Returns (q [Nq, H, dh], k, v [Nkv, H_kv, dh]
+    float32 arrays holding bf16 values, q_offsets, kv_offsets int32)."""
+    rng = np.random.default_rng(seed)
+    qo = np.concatenate([[0], np.cumsum(q_lens)]).astype(np.int32)
+    ko = np.concatenate([[0], np.cumsum(kv_lens)]).astype(np.int32)
+    q = bf16_round((rng.standard_normal((int(qo[-1]), n_heads, head_dim)) * q_scale).astype(np.float32))
+    k = bf16_round(rng.standard_normal((int(ko[-1]), n_kv_heads, head_dim)).astype(np.float32))
+    v = bf16_round(rng.standard_normal((int(ko[-1]), n_kv_heads, head_dim)).astype(np.float32))
+    return q, k, v, qo, ko

@@ -359,6 +359,43 @@ int ce_layer_gap(const ce_batch* batch, const void* x_in, const void* x_out, int
                  const int32_t* token_pos, float delta, float* cos, float* rho_all, float* rho_ret,
                  float* gap, uint8_t* skip, void* stream);
 
+/*
+ * Attention over the packed retained tokens of a routed layer (section 3.4,
+ * task-adaptive token compaction: retained tokens are packed into a shorter
+ * sequence for the layer's attention and FFN; for understanding, the packed
+ * keys / values are the compressed key-value cache that decoding reuses).
+ * For each sequence b and query head h, with kv(h) = h / (n_heads / n_kv_heads):
+ *   O_b[:, h] = softmax(scale * Q_b[:, h] K_b[:, kv(h)]^T + M) V_b[:, kv(h)]
+ * M = 0, or with causal != 0, -inf for key j > i + (n_kv - n_q) (end-aligned:
+ * prefill has n_q = n_kv, a decode step n_q = 1 over the whole cache). A query
+ * that sees no key outputs zeros. Sequences never attend to each other.
+ */
+typedef struct ce_attn {
+  int32_t B;                  /* sequences, >= 1 */
+  int32_t n_heads;            /* query heads H */
+  int32_t n_kv_heads;         /* key/value heads; divides H */
+  int32_t head_dim;           /* 128 */
+  const int32_t* q_offsets;   /* device int32 [B+1]: packed query rows of each sequence */
+  const int32_t* kv_offsets;  /* device int32 [B+1]: packed key/value rows of each sequence */
+  int32_t q_capacity;         /* rows of q and o (grid bound; offsets are clamped to it) */
+  int32_t kv_capacity;        /* rows of k and v */
+  int32_t causal;             /* 0 or 1 */
+  float scale;                /* softmax scale > 0, e.g. 1 / sqrt(head_dim) */
+  int32_t dtype;              /* CE_BF16 */
+} ce_attn;
+
+/*
+ *   q, o   device bf16 [q_capacity x n_heads x head_dim], row-major (o written
+ *          for the rows of real queries only)
+ *   k, v   device bf16 [kv_capacity x n_kv_heads x head_dim], row-major
+ * fp32 accumulation; the probabilities are rounded to bf16 for the product
+ * with V. Deterministic. Errors: CE_ERR_INVALID_ARG for null pointers, sizes,
+ * a scale that is not a positive finite number or causal outside {0, 1}; CE_ERR_UNSUPPORTED for another
+ * dtype or head_dim, or buffers of 2 GiB or more; CE_ERR_HIP.
+ */
+int ce_routed_attention(const ce_attn* attn, const void* q, const void* k, const void* v, void* o,
+                        void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,6 +15,7 @@ this package fails loudly when the library has not been built.
     ce_ffn_down_colnorms, ce_ffn_saliency, ce_ffn_mask_channels
                          FFN-pruning saliency / leakage on the retained rows (Eq. 8-9)
     ce_layer_gap         layer-skipping redundancy gap of input/output cosines (Eq. 7)
+    ce_routed_attention  attention over the packed retained tokens (compressed KV cache)
 """
 from __future__ import annotations
 
@@ -37,6 +38,7 @@ EXPORTED = [
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
+    "ce_routed_attention",
 ]
 
 
@@ -78,6 +80,12 @@ class CEFFNW(ctypes.Structure):
                 ("w_gate", _p * 2), ("w_up", _p * 2), ("w_down", _p * 2)]
 
 
+class CEAttn(ctypes.Structure):
+    _fields_ = [("B", _i32), ("n_heads", _i32), ("n_kv_heads", _i32), ("head_dim", _i32),
+                ("q_offsets", _p), ("kv_offsets", _p), ("q_capacity", _i32), ("kv_capacity", _i32),
+                ("causal", _i32), ("scale", ctypes.c_float), ("dtype", _i32)]
+
+
 def _sig(name, res, args):
     f = getattr(lib, name)
     f.restype = res
@@ -109,6 +117,7 @@ _sig("ce_ffn_down_colnorms", ctypes.c_int, [ctypes.POINTER(CEFFNW), _p, _p])
 _sig("ce_ffn_saliency", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
                                        ctypes.c_float, _p, _p, _p, _p, ctypes.c_size_t, _p])
 _sig("ce_ffn_mask_channels", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p])
+_sig("ce_routed_attention", ctypes.c_int, [ctypes.POINTER(CEAttn), _p, _p, _p, _p, _p])
 _sig("ce_layer_gap", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, ctypes.c_float,
                                     _p, _p, _p, _p, _p, _p])
 
@@ -350,12 +359,24 @@ def ce_layer_gap(batch: Batch, x_in, x_out, token_pos, delta, cos, rho_all, rho_
                             _stream(stream)), "ce_layer_gap")
 
 
+
+def ce_routed_attention(q, k, v, o, q_offsets, kv_offsets, causal, scale, stream=None):
+    """q, o [rows, H, head_dim], k, v [rows, H_kv, head_dim] bf16 device tensors;
+    q_offsets / kv_offsets int32 device tensors [B+1]."""
+    at = CEAttn(int(q_offsets.numel() - 1), int(q.shape[1]), int(k.shape[1]), int(q.shape[2]),
+                _dev_ptr(q_offsets), _dev_ptr(kv_offsets), int(q.shape[0]), int(k.shape[0]),
+                int(bool(causal)), float(scale), _dtype_code(q))
+    _check(lib.ce_routed_attention(ctypes.byref(at), _dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o),
+                                   _stream(stream)), "ce_routed_attention")
+
+
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
     "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
+    "ce_routed_attention", "CEAttn",
     "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -26,7 +26,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["ce_api.hip", "ce_score.hip", "ce_topk.hip", "ce_ffn.hip", "ce_scatter.hip", "ce_stability.hip",
-           "ce_ucs_ffn.hip", "ce_layer_gap.hip", "ce_host.cpp"]
+           "ce_ucs_ffn.hip", "ce_layer_gap.hip", "ce_attention.hip", "ce_host.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -415,4 +415,24 @@ int ce_layer_gap(const ce_batch* batch, const void* x_in, const void* x_out, int
                                      delta, cos, rho_all, rho_ret, gap, skip, static_cast<hipStream_t>(stream)));
 }
 
+int ce_routed_attention(const ce_attn* at, const void* q, const void* k, const void* v, void* o, void* stream) {
+  if (!at) return CE_ERR_INVALID_ARG;
+  if (at->B < 1 || at->n_heads < 1 || at->n_kv_heads < 1 || at->q_capacity < 0 || at->kv_capacity < 0)
+    return CE_ERR_INVALID_ARG;
+  if (at->n_heads % at->n_kv_heads != 0) return CE_ERR_INVALID_ARG;
+  if (at->causal != 0 && at->causal != 1) return CE_ERR_INVALID_ARG;
+  if (!isfinite(at->scale) || !(at->scale > 0.0f)) return CE_ERR_INVALID_ARG;
+  if (!at->q_offsets || !at->kv_offsets) return CE_ERR_INVALID_ARG;
+  if (at->dtype != CE_BF16 || at->head_dim != 128) return CE_ERR_UNSUPPORTED;
+  const int64_t lim = (int64_t)1 << 31;
+  if ((int64_t)at->q_capacity * at->n_heads * 256 >= lim || (int64_t)at->kv_capacity * at->n_kv_heads * 256 >= lim)
+    return CE_ERR_UNSUPPORTED;
+  if (at->q_capacity > 0 && (!q || !o)) return CE_ERR_INVALID_ARG;
+  if (at->q_capacity > 0 && at->kv_capacity > 0 && (!k || !v)) return CE_ERR_INVALID_ARG;
+  return hip_status(launch_attention(static_cast<const char*>(q), static_cast<const char*>(k),
+                                     static_cast<const char*>(v), static_cast<char*>(o), at->q_offsets,
+                                     at->kv_offsets, at->B, at->n_heads, at->n_kv_heads, at->q_capacity,
+                                     at->kv_capacity, at->causal != 0, at->scale, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

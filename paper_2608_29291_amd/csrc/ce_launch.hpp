@@ -131,4 +131,8 @@ hipError_t launch_layer_gap(const char* x_in, const char* x_out, const int32_t* 
                             bool bf16, const int32_t* token_pos, float delta, float* cos_tok, float* rho_all,
                             float* rho_ret, float* gap, uint8_t* skip, hipStream_t stream);
 
+hipError_t launch_attention(const char* q, const char* k, const char* v, char* o, const int32_t* q_offsets,
+                            const int32_t* kv_offsets, int B, int H, int Hkv, int q_cap, int kv_cap, bool causal,
+                            float scale, hipStream_t stream);
+
 }  // namespace ce

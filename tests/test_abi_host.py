@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -278,3 +278,37 @@ def test_layer_gap_validation():
     assert gap(d=100) == ce.CE_ERR_UNSUPPORTED
     assert gap(d=0) == ce.CE_ERR_UNSUPPORTED
     assert gap(dtype=9) == ce.CE_ERR_UNSUPPORTED
+
+
+def _attn(**kw):
+    f = dict(B=2, n_heads=12, n_kv_heads=2, head_dim=128, q_offsets=FAKE, kv_offsets=FAKE, q_capacity=100,
+             kv_capacity=100, causal=1, scale=0.088, dtype=ce.CE_BF16)
+    f.update(kw)
+    return ce.CEAttn(**f)
+
+
+@pytest.mark.parametrize("kw,ptrs,code", [
+    ({}, {"q": None}, ce.CE_ERR_INVALID_ARG),
+    ({}, {"o": None}, ce.CE_ERR_INVALID_ARG),
+    ({}, {"k": None}, ce.CE_ERR_INVALID_ARG),
+    ({}, {"v": None}, ce.CE_ERR_INVALID_ARG),
+    ({"B": 0}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"n_heads": 12, "n_kv_heads": 5}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"n_kv_heads": 0}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"causal": 2}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"scale": float("nan")}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"scale": 0.0}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"scale": -0.1}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"q_offsets": None}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"kv_offsets": None}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"q_capacity": -1}, {}, ce.CE_ERR_INVALID_ARG),
+    ({"head_dim": 64}, {}, ce.CE_ERR_UNSUPPORTED),
+    ({"dtype": ce.CE_F32}, {}, ce.CE_ERR_UNSUPPORTED),
+    ({"q_capacity": 1 << 20, "n_heads": 12}, {}, ce.CE_ERR_UNSUPPORTED),
+])
+def test_attention_validation(kw, ptrs, code):
+    p = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE)
+    p.update(ptrs)
+    at = _attn(**kw)
+    assert ce.lib.ce_routed_attention(ctypes.byref(at), p["q"], p["k"], p["v"], p["o"], None) == code
+    assert ce.lib.ce_routed_attention(None, FAKE, FAKE, FAKE, FAKE, None) == ce.CE_ERR_INVALID_ARG

@@ -1,0 +1,108 @@
+"""GPU parity of the routed attention over packed retained tokens (section 3.4
+token compaction; compressed KV cache for decoding) against the float64 oracle.
+
+Tolerance. The kernel accumulates scores and outputs in fp32 and rounds the
+probabilities to bf16 before the product with V: each weight p_j is off by at
+most 2^-9 of itself, so the output (a convex combination of value rows) is off
+by at most 2^-9 max|v|; the final bf16 rounding of O adds at most 2^-9 |O| <=
+2^-9 max|v|. fp32 scores and the hardware exp2 add far less. Bar:
+max |O_gpu - O_ref| <= 2^-8 max|v| + 1e-6.
+"""
+import numpy as np
+import pytest
+
+from ce_workloads import make_attention_inputs
+from oracle import attention as oa
+
+pytestmark = pytest.mark.gpu
+
+DH = 128
+
+
+@pytest.fixture(scope="module")
+def G():
+    import gpu_util
+    return gpu_util
+
+
+def run(G, q, k, v, qo, ko, causal, scale=None):
+    import torch
+    import paper_2608_29291_amd as ce
+    scale = 1.0 / np.sqrt(DH) if scale is None else scale
+    dq = G.to_dev(q, torch.bfloat16)
+    dk = G.to_dev(k, torch.bfloat16)
+    dv = G.to_dev(v, torch.bfloat16)
+    o = torch.full(dq.shape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    ce.ce_routed_attention(dq, dk, dv, o, G.to_dev(qo), G.to_dev(ko), causal, scale)
+    torch.cuda.synchronize()
+    return G.host(o), scale
+
+
+def check(got, ref, v):
+    tol = 2.0 ** -8 * float(np.max(np.abs(v))) + 1e-6 if v.size else 1e-6
+    err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    print(f"  max err {err:.3e} (bar {tol:.3e})")
+    assert err <= tol
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("H,Hkv", [(12, 2), (28, 4), (4, 4)])
+def test_ragged_prefill(G, causal, H, Hkv):
+    lens = [550, 1, 0, 129, 300, 64, 65]
+    q, k, v, qo, ko = make_attention_inputs(lens, lens, H, Hkv, DH, seed=H + Hkv + causal)
+    got, scale = run(G, q, k, v, qo, ko, causal)
+    print(f"[attn prefill H={H} Hkv={Hkv} causal={causal}]")
+    check(got, oa.attention(q, k, v, qo, ko, Hkv, causal, scale), v)
+
+
+@pytest.mark.parametrize("q_lens,kv_lens", [([1, 1, 1, 1], [550, 2176, 1, 63]),       # decode steps
+                                           ([200, 3, 64], [550, 3, 700]),            # chunked prefill
+                                           ([5, 7], [0, 9]),                         # a sequence with no keys
+                                           ([300], [100])])                          # more queries than keys
+def test_cache_shapes(G, q_lens, kv_lens):
+    q, k, v, qo, ko = make_attention_inputs(q_lens, kv_lens, 12, 2, DH, seed=sum(q_lens))
+    for causal in (True, False):
+        got, scale = run(G, q, k, v, qo, ko, causal)
+        ref = oa.attention(q, k, v, qo, ko, 2, causal, scale)
+        print(f"[attn cache q={q_lens} kv={kv_lens} causal={causal}]")
+        check(got, ref, v)
+    # rows of a sequence without keys are exactly zero
+    for b in range(len(q_lens)):
+        if kv_lens[b] == 0:
+            assert np.all(got[qo[b]:qo[b + 1]] == 0.0)
+
+
+def test_sharp_scores_and_scale(G):
+    q, k, v, qo, ko = make_attention_inputs([257, 90], [257, 90], 8, 2, DH, seed=5, q_scale=12.0)
+    for scale in (1.0 / np.sqrt(DH), 0.5):
+        got, _ = run(G, q, k, v, qo, ko, True, scale)
+        print(f"[attn sharp scale={scale}]")
+        check(got, oa.attention(q, k, v, qo, ko, 2, True, scale), v)
+
+
+def test_deterministic(G):
+    q, k, v, qo, ko = make_attention_inputs([550, 300], [550, 300], 12, 2, DH, seed=6)
+    a, _ = run(G, q, k, v, qo, ko, True)
+    b, _ = run(G, q, k, v, qo, ko, True)
+    np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_generation_size_sampled(G, causal):
+    """The generation workload's packed shape (4 x [2048 latent + 128 text]
+    retained, 12 heads, 2 KV heads) in one launch; the oracle checks the last
+    24 queries of every sequence (end-aligned, so causal masking is the same
+    for the sample) and 24 evenly spaced queries under full attention."""
+    n = 2176
+    q, k, v, qo, ko = make_attention_inputs([n] * 4, [n] * 4, 12, 2, DH, seed=7)
+    got, scale = run(G, q, k, v, qo, ko, causal)
+    rows = []
+    for b in range(4):
+        if causal:
+            rows.append(np.arange(qo[b + 1] - 24, qo[b + 1]))
+        else:
+            rows.append(qo[b] + np.linspace(0, n - 1, 24).astype(int))
+    for b, r in enumerate(rows):
+        ref = oa.attention(q[r], k[ko[b]:ko[b + 1]], v[ko[b]:ko[b + 1]], [0, len(r)], [0, n], 2, causal, scale)
+        print(f"[attn generation size b={b} causal={causal}]")
+        check(got[r], ref, v)
