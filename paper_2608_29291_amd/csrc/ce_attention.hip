@@ -27,12 +27,15 @@
 //     chunk c of row r stored at c ^ (r & 15), so 16 consecutive rows read by
 //     one 16-byte fragment load cover all 64 banks); V tiles are loaded to
 //     registers and written transposed, [dim][key], 8-byte units u of row d at
-//     u ^ vkey(d), vkey(d) = ((d >> 1) & 15) ^ (4 ((d >> 5) & 3)): 16
-//     consecutive rows of one parity get distinct units, and so do rows 32
-//     apart (the compiler pairs the reads of rows d and d + 32 in one
-//     instruction); each write instruction covers rows of both parities;
-//   * K and V are double-buffered: the next tile is fetched while the current
-//     one is computed, one barrier per tile. With causal masking the tiles
+//     u ^ ((d >> 1) & 15) (16 consecutive rows of one parity get distinct
+//     units); blocks of 32 rows sit 32 x 128 + 8 bytes apart, an offset the
+//     compiler cannot fold into one paired read (pairing rows of two blocks
+//     would put two reads on one bank); each write instruction covers rows of
+//     both parities;
+//   * each stage issues the score MFMAs of key tile t + 1 before the softmax
+//     of tile t (they are independent, so the matrix pipe can run while the
+//     VALU computes exponentials), then P V of tile t; K and V are
+//     double-buffered, one barrier per tile. With causal masking the tiles
 //     after the block's last query are skipped, and only tiles that reach past
 //     a wave's first visible limit are masked element by element;
 //   * the scale is folded into the exponent, p = 2^(s c - m c) with c = scale
@@ -52,7 +55,9 @@ constexpr int kQT = 128;       // queries per workgroup
 constexpr int kKT = 64;        // keys per tile
 constexpr int kKRow = kDh * 2; // bytes per key row
 constexpr int kKBytes = kKT * kKRow;       // 16 KB
-constexpr int kVBytes = kDh * kKT * 2;     // 16 KB
+constexpr int kVRow = kKT * 2;             // bytes per row of V^T (64 keys)
+constexpr int kVBlk = 32 * kVRow + 8;      // 32 rows of V^T, padded
+constexpr int kVBytes = 4 * kVBlk;         // 16 KB + 32
 
 struct AttnArgs {
   const char* q;
@@ -67,7 +72,10 @@ struct AttnArgs {
 
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
-__device__ __forceinline__ uint32_t vkey_of(int d) { return (uint32_t)(((d >> 1) & 15) ^ (((d >> 5) & 3) << 2)); }
+__device__ __forceinline__ uint32_t vkey_of(int d) { return (uint32_t)((d >> 1) & 15); }
+__device__ __forceinline__ uint32_t vt_off(int d, uint32_t unit) {  // byte offset of V^T row d, unit
+  return (uint32_t)((d >> 5) * kVBlk + (d & 31) * kVRow) + ((unit ^ vkey_of(d)) << 3);
+}
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void attention_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * kKBytes + 2 * kVBytes];
@@ -87,7 +95,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int tiles = (hi - lo + kQT - 1) / kQT;
     if (t < tiles) {
       b = s;
-      q0 = t * kQT;
+      q0 = (tiles - 1 - t) * kQT;  // last tiles first: under a causal mask they see the most keys
       nq = hi - lo;
       qbase = lo;
       break;
@@ -179,7 +187,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int d = 8 * vdg + (e ^ (vdg & 1));
-    vst[e] = opaque((uint32_t)(d * (kKT * 2) + ((vkg ^ vkey_of(d)) << 3)));
+    vst[e] = vt_off(d, (uint32_t)vkg);
   }
   const uint32_t sel_even = (vdg & 1) ? 0x07060302u : 0x05040100u;  // low or high halves
   const uint32_t sel_odd = (vdg & 1) ? 0x05040100u : 0x07060302u;
@@ -200,17 +208,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
   for (int s2 = 0; s2 < 8; ++s2)
     koff[s2] = opaque((uint32_t)(lrow * kKRow + ((((uint32_t)(2 * s2 + lhalf)) ^ (uint32_t)(lrow & 15)) << 4)));
-  // V^T: row 32 db + lrow, 8-byte unit lhalf + 2 i, swizzled; one register per
-  // read (reads sharing a base register would be paired into one instruction,
-  // and rows 64 apart share their swizzle key: a bank conflict)
-  uint32_t voffd[4][8];
+  uint32_t voff8[8];  // V^T: row lrow, logical unit lhalf + 2 i (block db adds db * kVBlk)
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int d = 32 * db + lrow;
-      voffd[db][i] = opaque((uint32_t)(d * (kKT * 2) + ((((uint32_t)(lhalf + 2 * i)) ^ vkey_of(d)) << 3)));
-    }
+  for (int i = 0; i < 8; ++i) voff8[i] = opaque(vt_off(lrow, (uint32_t)(lhalf + 2 * i)));
 
   f32x16_t oacc[4];
 #pragma unroll
@@ -221,25 +221,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
-  auto body = [&](auto cur_c, int tile) __attribute__((always_inline)) {
-    constexpr int kCur = decltype(cur_c)::value;
-    const bool more = tile + 1 < ntiles;
-    if (more) {
-      dma_k(tile + 1, kCur ^ 1);
-      load_v(tile + 1);
-    }
-    // ---- S^T = K Q^T: two blocks of 32 keys, two independent chains ----
-    const char* kb = kbuf + kCur * kKBytes;
-    f32x16_t sacc[2] = {f32x16_t{}, f32x16_t{}};
+  // scores of one key tile: S^T = K Q^T, two blocks of 32 keys, two chains
+  auto scores = [&](int kbuf_i, f32x16_t (&sc)[2]) __attribute__((always_inline)) {
+    const char* kb = kbuf + kbuf_i * kKBytes;
+    sc[0] = f32x16_t{};
+    sc[1] = f32x16_t{};
 #pragma unroll
     for (int s2 = 0; s2 < 8; ++s2)
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2) {
         const u32x4_t kf = *reinterpret_cast<const u32x4_t*>(kb + koff[s2] + 32 * kb2 * kKRow);
-        mfma_step<true>(sacc[kb2], kf, qf[s2]);
+        mfma_step<true>(sc[kb2], kf, qf[s2]);
       }
-    // ---- mask (only where some key of the tile is hidden from the wave's
-    //      first query), online softmax (lane = query) ----
+  };
+  // hide the keys of tile `tile` this lane may not see (ragged end, causal cut)
+  auto mask = [&](int tile, f32x16_t (&sc)[2]) __attribute__((always_inline)) {
     const int kbase = tile * kKT;
     if (kbase + kKT > vis0) {
 #pragma unroll
@@ -247,14 +243,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int j = kbase + 32 * kb2 + 8 * (v >> 2) + 4 * lhalf + (v & 3);
-          if (j >= vis) sacc[kb2][v] = -__builtin_inff();
+          if (j >= vis) sc[kb2][v] = -__builtin_inff();
         }
     }
+  };
+  // one pipeline stage: scores of tile + 1 (into sn) under the softmax of
+  // tile (from sc), then P V of tile
+  auto body = [&](auto cur_c, int tile, f32x16_t (&sc)[2], f32x16_t (&sn)[2]) __attribute__((always_inline)) {
+    constexpr int kCur = decltype(cur_c)::value;
+    const bool more = tile + 1 < ntiles;
+    if (tile + 2 < ntiles) dma_k(tile + 2, kCur);  // K of tile was read one stage ago
+    if (more) load_v(tile + 1);
+    // ---- scores of tile + 1 ----
+    if (more) scores(kCur ^ 1, sn);
+    // ---- online softmax of tile (lane = query) ----
     float mt = -__builtin_inff();
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[kb2][v]);
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb2][v]);
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
     const float mc = m_new == -__builtin_inff() ? 0.0f : m_new * a.scale_log2;
@@ -264,11 +271,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb2][v], a.scale_log2, -mc));
-        sacc[kb2][v] = p;
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[kb2][v], a.scale_log2, -mc));
+        sc[kb2][v] = p;
         rs += p;
       }
     rs += __shfl_xor(rs, 32);
+    u32x4_t pf[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        pf[st][i] = pack_bf16(sc[st >> 1][8 * (st & 1) + 2 * i], sc[st >> 1][8 * (st & 1) + 2 * i + 1]);
     l_run = l_run * alpha + rs;
     if (__builtin_amdgcn_ballot_w64(m_new != m_run)) {
 #pragma unroll
@@ -280,39 +293,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       const int kb2 = st >> 1, h2 = st & 1;
-      u32x4_t pf;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pf[i] = pack_bf16(sacc[kb2][8 * h2 + 2 * i], sacc[kb2][8 * h2 + 2 * i + 1]);
+      const int i0 = (8 * kb2 + 4 * h2) >> 1;  // logical units (8 kb2 + 4 h2 + lhalf) and +2
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        // logical units (8 kb2 + 4 h2 + lhalf) and +2 of row 32 db + lrow
-        const int i0 = (8 * kb2 + 4 * h2) >> 1;
-        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vb + voffd[db][i0]);
-        const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vb + voffd[db][i0 + 1]);
+        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vb + db * kVBlk + voff8[i0]);
+        const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vb + db * kVBlk + voff8[i0 + 1]);
         const u32x4_t vf = {lo.x, lo.y, hi.x, hi.y};
-        mfma_step<true>(oacc[db], vf, pf);
+        mfma_step<true>(oacc[db], vf, pf[st]);
       }
     }
     if (more) {
+      mask(tile + 1, sn);
       store_v(std::integral_constant<int, kCur ^ 1>{});
-      wait_vmcnt<0>();
     }
+    wait_vmcnt<0>();
     __syncthreads();
   };
 
+  f32x16_t sa[2], sb[2];
   if (ntiles > 0) {
     dma_k(0, 0);
+    if (ntiles > 1) dma_k(1, 1);
     load_v(0);
     store_v(B0{});
     wait_vmcnt<0>();
     __syncthreads();
+    scores(0, sa);
+    mask(0, sa);
+    lds_barrier();  // every wave has read K of tile 0 before the first stage refills it
   }
   int tile = 0;
   for (; tile + 1 < ntiles; tile += 2) {
-    body(B0{}, tile);
-    body(B1{}, tile + 1);
+    body(B0{}, tile, sa, sb);
+    body(B1{}, tile + 1, sb, sa);
   }
-  if (tile < ntiles) body(B0{}, tile);
+  if (tile < ntiles) body(B0{}, tile, sa, sb);
 
   // ---- epilogue: O = O^T / l, rows of real queries only ----
   if (qi >= nq) return;
