@@ -56,6 +56,7 @@ ScoreArgs make_score_args(const ce_batch* b, const void* hidden, const ce_scorer
   a.n_seg = w->n_seg;
   a.logits = logits;
   a.probs = probs;
+  a.info = nullptr;
   return a;
 }
 
@@ -303,13 +304,11 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   int32_t* token_pos = at<int32_t>(ws, L.token_pos);
   int32_t* info = at<int32_t>(ws, L.seq_info);
 
-  // 1. routing logits (Eq. 4)
-  if (batch->T > 0) {
-    const ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
-    CE_TRY(launch_score(sa, bf16, s));
-  }
+  // 1. routing logits (Eq. 4); the same launch writes the per-sequence summaries
+  ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
+  sa.info = info;
+  CE_TRY(launch_score(sa, bf16, s));
   // 2-3. per-sequence TopK + packed index maps (Eq. 6)
-  CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));
   SelectArgs sel;
   sel.logits = logits;
   sel.flags = batch->flags;

@@ -186,4 +186,37 @@ __device__ __forceinline__ int32_t num_keep_dev(float keep, int32_t n) {
   return (int32_t)k;
 }
 
+// Sum of one int64 per thread over the workgroup (wave reduction, then LDS
+// across waves; scratch holds one value per wave).
+__device__ __forceinline__ int64_t block_sum_i64(int64_t v, int64_t* scratch) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) scratch[wave] = v;
+  __syncthreads();
+  int64_t s = 0;
+  const int nw = blockDim.x >> 6;
+  for (int w = 0; w < nw; ++w) s += scratch[w];
+  return s;
+}
+
+// Per-sequence summary of sequence b, computed by one workgroup:
+// info[3b] = lo (clamped), info[3b+1] = len (clamped), info[3b+2] = number of
+// always-kept tokens | bad << 31 (offsets out of order or not covering [0, T)).
+__device__ __forceinline__ void seq_summary(const int32_t* __restrict__ offs, const uint8_t* __restrict__ flags,
+                                            int B, int T, int b, int32_t* __restrict__ info, int64_t* scratch) {
+  const int o0 = offs[b], o1 = offs[b + 1];
+  const bool bad = o0 < 0 || o1 < o0 || o1 > T || (b == 0 && o0 != 0) || (b == B - 1 && o1 != T);
+  const int lo = o0 < 0 ? 0 : (o0 > T ? T : o0);
+  const int hi = o1 < lo ? lo : (o1 > T ? T : o1);
+  int64_t c = 0;
+  for (int i = lo + threadIdx.x; i < hi; i += blockDim.x) c += (flags[i] & 2) ? 1 : 0;
+  c = block_sum_i64(c, scratch);
+  if (threadIdx.x == 0) {
+    info[3 * b + 0] = lo;
+    info[3 * b + 1] = hi - lo;
+    info[3 * b + 2] = (int32_t)c | (bad ? (int32_t)0x80000000 : 0);
+  }
+}
+
 }  // namespace ce

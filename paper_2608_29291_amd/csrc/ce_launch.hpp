@@ -70,6 +70,7 @@ struct ScoreArgs {
   int r_core, r_exp, n_seg;
   float* logits;
   float* probs;
+  int32_t* info;  // if set, B extra workgroups also write the per-sequence summary (seq_info layout)
 };
 hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream);
 

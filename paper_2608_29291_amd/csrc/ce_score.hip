@@ -94,7 +94,7 @@ __device__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo
 template <bool kBF16>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kLds];
-  __shared__ int sh[260];
+  __shared__ __attribute__((aligned(8))) int sh[260];  // also the summary's int64 scratch
   __shared__ float red[4][2][kTok];
   __shared__ float ep[4][kMaxBlocks / 4][64];  // per wave and block: b1 (32 ranks), w2 (32 ranks)
 
@@ -102,8 +102,18 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
+  int tile = blockIdx.x;
+  if (a.info) {
+    // the first B workgroups write the per-sequence summaries the TopK step
+    // reads (they run on CUs the scoring tiles leave free)
+    if (tile < a.B) {
+      seq_summary(a.seq_offsets, a.flags, a.B, a.T, tile, a.info, reinterpret_cast<int64_t*>(sh));
+      return;
+    }
+    tile -= a.B;
+  }
   int b, lo, hi;
-  find_tile(a, blockIdx.x, sh, b, lo, hi);
+  find_tile(a, tile, sh, b, lo, hi);
   // the same for every lane (read from LDS after a barrier): keep them scalar
   b = __builtin_amdgcn_readfirstlane(b);
   lo = __builtin_amdgcn_readfirstlane(lo);
@@ -307,8 +317,8 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 }  // namespace
 
 hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream) {
-  if (a.T == 0) return hipSuccess;
-  const int tiles = (a.T + kTok - 1) / kTok + a.B;  // >= the per-sequence tile count
+  if (a.T == 0 && !a.info) return hipSuccess;
+  const int tiles = (a.T + kTok - 1) / kTok + a.B + (a.info ? a.B : 0);  // >= the tile count (+ summaries)
   if (bf16)
     hipLaunchKernelGGL(score_kernel<true>, dim3(tiles), dim3(256), 0, stream, a);
   else
