@@ -158,6 +158,34 @@ def time_attention(ce, stream, reps: int) -> dict:
     return out
 
 
+def achievable_peaks() -> dict:
+    """Context for the spec peaks: a 1 GiB device-to-device copy (read + write
+    bytes per second) and an 8192^3 bf16 GEMM through torch (hipBLASLt)."""
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    b = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    out = {}
+    for name, fn, work in (("device_copy_GBps", lambda: dst.copy_(src), 2.0 * n / 1e9),
+                           ("torch_bf16_gemm_8192_TFLOPs", lambda: torch.matmul(a, b), 2.0 * 8192 ** 3 / 1e12)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = round(work / (e0.elapsed_time(e1) / 10 * 1e-3), 1)
+    log(f"achievable: copy {out['device_copy_GBps']} GB/s, bf16 GEMM {out['torch_bf16_gemm_8192_TFLOPs']} TFLOP/s")
+    del src, dst, a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -244,13 +272,24 @@ def main():
     assert ce.ce_workspace_status(ws) == 0, "device status error"
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    # one event before every step as well, for the per-step statistics; the
+    # value is the total over the K steps
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ev0.record(stream)
     for i in range(args.steps):
+        sev[i].record(stream)
         step(i)
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / args.steps
-    log(f"routed block: {ms * 1e3:.1f} us/step")
+    marks = sev + [ev1]
+    step_us = [marks[i].elapsed_time(marks[i + 1]) * 1e3 for i in range(args.steps)]
+    cut = args.steps // 16  # drop the first and last 1/16 in run order, average the middle 7/8
+    mid = step_us[cut:args.steps - cut] or step_us
+    step_stats = {"median": round(float(np.median(step_us)), 2), "mean_middle_7_8": round(float(np.mean(mid)), 2),
+                  "min": round(min(step_us), 2), "max": round(max(step_us), 2)}
+    log(f"routed block: {ms * 1e3:.1f} us/step (median {step_stats['median']}, middle 7/8 "
+        f"{step_stats['mean_middle_7_8']})")
 
     # ---- per-stage launches (staged entry points on the same data) ----
     logits = torch.empty(T, device=dev)
@@ -360,6 +399,7 @@ def main():
                    "parallelism": "single GPU"},
         "kept_tokens_per_s": round(cap / (ms * 1e-3), 1),
         "block_tflops": round(block_flops / (ms * 1e-3) / 1e12, 2),
+        "step_us": step_stats,
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
         "roofline": roofline,
     }
@@ -367,6 +407,7 @@ def main():
     result["ucs_signals"]["ffn_saliency_leakage"] = ucs_ffn
     result["ucs_signals"]["layer_gap"] = ucs_gap
     result["routed_attention"] = time_attention(ce, stream, max(args.steps, 10))
+    result["achievable_peaks"] = achievable_peaks()
     if not args.no_cpu_baseline:
         n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
         log(f"oracle CPU baseline on {n_seq} sequence(s)...")
