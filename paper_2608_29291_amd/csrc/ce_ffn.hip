@@ -334,6 +334,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const bool late = wave >= 4;  // group B
 
   static_assert(kSplit == 1 || kSplit == 2, "two K halves at most (their sum is order-free)");
+  static_assert(kSplit == 1 || kMode == 1, "only the down GEMM splits K");
   const int total = n_tt * n_ft * kSplit;
   const int per = (total + kXcds - 1) / kXcds;
   const int wk = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
@@ -534,7 +535,6 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     constexpr int kSC1 = 16;  // cache-policy operand: sc1
     const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.part + (int64_t)w * 2 * (256 * 256), 2 * 256 * 256 * 4);
     const uint32_t mine = (uint32_t)kz * (256 * 256 * 4);
-    const uint32_t other = (uint32_t)(kz ^ 1) * (256 * 256 * 4);
     // register order: per lane 32 float4, one store instruction = 1 KB contiguous
 #pragma unroll
     for (int i = 0; i < kMW; ++i)
@@ -554,66 +554,143 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       arrived[0] = __hip_atomic_fetch_add(a.tile_cnt + w, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (arrived[0] == 0) return;  // first half done: the other finishes the tile
-#pragma unroll
-    for (int i = 0; i < kMW; ++i)
-#pragma unroll
-      for (int j = 0; j < kMT; ++j)
-#pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
-          const uint32_t o = (uint32_t)((((wave * 32 + (i * kMT + j) * 4 + v4) * 64) + lane) * 16);
-          const u32x4_t y = __builtin_bit_cast(
-              u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, (int)(other + o), 0, kSC1));
-          // two addends: the sum does not depend on which half came last
-          acc[i][j][4 * v4] += __uint_as_float(y.x);
-          acc[i][j][4 * v4 + 1] += __uint_as_float(y.y);
-          acc[i][j][4 * v4 + 2] += __uint_as_float(y.z);
-          acc[i][j][4 * v4 + 3] += __uint_as_float(y.w);
-        }
+    // the other half's sums are added row block by row block in the epilogue
   }
+  // adds the other K half's sums to row block j, in batches of 8 loads (32
+  // registers next to the 128 accumulators)
+  auto merge_block = [&](int j) __attribute__((always_inline)) {
+    if constexpr (kSplit == 2) {
+      const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.part + (int64_t)w * 2 * (256 * 256), 2 * 256 * 256 * 4);
+      const uint32_t other = (uint32_t)(kz ^ 1) * (256 * 256 * 4);
+#pragma unroll
+      for (int i0 = 0; i0 < kMW; i0 += 2) {
+        u32x4_t y[2][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int v4 = 0; v4 < 4; ++v4) {
+            const uint32_t o = (uint32_t)((((wave * 32 + ((i0 + i) * kMT + j) * 4 + v4) * 64) + lane) * 16);
+            y[i][v4] = __builtin_bit_cast(u32x4_t,
+                                          __builtin_amdgcn_raw_buffer_load_b128(prs, (int)(other + o), 0, 16 /* sc1 */));
+          }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int v4 = 0; v4 < 4; ++v4) {
+            // two addends: the sum does not depend on which half came last
+            acc[i0 + i][j][4 * v4] += __uint_as_float(y[i][v4].x);
+            acc[i0 + i][j][4 * v4 + 1] += __uint_as_float(y[i][v4].y);
+            acc[i0 + i][j][4 * v4 + 2] += __uint_as_float(y[i][v4].z);
+            acc[i0 + i][j][4 * v4 + 3] += __uint_as_float(y[i][v4].w);
+          }
+        // the sums are materialized here: otherwise the compiler sinks the
+        // adds to the epilogue's stores and keeps every loaded value live
+        // (spilling) until then
+        asm volatile("" : "+v"(acc[i0][j]), "+v"(acc[i0 + 1][j])::"memory");
+      }
+    }
+  };
 
+  if constexpr (kMode == 0) {
+    // SwiGLU tile staged in LDS (the rings are no longer read: group B's last
+    // fragment reads ended before the barrier group A last passed), then
+    // written out in whole cache lines. Layout: [256 token rows][128
+    // features] bf16, 16-byte chunk c of row r at chunk c ^ (r & 15).
+    // Group A stages while group B runs its last compute phase; one barrier
+    // later group B stages; after the next barrier every wave writes out.
+    char* const ost = smem;
+    auto stage = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int j = 0; j < kMT; ++j) {
-    const int jr = row_lo + wt * 64 + 32 * j + lrow;
-    if (jr >= row_hi) continue;
-    const int orow_idx = map_row(jr, a.omap1, a.omap2);
-    char* orow = a.out + (int64_t)orow_idx * a.out_ld;
-    if constexpr (kMode == 0) {
+      for (int j = 0; j < kMT; ++j) {
+        const int r = wt * 64 + 32 * j + lrow;
 #pragma unroll
-      for (int p = 0; p < kMW / 2; ++p) {
-        const int fb0_ = f0 + 32 * (ww * (kMW / 2) + p) + 4 * lhalf;
-        if (fb0_ >= n_feat) continue;
+        for (int p = 0; p < kMW / 2; ++p)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x16_t& ag = acc[2 * p][j];
-          const f32x16_t& au = acc[2 * p + 1][j];
-          float v0 = silu_f32(ag[4 * g + 0]) * au[4 * g + 0];
-          float v1 = silu_f32(ag[4 * g + 1]) * au[4 * g + 1];
-          float v2 = silu_f32(ag[4 * g + 2]) * au[4 * g + 2];
-          float v3 = silu_f32(ag[4 * g + 3]) * au[4 * g + 3];
-          store4<true>(orow + (int64_t)(fb0_ + 8 * g) * 2, v0, v1, v2, v3);
+          for (int g = 0; g < 4; ++g) {
+            const f32x16_t& ag = acc[2 * p][j];
+            const f32x16_t& au = acc[2 * p + 1][j];
+            u32x2_t v;
+            v.x = pack_bf16(silu_f32(ag[4 * g + 0]) * au[4 * g + 0], silu_f32(ag[4 * g + 1]) * au[4 * g + 1]);
+            v.y = pack_bf16(silu_f32(ag[4 * g + 2]) * au[4 * g + 2], silu_f32(ag[4 * g + 3]) * au[4 * g + 3]);
+            const int c = 4 * (2 * ww + p) + g;  // 16-byte chunk of features 8c .. 8c + 7
+            *reinterpret_cast<u32x2_t*>(ost + r * 256 + ((c ^ (r & 15)) << 4) + 8 * lhalf) = v;
+          }
+      }
+    };
+    if (!late) {
+      stage();
+      lds_barrier();
+      lds_barrier();
+    } else {
+      stage();
+      lds_barrier();
+    }
+    // write-out: wave w stores rows 32w .. 32w + 31, 4 rows (16 lanes x 16
+    // bytes each) per instruction
+    const int cc = lane & 15;
+    const bool fok = f0 + 8 * cc < n_feat;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = 32 * wave + 4 * q + (lane >> 4);
+      const int jr = row_lo + r;
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(ost + r * 256 + ((cc ^ (r & 15)) << 4));
+      if (jr < row_hi && fok)
+        *reinterpret_cast<u32x4_t*>(a.out + (int64_t)map_row(jr, a.omap1, a.omap2) * a.out_ld +
+                                    (int64_t)(f0 + 8 * cc) * 2) = v;
+    }
+  } else {
+    __builtin_amdgcn_sched_barrier(0);  // keep the residual loads out of the split-K merge above
+    char* orow[kMT];
+    const char* rrow[kMT];
+#pragma unroll
+    for (int j = 0; j < kMT; ++j) {
+      const int jr = row_lo + wt * 64 + 32 * j + lrow;
+      const int oi = jr < row_hi ? map_row(jr, a.omap1, a.omap2) : 0;
+      orow[j] = jr < row_hi ? a.out + (int64_t)oi * a.out_ld : nullptr;
+      rrow[j] = (jr < row_hi && a.res) ? a.res + (int64_t)oi * a.res_ld : nullptr;
+    }
+    // The residual rows are usually the output rows themselves (in-place
+    // scatter), so the compiler keeps every residual load behind the stores
+    // before it: all of a row block's residual values are loaded before its
+    // first store (each lane reads and writes only its own elements).
+#pragma unroll
+    for (int j = 0; j < kMT; ++j) {
+      if (!orow[j]) continue;
+      // residual loads first: their latency overlaps the merge's
+      u32x2_t rv[kMW][4];
+      if (rrow[j]) {
+#pragma unroll
+        for (int i = 0; i < kMW; ++i) {
+          const int fb0_ = f0 + ww * 128 + 32 * i + 4 * lhalf;
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            rv[i][g] = fb0_ < n_feat ? *reinterpret_cast<const u32x2_t*>(rrow[j] + (int64_t)(fb0_ + 8 * g) * 2)
+                                     : u32x2_t{0u, 0u};
         }
       }
-    } else {
-      const char* rrow = a.res ? a.res + (int64_t)orow_idx * a.res_ld : nullptr;
+      merge_block(j);
 #pragma unroll
       for (int i = 0; i < kMW; ++i) {
         const int fb0_ = f0 + ww * 128 + 32 * i + 4 * lhalf;
         if (fb0_ >= n_feat) continue;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int f = fb0_ + 8 * g;
           float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
           float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-          if (rrow) {
-            f32x4_t rr = load4<true>(rrow + (int64_t)f * 2);
-            v0 += rr.x; v1 += rr.y; v2 += rr.z; v3 += rr.w;
+          if (rrow[j]) {
+            v0 += bf16_to_f32(rv[i][g].x & 0xffffu);
+            v1 += bf16_to_f32(rv[i][g].x >> 16);
+            v2 += bf16_to_f32(rv[i][g].y & 0xffffu);
+            v3 += bf16_to_f32(rv[i][g].y >> 16);
           }
-          store4<true>(orow + (int64_t)f * 2, v0, v1, v2, v3);
+          store4<true>(orow[j] + (int64_t)(fb0_ + 8 * g) * 2, v0, v1, v2, v3);
         }
       }
     }
   }
-  if (kSplit == 1 && !late) lds_barrier();  // matches group B's extra barrier at the start
+  // group A's extra barrier at the end matches group B's at the start (the
+  // gate/up path above already ends in step)
+  if (kMode == 1 && kSplit == 1 && !late) lds_barrier();
 }
 
 __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, int n) {
