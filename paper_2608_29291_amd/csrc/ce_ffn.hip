@@ -379,7 +379,11 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const __amdgpu_buffer_rsrc_t wr0 = make_rsrc(a.w0[set], (uint32_t)(n_feat * a.w_ld));
   const __amdgpu_buffer_rsrc_t wr1 =
       (kMode == 0) ? make_rsrc(a.w1[set], (uint32_t)(n_feat * a.w_ld)) : wr0;
-  const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, 0xffffffffu);
+  // Token rows past the tile's last packed row (the final token tile is
+  // partial) are fetched from past the resource's end: zeros and no memory
+  // traffic. Their MFMAs then multiply zeros, which draws less power than
+  // real data, and the clock is power-bound under MFMA load.
+  const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, (uint32_t)(a.tok_rows * a.tok_ld));
   uint32_t voff[8];
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
@@ -391,9 +395,8 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       else feat = f0 + r;
       voff[q] = (uint32_t)((int64_t)feat * a.w_ld + c * 16);
     } else {
-      int j = row_lo + r;
-      j = j < row_hi ? j : row_hi - 1;
-      voff[q] = (uint32_t)((int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + c * 16);
+      const int j = row_lo + r;
+      voff[q] = j < row_hi ? (uint32_t)((int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + c * 16) : 0x80000000u;
     }
   }
   // weight row block (64 w + 8 q) / 32 has the parity of q / 4: the gate / up
