@@ -758,12 +758,19 @@ hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
 //            for d < 3072 and 128 x 128 (2 x 2 waves) for the 7B width,
 //            token-tile-major order (every weight tile of a token tile stays in
 //            one XCD's L2).
-// fp32 data (tiny workloads) uses 128 x 128 tiles.
+// fp32 data (tiny workloads) uses 128 x 128 tiles, or smaller ones when those
+// would leave most of the chip idle (fp32 MFMAs run at 1/16 of the bf16 rate,
+// so a handful of large tiles would each take tens of microseconds).
+inline int64_t grid_tiles(const FfnGemmArgs& a, int feat_tile, int tok_tile) {
+  return (int64_t)((a.cap + tok_tile - 1) / tok_tile + a.n_sets - 1) * ((a.n_feat + feat_tile - 1) / feat_tile);
+}
+
 hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
   if (bf16) {
     if (pp2_ok(a)) return launch_pp2<0, 8, true>(a, stream);
     return launch_cfg<true, 0, 256, 256, 4, 2, 1, 1, 4>(a, stream);
   }
+  if (grid_tiles(a, 64, 128) < 128) return launch_cfg<false, 0, 64, 64, 1, 2, 2>(a, stream);
   return launch_cfg<false, 0, 128, 128, 2, 2, 2>(a, stream);
 }
 
@@ -785,6 +792,7 @@ hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, 
     if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2, 1, 64>(a, stream);
     return launch_cfg<true, 1, 128, 128, 2, 2, 2, 1, 64>(a, stream);
   }
+  if (grid_tiles(a, 128, 128) < 128) return launch_cfg<false, 1, 32, 32, 1, 1, 2>(a, stream);
   return launch_cfg<false, 1, 128, 128, 2, 2, 2>(a, stream);
 }
 
