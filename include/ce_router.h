@@ -269,6 +269,26 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                     size_t ws_bytes, void* stream);
 
 /*
+ * Host query: how the routing logits (section 3.2, Eq. 4) are computed for
+ * this batch. ce_score runs the single-launch scorer: tiles of 32 or 128
+ * tokens of one sequence, each streaming every active rank of W1 (128 for
+ * bf16 batches large enough that 32-token tiles would need several rounds of
+ * workgroups). For large bf16 batches with many ranks, ce_routed_block
+ * instead scores tiles of tm tokens x tn ranks (tm, tn in {64, 128}; a tile
+ * covers core or expansion ranks, never both), each writing per-token
+ * partial sums of w2 . SiLU(W1 h + b1) over its ranks into the workspace,
+ * and the TopK step assembles the logits from them in a fixed order (core
+ * tiles, b2_core, then for generation tokens the expansion tiles and
+ * b2_exp[m]). The choice depends only on B, T, d, r_core, r_exp and dtype.
+ *   tile_out  host int32 [2] or NULL: {tm, tn} of the block's rank tiles, or
+ *             {token tile, 0} for the single-launch scorer
+ * Returns 1 (rank-tiled block), 0 (single-launch scorer) or a negative
+ * status for an invalid batch or scorer description (device pointers are not
+ * read).
+ */
+int ce_score_tiling(const ce_batch* batch, const ce_scorer_w* scorer, int32_t* tile_out);
+
+/*
  * Drop-set stability between two timesteps (section 3.4, UCS operators (3)
  * diffusion-head cache reuse and (4) denoising-step early exit; Eq. 10-11).
  * For each sequence b the drop set D of a timestep is its routable tokens

@@ -38,7 +38,7 @@ EXPORTED = [
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
-    "ce_routed_attention",
+    "ce_routed_attention", "ce_score_tiling",
 ]
 
 
@@ -118,6 +118,7 @@ _sig("ce_ffn_saliency", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctyp
                                        ctypes.c_float, _p, _p, _p, _p, ctypes.c_size_t, _p])
 _sig("ce_ffn_mask_channels", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p])
 _sig("ce_routed_attention", ctypes.c_int, [ctypes.POINTER(CEAttn), _p, _p, _p, _p, _p])
+_sig("ce_score_tiling", ctypes.c_int, [ctypes.POINTER(CEBatch), ctypes.POINTER(CEScorerW), _p])
 _sig("ce_layer_gap", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, ctypes.c_float,
                                     _p, _p, _p, _p, _p, _p])
 
@@ -318,6 +319,17 @@ def ce_routed_block(batch: Batch, hidden_in, hidden_out, scorer: Scorer, ffn: FF
                                ctypes.byref(sw), ctypes.byref(fw), _dev_ptr(logits_out),
                                _dev_ptr(kept_idx_out), _dev_ptr(kept_offsets_out), _dev_ptr(ws),
                                ws.numel(), _stream(stream)), "ce_routed_block")
+
+
+def ce_score_tiling(batch: Batch, scorer: Scorer):
+    """(tm, tn) of the rank-tiled scorer ce_routed_block uses for this batch,
+    or (token_tile, 0) for the single-launch scorer (host query, no GPU work)."""
+    cb, sw = batch.c(), scorer.c()
+    out = (ctypes.c_int32 * 2)()
+    r = lib.ce_score_tiling(ctypes.byref(cb), ctypes.byref(sw), out)
+    if r < 0:
+        _check(r, "ce_score_tiling")
+    return int(out[0]), int(out[1])
 
 
 def ce_drop_stability(batch: Batch, token_pos_t, token_pos_ref, jaccard, j_rand=None, rda=None,

@@ -34,7 +34,7 @@ T* at(void* ws, size_t off) {
 ScoreArgs make_score_args(const ce_batch* b, const void* hidden, const ce_scorer_w* w, float* logits,
                           float* probs) {
   const int elem = elem_size(w->dtype);
-  ScoreArgs a;
+  ScoreArgs a{};
   a.hidden = static_cast<const char*>(hidden);
   a.h_ld = (int64_t)w->d * elem;
   a.k_bytes = w->d * elem;
@@ -191,7 +191,7 @@ int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidd
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* info = at<int32_t>(ws, L.seq_info);
   CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));
-  SelectArgs sa;
+  SelectArgs sa{};
   sa.logits = logits;
   sa.flags = batch->flags;
   sa.info = info;
@@ -304,13 +304,35 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   int32_t* token_pos = at<int32_t>(ws, L.token_pos);
   int32_t* info = at<int32_t>(ws, L.seq_info);
 
-  // 1. routing logits (Eq. 4); the same launch writes the per-sequence summaries
+  // 1. routing logits (Eq. 4); the same launch writes the per-sequence
+  //    summaries. bf16: rank-tiled partial logits when that moves fewer
+  //    bytes per workgroup; the TopK step adds them up.
   ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
   sa.info = info;
-  CE_TRY(launch_score(sa, bf16, s));
+  int tm = 0, tn = 0;
+  const bool tiled = bf16 && score_tiling(batch->B, batch->T, scorer->d, scorer->r_core, scorer->r_exp, elem,
+                                          &tm, &tn, &sa.n_ct, &sa.n_rt);
+  if (tiled) {
+    sa.part = at<float>(ws, L.score_part);
+    CE_TRY(launch_score_tiles(sa, tm, tn, s));
+  } else {
+    CE_TRY(launch_score(sa, bf16, s));
+  }
   // 2-3. per-sequence TopK + packed index maps (Eq. 6)
-  SelectArgs sel;
+  SelectArgs sel{};
   sel.logits = logits;
+  if (tiled) {
+    sel.part = sa.part;
+    sel.logits_w = logits;
+    sel.n_ct = sa.n_ct;
+    sel.n_rt = sa.n_rt;
+    sel.T = batch->T;
+    sel.r_exp = scorer->r_exp;
+    sel.n_seg = scorer->n_seg;
+    sel.b2c = scorer->b2_core;
+    sel.b2e = scorer->b2_exp;
+    sel.t = batch->t;
+  }
   sel.flags = batch->flags;
   sel.info = info;
   sel.B = batch->B;
@@ -348,6 +370,20 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   // 5. down projection + residual, scattered straight into the token rows
   CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
   return CE_OK;
+}
+
+int ce_score_tiling(const ce_batch* batch, const ce_scorer_w* scorer, int32_t* tile_out) {
+  if (!batch || batch->B < 1 || batch->T < 0) return CE_ERR_INVALID_ARG;
+  CE_CHECK(check_scorer(scorer));
+  int tm = 0, tn = 0, n_ct = 0, n_rt = 0;
+  const int elem = elem_size(scorer->dtype);
+  const int tiled = score_tiling(batch->B, batch->T, scorer->d, scorer->r_core, scorer->r_exp, elem, &tm, &tn,
+                                 &n_ct, &n_rt);
+  if (tile_out) {
+    tile_out[0] = tiled ? tm : score_token_tile(batch->B, batch->T, scorer->d, scorer->r_core, scorer->r_exp, elem);
+    tile_out[1] = tiled ? tn : 0;
+  }
+  return tiled;
 }
 
 int ce_drop_stability(const ce_batch* batch, const int32_t* token_pos_t,

@@ -27,6 +27,57 @@ int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem) {
   return tiles <= kSplitMaxTiles ? (int)tiles : 0;
 }
 
+int score_token_tile(int B, int T, int d, int r_core, int r_exp, int elem) {
+  const int r = r_core + (r_exp > 0 ? r_exp : 0);
+  if (elem != 2 || B < 1 || T < 1 || d < 1 || r > 384) return 32;
+  auto rounds = [](int64_t items) { return (items + 255) / 256; };
+  const int64_t c32 = rounds(((int64_t)T + 31) / 32) * (32 + r);
+  const int64_t c128 = rounds(((int64_t)T + 127) / 128) * (128 + r);
+  return c128 < c32 ? 128 : 32;
+}
+
+int score_tiling(int B, int T, int d, int r_core, int r_exp, int elem, int* tm, int* tn, int* n_ct, int* n_rt) {
+  if (elem != 2 || B < 1 || T < 1 || d < 1 || r_core < 32) return 0;
+  auto rounds = [](int64_t items) { return (items + 255) / 256; };
+  // The host sees neither the always-kept nor the generation tokens, so both
+  // costs count every token as scored, once with the expansion ranks active
+  // (generation batches) and once without (understanding batches, where the
+  // expansion tiles exit at once); the rank tiles must win both ways.
+  auto single = [&](int re) {
+    // the single-launch kernel: tiles of t1 tokens x every active rank; with
+    // only two slabs in its LDS ring (stages over 48 KB: 128 tokens + more
+    // than 256 ranks) a slab lands while the previous one is multiplied,
+    // measured about 1.5x slower per byte than the deeper rings
+    const int t1 = score_token_tile(B, T, d, r_core, r_exp, elem);
+    const int r = r_core + re;
+    int64_t c = rounds(((int64_t)T + t1 - 1) / t1) * (t1 + r);
+    if ((t1 + r) * 128 > 48 * 1024) c = c * 3 / 2;
+    return c;
+  };
+  auto tiled = [&](int m, int rt, int re) {
+    const int ct = (r_core + rt - 1) / rt;
+    const int et = re > 0 ? (re + rt - 1) / rt : 0;
+    return rounds(((int64_t)T + m - 1) / m * (ct + et)) * (m + rt);
+  };
+  int64_t best = -1;
+  for (int m = 64; m <= 128; m += 64)
+    for (int rt = 64; rt <= 128; rt += 64) {
+      const int ct = (r_core + rt - 1) / rt;
+      const int et = r_exp > 0 ? (r_exp + rt - 1) / rt : 0;
+      if (ct + et > kScoreMaxTiles) continue;
+      const int64_t cost = tiled(m, rt, r_exp);
+      if (best < 0 || cost < best) {
+        best = cost;
+        *tm = m;
+        *tn = rt;
+        *n_ct = ct;
+        *n_rt = ct + et;
+      }
+    }
+  if (best < 0) return 0;
+  return best < single(r_exp) && tiled(*tm, *tn, 0) < single(0);
+}
+
 WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) {
   WsLayout L;
   memset(&L, 0, sizeof(L));
@@ -47,6 +98,7 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
     L.kept_idx = take(sC * 4);
     L.token_pos = take(sT * 4);
     L.logits = take(sT * 4);
+    L.score_part = take((size_t)kScoreMaxTiles * sT * 4);
   }
   if (which == CE_WS_FFN || which == CE_WS_BLOCK) {
     L.grp_rows = take(sC * 4);

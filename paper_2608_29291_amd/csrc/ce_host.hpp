@@ -22,6 +22,7 @@ struct WsLayout {
   size_t kept_idx;   // int32 [cap]    (block path)
   size_t token_pos;  // int32 [T]      (block path)
   size_t logits;     // float [T]      (block path)
+  size_t score_part; // float [kScoreMaxTiles x T] rank-tiled scorer partial logits (block path)
   size_t grp_rows;   // int32 [cap]    (MoT grouping)
   size_t grp_n0;     // int32          (MoT group size)
   size_t act;        // dtype [cap * d_ff] SwiGLU activations
@@ -43,6 +44,23 @@ constexpr int kSplitMaxTiles = 128;
 // many workgroups (partial sums in the workspace, summed in a fixed order).
 constexpr int kSalSplits = 16;
 int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem);
+
+// Token tile of the single-launch scorer: 32, or (bf16, r_core + r_exp <=
+// 384) 128 when that takes fewer rounds of 256 workgroups x rows of K each
+// workgroup streams (tile tokens + every rank; the expansion ranks counted
+// whenever r_exp > 0). 128-token tiles move the W1 rows once per 128 tokens
+// instead of once per 32.
+int score_token_tile(int B, int T, int d, int r_core, int r_exp, int elem);
+
+// The fused block's rank-tiled scorer (bf16): tiles of tm tokens x tn ranks,
+// tm, tn in {64, 128}, with n_ct core and n_rt - n_ct expansion rank tiles,
+// writing partial logits that the TopK step assembles. Chosen (returns 1)
+// when it takes fewer rounds of 256 workgroups x rows of K per workgroup than
+// the single-launch scorer with score_token_tile's tile (weighted 1.5x when
+// only two of its slabs fit in LDS), counting every token as scored, both
+// with the expansion ranks active and without them.
+constexpr int kScoreMaxTiles = 10;  // ceil(r_core / 64) + ceil(r_exp / 64) with r_core + r_exp <= 512
+int score_tiling(int B, int T, int d, int r_core, int r_exp, int elem, int* tm, int* tn, int* n_ct, int* n_rt);
 
 int elem_size(int dtype);  // 2 for bf16, 4 for f32, 0 if unknown
 

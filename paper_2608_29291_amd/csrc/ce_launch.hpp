@@ -71,8 +71,15 @@ struct ScoreArgs {
   float* logits;
   float* probs;
   int32_t* info;  // if set, B extra workgroups also write the per-sequence summary (seq_info layout)
+  // rank-tiled scorer only: per-token partial logits [n_rt x T], rank tiles
+  // 0 .. n_ct - 1 over the core ranks, the rest over the expansion ranks
+  float* part;
+  int n_ct, n_rt;
 };
 hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream);
+// Rank-tiled scorer (bf16): tiles of tm tokens x tn ranks (tm, tn in {64, 128})
+// write per-token partial logits to a.part; the TopK step adds them up.
+hipError_t launch_score_tiles(const ScoreArgs& a, int tm, int tn, hipStream_t stream);
 
 // Per-sequence summary written by the count kernel: {lo, len, keep_count | bad<<31}.
 hipError_t launch_seq_info(const int32_t* seq_offsets, const uint8_t* flags, int B, int T,
@@ -80,6 +87,15 @@ hipError_t launch_seq_info(const int32_t* seq_offsets, const uint8_t* flags, int
 
 struct SelectArgs {
   const float* logits;
+  // When part is set, the logits are first assembled from the rank-tiled
+  // scorer's partial sums [n_rt x T] (fixed order: core tiles, b2c, then for
+  // generation tokens the expansion tiles and b2e[m]) and written to logits_w.
+  const float* part;
+  float* logits_w;
+  int n_ct, n_rt, T, r_exp, n_seg;
+  float b2c;
+  const float* b2e;
+  const float* t;
   const uint8_t* flags;
   const int32_t* info;
   int B;

@@ -26,15 +26,14 @@
 
 #include "ce_device.hpp"
 #include "ce_launch.hpp"
+#include "ce_host.hpp"
 #include "ce_router.h"
 
 namespace ce {
 
 namespace {
 
-constexpr int kTok = 32;         // tokens per tile
 constexpr int kSlabRow = 128;    // bytes of K per staged row
-constexpr int kLds = 152 * 1024;  // ring bytes (the rest of the 160 KB holds the small arrays)
 constexpr int kMaxBlocks = 16;   // (r_core + r_exp) / 32 <= 512 / 32
 
 // s_waitcnt with a run-time vmcnt (0..63): the immediate is chosen by a switch.
@@ -57,11 +56,13 @@ __device__ __forceinline__ void wait_vm(int n) {
   else wait_vm_upto<48>(n);
 }
 
-// Locate tile `tile` among the per-sequence tilings: sequence b, tokens [lo, hi).
+// Locate tile `tile` among the per-sequence tilings into kTile tokens:
+// sequence b, tokens [lo, hi).
 // The offsets are read into LDS 256 sequences at a time (one load per thread),
 // then every thread walks them: one memory latency plus a few LDS reads per
 // sequence.
-__device__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo, int& hi) {
+template <int kTile>
+__device__ __forceinline__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo, int& hi) {
   const int tid = threadIdx.x;
   int base = 0;  // tiles before the current chunk of sequences
   b = -1;
@@ -77,11 +78,11 @@ __device__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo
     for (int j = 0; j < cnt; ++j) {
       int se = sh[j + 1];
       se = se < prev ? prev : se;
-      const int nt = (se - prev + kTok - 1) / kTok;
+      const int nt = (se - prev + kTile - 1) / kTile;
       if (b < 0 && tile < base + nt) {
         b = s0 + j;
-        lo = prev + (tile - base) * kTok;
-        hi = min(lo + kTok, se);
+        lo = prev + (tile - base) * kTile;
+        hi = min(lo + kTile, se);
       }
       base += nt;
       prev = se;
@@ -91,11 +92,17 @@ __device__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo
   }
 }
 
-template <bool kBF16>
+template <bool kBF16, int kTM>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
+  static_assert(kTM == 32 || kTM == 128, "token tiles of 32 or 128");
+  constexpr int MB = kTM / 32;  // token blocks of the tile
+  // ring bytes: the rest of the 160 KB holds the small arrays (more of them
+  // for 128-token tiles)
+  constexpr int kLds = kTM == 32 ? 152 * 1024 : 144 * 1024;
   __shared__ __attribute__((aligned(1024))) char smem[kLds];
   __shared__ __attribute__((aligned(8))) int sh[260];  // also the summary's int64 scratch
-  __shared__ float red[4][2][kTok];
+  __shared__ float red[4][2][kTM];
+  __shared__ uint8_t keep_s[kTM];
   __shared__ float ep[4][kMaxBlocks / 4][64];  // per wave and block: b1 (32 ranks), w2 (32 ranks)
 
   const int tid = threadIdx.x;
@@ -113,7 +120,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
     tile -= a.B;
   }
   int b, lo, hi;
-  find_tile(a, tile, sh, b, lo, hi);
+  find_tile<kTM>(a, tile, sh, b, lo, hi);
   // the same for every lane (read from LDS after a barrier): keep them scalar
   b = __builtin_amdgcn_readfirstlane(b);
   lo = __builtin_amdgcn_readfirstlane(lo);
@@ -128,6 +135,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
     kp = (f & CE_TOK_KEEP) != 0;
     gen = ((f & CE_TOK_GEN) != 0) && !kp;
   }
+  if (tid < kTM) keep_s[tid] = kp ? 1 : 0;
   const int any_scored = __syncthreads_or(!kp);
   const bool any_gen = __syncthreads_or(gen) && a.r_exp > 0;
   if (!any_scored) {
@@ -146,12 +154,14 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   }
   const int nbc = a.r_core / 32;
   const int nb = nbc + (any_gen ? a.r_exp / 32 : 0);  // weight blocks of this tile (<= 16)
-  const int stage = (kTok + 32 * nb) * kSlabRow;
+  const int stage = (kTM + 32 * nb) * kSlabRow;
   // two slabs in flight: deeper rings measured slower (the extra LDS DMA in
-  // flight only adds queueing)
-  int nstage = kLds / stage;         // >= 2: a stage is at most (32 + 512) x 128 B = 68 KB
+  // flight only adds queueing); a stage is at most (32 + 512) x 128 B = 68 KB
+  // for 32-token tiles and (128 + 384) x 128 B = 64 KB for 128-token tiles
+  // (the launcher takes those only for r_core + r_exp <= 384)
+  int nstage = kLds / stage;
   nstage = nstage > 3 ? 3 : nstage;
-  const int per_slab = 1 + nb;       // DMA instructions per wave per slab
+  const int per_slab = MB + nb;      // DMA instructions per wave per slab
 
   // ---- DMA plan: instruction i of a slab covers stage rows 8i .. 8i + 7 and
   //      belongs to wave i % 4: wave w fetches token rows 8w .. 8w + 7 and rows
@@ -159,10 +169,14 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int r8 = lane >> 3;
   const int pch = lane & 7;
   const int trow = 8 * wave + r8;  // this lane's row inside a 32-row block
-  const bool tlive = trow < n && !(a.flags[lo + (trow < n ? trow : 0)] & CE_TOK_KEEP);
   const uint32_t chunk_off = (uint32_t)((pch ^ ((trow >> 1) & 7)) << 4);
   // rows that are never scored read past the resource end: zeros, no traffic
-  const uint32_t t_voff = tlive ? (uint32_t)(trow * a.h_ld) + chunk_off : 0x7ffffff0u;
+  uint32_t t_voff[MB];
+#pragma unroll
+  for (int j = 0; j < MB; ++j) {
+    const int r = 32 * j + trow;
+    t_voff[j] = (r < n && !keep_s[r]) ? (uint32_t)(r * a.h_ld) + chunk_off : 0x7ffffff0u;
+  }
   const uint32_t w_voff = (uint32_t)(trow * a.h_ld) + chunk_off;
   const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.hidden + (int64_t)lo * a.h_ld, (uint32_t)(n * a.h_ld));
   const __amdgpu_buffer_rsrc_t crs = make_rsrc(a.w1c, (uint32_t)(a.r_core * a.h_ld));
@@ -186,13 +200,16 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
     int ks = kb + rot;
     ks = ks >= nk_all ? ks - nk_all : ks;
     const int soff = ks * kSlabRow;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, st + 8 * wave * kSlabRow, 16, (int)t_voff, soff, 0, 0);
+#pragma unroll
+    for (int j = 0; j < MB; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, st + (32 * j + 8 * wave) * kSlabRow, 16, (int)t_voff[j], soff, 0,
+                                               0);
     // one loop per weight matrix: each instruction's resource is fixed
     for (int blk = 0; blk < nbc; ++blk)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(crs, st + (kTok + 32 * blk + 8 * wave) * kSlabRow, 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(crs, st + (kTM + 32 * blk + 8 * wave) * kSlabRow, 16,
                                                (int)w_voff, soff + (int)(32 * blk * a.h_ld), 0, 0);
     for (int blk = nbc; blk < nb; ++blk)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ers, st + (kTok + 32 * blk + 8 * wave) * kSlabRow, 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ers, st + (kTM + 32 * blk + 8 * wave) * kSlabRow, 16,
                                                (int)w_voff, soff + (int)(32 * (blk - nbc) * a.h_ld), 0, 0);
   };
 
@@ -221,14 +238,21 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   }
   const int pre = min(nk, nstage - 1);
   for (int s = 0; s < pre; ++s) dma(s, s);
-  float pc = 0.0f, pe = 0.0f;
+  float pc[MB], pe[MB];
+#pragma unroll
+  for (int j = 0; j < MB; ++j) pc[j] = pe[j] = 0.0f;
   auto run = [&](auto nbw_c) __attribute__((always_inline)) {
     constexpr int NBW = decltype(nbw_c)::value;
-    // two accumulators per block (even and odd K steps) halve the chain of
-    // dependent MFMAs; they are added before the epilogue
-    f32x16_t acc[NBW > 0 ? NBW : 1][2];
+    // a 32-token tile keeps two accumulators per block (even and odd K steps),
+    // halving the chain of dependent MFMAs; they are added before the epilogue
+    constexpr int NACC = MB == 1 ? 2 : 1;
+    f32x16_t acc[NBW > 0 ? NBW : 1][MB][NACC];
 #pragma unroll
-    for (int i = 0; i < NBW; ++i) acc[i][0] = acc[i][1] = f32x16_t{};
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int j = 0; j < MB; ++j)
+#pragma unroll
+        for (int e = 0; e < NACC; ++e) acc[i][j][e] = f32x16_t{};
     int buf = 0;
     for (int kb = 0; kb < nk; ++kb) {
       // slab kb must have landed; the later slabs already issued may stay in flight
@@ -237,20 +261,24 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
       lds_barrier();
       if constexpr (NBW > 0) {
         const char* st = smem + buf * stage;
-        u32x4_t fb[4], fa[4][NBW];
+        u32x4_t fb[4][MB], fa[4][NBW];
 #pragma unroll
         for (int step = 0; step < 4; ++step) {
           const uint32_t off = (((uint32_t)(2 * step + lhalf)) ^ rkey) << 4;
-          fb[step] = *reinterpret_cast<const u32x4_t*>(st + lrow * kSlabRow + off);
+#pragma unroll
+          for (int j = 0; j < MB; ++j)
+            fb[step][j] = *reinterpret_cast<const u32x4_t*>(st + (32 * j + lrow) * kSlabRow + off);
 #pragma unroll
           for (int i = 0; i < NBW; ++i)
             fa[step][i] = *reinterpret_cast<const u32x4_t*>(
-                st + (kTok + 32 * (wave + 4 * i) + lrow) * kSlabRow + off);
+                st + (kTM + 32 * (wave + 4 * i) + lrow) * kSlabRow + off);
         }
 #pragma unroll
         for (int step = 0; step < 4; ++step)
 #pragma unroll
-          for (int i = 0; i < NBW; ++i) mfma_step<kBF16>(acc[i][step & 1], fa[step][i], fb[step]);
+          for (int i = 0; i < NBW; ++i)
+#pragma unroll
+            for (int j = 0; j < MB; ++j) mfma_step<kBF16>(acc[i][j][NACC == 2 ? (step & 1) : 0], fa[step][i], fb[step][j]);
       }
       // every wave is past slab kb - 1 (the barrier above): its buffer receives
       // slab kb + nstage - 1. Issued after this slab's fragment reads, so no
@@ -269,16 +297,20 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
     for (int i = 0; i < NBW; ++i) {
       const int blk = wave + 4 * i;
       const bool hb = (blk >= nbc ? a.b1e : a.b1c) != nullptr;
-      float p = 0.0f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = 8 * (v >> 2) + 4 * lhalf + (v & 3);  // rank inside the block
-        float z = acc[i][0][v] + acc[i][1][v];
-        if (hb) z += ep[wave][i][r];
-        p += ep[wave][i][32 + r] * silu_f32(z);
+      for (int j = 0; j < MB; ++j) {
+        float p = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = 8 * (v >> 2) + 4 * lhalf + (v & 3);  // rank inside the block
+          float z = acc[i][j][0][v];
+          if constexpr (NACC == 2) z += acc[i][j][1][v];
+          if (hb) z += ep[wave][i][r];
+          p += ep[wave][i][32 + r] * silu_f32(z);
+        }
+        if (blk < nbc) pc[j] += p;
+        else pe[j] += p;
       }
-      if (blk < nbc) pc += p;
-      else pe += p;
     }
   };
   switch (nbw) {
@@ -286,13 +318,19 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
     case 1: run(std::integral_constant<int, 1>{}); break;
     case 2: run(std::integral_constant<int, 2>{}); break;
     case 3: run(std::integral_constant<int, 3>{}); break;
-    default: run(std::integral_constant<int, 4>{}); break;
+    default:
+      // 128-token tiles are launched for at most 12 rank blocks (3 per wave)
+      if constexpr (kTM == 32) run(std::integral_constant<int, 4>{});
+      break;
   }
-  pc += __shfl_xor(pc, 32);
-  pe += __shfl_xor(pe, 32);
-  if (lhalf == 0) {
-    red[wave][0][lrow] = pc;
-    red[wave][1][lrow] = pe;
+#pragma unroll
+  for (int j = 0; j < MB; ++j) {
+    pc[j] += __shfl_xor(pc[j], 32);
+    pe[j] += __shfl_xor(pe[j], 32);
+    if (lhalf == 0) {
+      red[wave][0][32 * j + lrow] = pc[j];
+      red[wave][1][32 * j + lrow] = pe[j];
+    }
   }
   __syncthreads();
   if (tid < n) {
@@ -314,15 +352,254 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   }
 }
 
+// ---- rank-tiled scorer (bf16) ----
+//
+// The single-launch kernel above streams every rank of W1 for each 32-token
+// tile, so at the 7B width (384 ranks x 7 KB) a workgroup moves 2.8 MB from
+// L2 for 32 tokens, and L2-to-CU bytes per workgroup set the time. Here a
+// workgroup owns a tile of TM tokens of one sequence x TN ranks (core or the
+// active expansion, never both) and writes, per token, the partial logit
+// sum over its ranks of w2 . SiLU(W1 h + b1); the TopK step adds the tiles'
+// partials in a fixed order. Per workgroup TM token rows and TN rank rows
+// stream through LDS by the same whole-line DMA as above; the four waves form
+// a 2 x 2 grid over the rank and token halves of the tile. Tiles without a
+// scored token, and expansion tiles without a generation token, exit at once
+// (their partials are never read). The token rows come from HBM on first
+// touch and the rank rows mostly from L2, so each operand has a ring of its
+// own: tokens run kTokRing - 1 slabs ahead, ranks kRankRing - 1.
+constexpr int kTokRing = 6;
+constexpr int kRankRing = 3;
+
+template <int TM, int TN>
+__global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
+  constexpr int MBW = TM / 64;  // token blocks per wave
+  constexpr int NBW = TN / 64;  // rank blocks per wave
+  constexpr int kTokB = TM * kSlabRow;   // one token slab
+  constexpr int kRankB = TN * kSlabRow;  // one rank slab
+  constexpr int IT = TM / 32;            // token DMA instructions per wave per slab (8 rows each)
+  constexpr int IR = TN / 32;            // rank DMA instructions per wave per slab
+  constexpr bool kTwoAcc = MBW * NBW == 1;  // a lone block keeps two accumulators (even / odd K steps)
+  constexpr int NACC = kTwoAcc ? 2 : 1;
+  __shared__ __attribute__((aligned(1024))) char smem[kTokRing * kTokB + kRankRing * kRankB];
+  __shared__ __attribute__((aligned(8))) int sh[260];
+  __shared__ float red[2][TM];
+  __shared__ float ep[4][NBW][64];
+  __shared__ uint8_t keep_s[TM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave & 1;   // rank half of the tile
+  const int wk = wave >> 1;  // token half of the tile
+
+  int item = blockIdx.x;
+  if (a.info) {
+    if (item < a.B) {
+      seq_summary(a.seq_offsets, a.flags, a.B, a.T, item, a.info, reinterpret_cast<int64_t*>(sh));
+      return;
+    }
+    item -= a.B;
+  }
+  // XCD-aware order: the rank tiles of a token tile run next to each other
+  // on one XCD (workgroup L runs on XCD L % 8), so the token rows are read
+  // from HBM once and from that XCD's L2 after
+  const int total = (a.T / TM + a.B) * a.n_rt;  // >= the number of (token tile, rank tile) items
+  const int per = (total + 7) / 8;
+  const int w = (item & 7) * per + (item >> 3);
+  if (w >= total) return;
+  const int tile = w / a.n_rt;
+  const int q = w - tile * a.n_rt;
+  int b, lo, hi;
+  find_tile<TM>(a, tile, sh, b, lo, hi);
+  b = __builtin_amdgcn_readfirstlane(b);
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  hi = __builtin_amdgcn_readfirstlane(hi);
+  if (b < 0) return;
+  const int n = hi - lo;
+
+  bool kp = true, gen = false;
+  if (tid < n) {
+    const uint8_t f = a.flags[lo + tid];
+    kp = (f & CE_TOK_KEEP) != 0;
+    gen = ((f & CE_TOK_GEN) != 0) && !kp;
+  }
+  if (tid < TM) keep_s[tid] = kp ? 1 : 0;
+  const int any_scored = __syncthreads_or(!kp);
+  const bool any_gen = __syncthreads_or(gen) && a.r_exp > 0;
+  const bool exp_tile = q >= a.n_ct;
+  if (!any_scored || (exp_tile && !any_gen)) return;
+  int m = 0;
+  if (exp_tile) {
+    const double mf = floor((double)a.n_seg * (double)a.t[b]);
+    m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
+    m = __builtin_amdgcn_readfirstlane(m);
+  }
+  const int rank0 = (exp_tile ? q - a.n_ct : q) * TN;  // first rank of the tile
+  const int nranks = exp_tile ? a.r_exp : a.r_core;
+  const int tranks = min(TN, nranks - rank0);        // ranks of this tile (> 0)
+  const char* w1 = exp_tile ? a.w1e + ((int64_t)m * a.r_exp + rank0) * a.h_ld : a.w1c + (int64_t)rank0 * a.h_ld;
+  const float* b1 = exp_tile ? (a.b1e ? a.b1e + m * a.r_exp : nullptr) : a.b1c;
+  const float* w2 = exp_tile ? a.w2e + m * a.r_exp : a.w2c;
+
+  const int lrow = lane & 31;
+  const int lhalf = lane >> 5;
+  // epilogue values of this wave's rank blocks (lane l < 32: b1 of rank l of
+  // the block, l >= 32: w2), zero for ranks past the tile's end
+  float epv[NBW];
+#pragma unroll
+  for (int i = 0; i < NBW; ++i) {
+    const int r = rank0 + 32 * (wr * NBW + i) + lrow;
+    epv[i] = 0.0f;
+    if (r - rank0 < tranks) epv[i] = lhalf ? w2[r] : (b1 ? b1[r] : 0.0f);
+  }
+
+  // ---- DMA plan: instruction i of a wave covers rows 32i + 8w .. +7 of a
+  //      token slab (i < IT) or of a rank slab ----
+  const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.hidden + (int64_t)lo * a.h_ld, (uint32_t)(n * a.h_ld));
+  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(w1, (uint32_t)(tranks * a.h_ld));
+  uint32_t tvo[IT], rvo[IR];
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    const int r = 32 * i + 8 * wave + (lane >> 3);
+    const uint32_t c = (uint32_t)(((lane & 7) ^ ((r >> 1) & 7)) << 4);
+    // rows past the tile and always-kept rows read past the resource: zeros, no traffic
+    tvo[i] = (r < n && !keep_s[r]) ? (uint32_t)(r * a.h_ld) + c : 0x7ffffff0u;
+  }
+#pragma unroll
+  for (int i = 0; i < IR; ++i) {
+    const int r = 32 * i + 8 * wave + (lane >> 3);
+    const uint32_t c = (uint32_t)(((lane & 7) ^ ((r >> 1) & 7)) << 4);
+    rvo[i] = (uint32_t)(r * a.h_ld) + c;  // ranks past the tile: past the resource
+  }
+  typedef __attribute__((address_space(3))) char lds_char;
+  lds_char* ring = (lds_char*)smem;
+  asm volatile("" : "+s"(ring));
+  const int nk = a.k_bytes / kSlabRow;
+  // each workgroup walks K from its own slab, so the workgroups running at
+  // the same time read different lines instead of the same slab column of
+  // every row (the sum order is fixed per workgroup)
+  const int rot = (int)(blockIdx.x % (unsigned)nk);
+  auto slab_off = [&](int k) __attribute__((always_inline)) {
+    int ks = k + rot;
+    ks = ks >= nk ? ks - nk : ks;
+    return k < nk ? ks * kSlabRow : 0x40000000;  // past the last slab: past the resources, zeros
+  };
+  auto dma_t = [&](int k, int st) __attribute__((always_inline)) {
+    const int so = slab_off(k);
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      lds_char* dst = ring + st * kTokB + (32 * i + 8 * wave) * kSlabRow;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, dst, 16, (int)tvo[i], so, 0, 0);
+    }
+  };
+  auto dma_r = [&](int k, int st) __attribute__((always_inline)) {
+    const int so = slab_off(k);
+#pragma unroll
+    for (int i = 0; i < IR; ++i) {
+      lds_char* dst = ring + kTokRing * kTokB + st * kRankB + (32 * i + 8 * wave) * kSlabRow;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, dst, 16, (int)rvo[i], so, 0, 0);
+    }
+  };
+
+  f32x16_t acc[NBW][MBW][NACC];
+#pragma unroll
+  for (int i = 0; i < NBW; ++i)
+#pragma unroll
+    for (int j = 0; j < MBW; ++j)
+#pragma unroll
+      for (int e = 0; e < NACC; ++e) acc[i][j][e] = f32x16_t{};
+
+  // Issue order: iteration k issues token slab k + kTokRing - 1, then rank
+  // slab k + kRankRing - 1; the prologue runs the same pattern for
+  // k = -(kTokRing - 1) .. -1 (negative slabs skipped). Operations complete
+  // in order and rank slab k is issued after token slab k, so "slab k has
+  // landed" is "at most (kRankRing - 2) iterations' operations are in flight".
+  for (int k = -(kTokRing - 1); k < 0; ++k) {
+    dma_t(k + kTokRing - 1, k + kTokRing - 1);
+    if (k + kRankRing - 1 >= 0) dma_r(k + kRankRing - 1, k + kRankRing - 1);
+  }
+  const uint32_t rkey = (uint32_t)((lrow >> 1) & 7);
+  int tst = 0, rst = 0;  // ring stages of slab k
+  for (int k = 0; k < nk; ++k) {
+    wait_vmcnt<(kRankRing - 2) * (IT + IR)>();
+    lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    const char* sa = smem + kTokRing * kTokB + rst * kRankB;
+    const char* sb = smem + tst * kTokB;
+    u32x4_t fa[4][NBW], fb[4][MBW];
+#pragma unroll
+    for (int step = 0; step < 4; ++step) {
+      const uint32_t off = (((uint32_t)(2 * step + lhalf)) ^ rkey) << 4;
+#pragma unroll
+      for (int i = 0; i < NBW; ++i)
+        fa[step][i] = *reinterpret_cast<const u32x4_t*>(sa + (32 * (wr * NBW + i) + lrow) * kSlabRow + off);
+#pragma unroll
+      for (int j = 0; j < MBW; ++j)
+        fb[step][j] = *reinterpret_cast<const u32x4_t*>(sb + (32 * (wk * MBW + j) + lrow) * kSlabRow + off);
+    }
+    // every wave is past slab k - 1 (the barrier above): its stages receive
+    // token slab k + kTokRing - 1 and rank slab k + kRankRing - 1
+    dma_t(k + kTokRing - 1, tst == 0 ? kTokRing - 1 : tst - 1);
+    dma_r(k + kRankRing - 1, rst == 0 ? kRankRing - 1 : rst - 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int step = 0; step < 4; ++step)
+#pragma unroll
+      for (int i = 0; i < NBW; ++i)
+#pragma unroll
+        for (int j = 0; j < MBW; ++j) mfma_step<true>(acc[i][j][kTwoAcc ? (step & 1) : 0], fa[step][i], fb[step][j]);
+    tst = tst + 1 == kTokRing ? 0 : tst + 1;
+    rst = rst + 1 == kRankRing ? 0 : rst + 1;
+  }
+  wait_vmcnt<0>();  // the slabs issued past the end (zeros) land before the workgroup ends
+
+  // ---- epilogue: b1, SiLU, w2 over this wave's ranks; the two rank halves
+  //      meet in LDS in a fixed order ----
+#pragma unroll
+  for (int i = 0; i < NBW; ++i) ep[wave][i][lane] = epv[i];
+#pragma unroll
+  for (int j = 0; j < MBW; ++j) {
+    float p = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = 8 * (v >> 2) + 4 * lhalf + (v & 3);  // rank inside the block
+        float z = acc[i][j][0][v];
+        if constexpr (kTwoAcc) z += acc[i][j][NACC - 1][v];
+        p += ep[wave][i][32 + r] * silu_f32(z + ep[wave][i][r]);
+      }
+    p += __shfl_xor(p, 32);
+    if (lhalf == 0) red[wr][32 * (wk * MBW + j) + lrow] = p;
+  }
+  __syncthreads();
+  if (tid < n) a.part[(int64_t)q * a.T + lo + tid] = red[0][tid] + red[1][tid];
+}
+
 }  // namespace
 
 hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream) {
   if (a.T == 0 && !a.info) return hipSuccess;
-  const int tiles = (a.T + kTok - 1) / kTok + a.B + (a.info ? a.B : 0);  // >= the tile count (+ summaries)
-  if (bf16)
-    hipLaunchKernelGGL(score_kernel<true>, dim3(tiles), dim3(256), 0, stream, a);
+  const int tm = score_token_tile(a.B, a.T, a.k_bytes / (bf16 ? 2 : 4), a.r_core, a.r_exp, bf16 ? 2 : 4);
+  const int tiles = (a.T + tm - 1) / tm + a.B + (a.info ? a.B : 0);  // >= the tile count (+ summaries)
+  if (bf16 && tm == 128)
+    hipLaunchKernelGGL((score_kernel<true, 128>), dim3(tiles), dim3(256), 0, stream, a);
+  else if (bf16)
+    hipLaunchKernelGGL((score_kernel<true, 32>), dim3(tiles), dim3(256), 0, stream, a);
   else
-    hipLaunchKernelGGL(score_kernel<false>, dim3(tiles), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((score_kernel<false, 32>), dim3(tiles), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_tiles(const ScoreArgs& a, int tm, int tn, hipStream_t stream) {
+  if (!a.part || a.n_rt <= 0) return hipErrorInvalidValue;
+  const int items = (a.T / tm + a.B) * a.n_rt;
+  const int grid = (a.info ? a.B : 0) + (items + 7) / 8 * 8;
+  if (tm == 64 && tn == 64) hipLaunchKernelGGL((score_tile_kernel<64, 64>), dim3(grid), dim3(256), 0, stream, a);
+  else if (tm == 128 && tn == 64) hipLaunchKernelGGL((score_tile_kernel<128, 64>), dim3(grid), dim3(256), 0, stream, a);
+  else if (tm == 64 && tn == 128) hipLaunchKernelGGL((score_tile_kernel<64, 128>), dim3(grid), dim3(256), 0, stream, a);
+  else if (tm == 128 && tn == 128) hipLaunchKernelGGL((score_tile_kernel<128, 128>), dim3(grid), dim3(256), 0, stream, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

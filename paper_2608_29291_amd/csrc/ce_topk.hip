@@ -49,6 +49,33 @@ __device__ void select_body(const SelectArgs& a, SelShared& sh, int lo, int len,
   const int wave = tid >> 6;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
+  // ---- logits from the rank-tiled scorer's partial sums (fixed order) ----
+  float b2e_m = 0.0f;
+  if (a.part && a.r_exp > 0 && a.b2e) {
+    const double mf = floor((double)a.n_seg * (double)a.t[blockIdx.x]);
+    const int m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
+    b2e_m = a.b2e[m];
+  }
+  auto assemble = [&](int i) -> float {
+    const uint8_t f = a.flags[lo + i];
+    if (f & 2) return __builtin_inff();
+    const float* pp = a.part + lo + i;
+    float l = pp[0];
+    for (int qq = 1; qq < a.n_ct; ++qq) l += pp[(int64_t)qq * a.T];
+    l += a.b2c;
+    if ((f & 1) && a.r_exp > 0) {
+      float e = pp[(int64_t)a.n_ct * a.T];
+      for (int qq = a.n_ct + 1; qq < a.n_rt; ++qq) e += pp[(int64_t)qq * a.T];
+      l += e + b2e_m;
+    }
+    return l;
+  };
+  if (!kLds && a.part) {
+    for (int i = tid; i < len; i += kSelThreads) a.logits_w[lo + i] = assemble(i);
+    __threadfence_block();
+    __syncthreads();
+  }
+
   // ---- keys ----
   if constexpr (kLds) {
     for (int base = 0; base < len; base += kSelThreads) {
@@ -56,7 +83,14 @@ __device__ void select_body(const SelectArgs& a, SelShared& sh, int lo, int len,
       bool kp = false;
       if (i < len) {
         kp = (a.flags[lo + i] & 2) != 0;
-        sh.keys[i] = logit_key(a.logits[lo + i]);
+        float l;
+        if (a.part) {
+          l = assemble(i);
+          a.logits_w[lo + i] = l;
+        } else {
+          l = a.logits[lo + i];
+        }
+        sh.keys[i] = logit_key(l);
       }
       const uint64_t bal = __ballot(kp);
       if (lane == 0 && base + wave * 64 < len) sh.keepmask[(base >> 6) + wave] = bal;

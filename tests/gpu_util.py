@@ -5,6 +5,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
+import oracle
 import paper_2608_29291_amd as ce
 
 DEV = "cuda"
@@ -105,3 +106,47 @@ def selection_swaps_ok(gpu_kept, ref_l32, ref_sel, flags, offs, eps):
         theta = vals[k - 1] if k > 0 else np.inf
         assert abs(float(ref_l32[i]) - theta) <= 4 * eps * max(1.0, abs(theta)), (i, ref_l32[i], theta)
     return int(diff.size)
+
+
+# ---- the fused block: run on the device, check against the oracle ----
+
+def run_block(wl, inplace=True, want_logits=True):
+    dw = DevWorkload(wl)
+    ws = dw.ws(ce.CE_WS_BLOCK)
+    kept_idx, kept_off = dw.new_idx()
+    logits = torch.empty(max(wl.T, 1), device="cuda")
+    h_in = dw.hidden.clone()
+    h_out = h_in if inplace else torch.full_like(h_in, 3.0)
+    ce.ce_routed_block(dw.batch, h_in, h_out, dw.scorer, dw.ffn, ws,
+                       logits_out=logits if want_logits else None, kept_idx_out=kept_idx,
+                       kept_offsets_out=kept_off)
+    torch.cuda.synchronize()
+    st = ce.ce_workspace_status(ws)
+    return dict(y=host(h_out), logits=host(logits)[:wl.T], kidx=host(kept_idx),
+                koff=host(kept_off), status=st)
+
+
+def check_block(wl, r):
+    assert r["status"] == 0
+    l64, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    eps = logit_err(r["logits"], l64)
+    assert eps <= LOGIT_TOL[wl.dtype]
+    # the GPU's top-k of its own logits is exact
+    sel_g = oracle.select(r["logits"].astype(np.float32), wl.flags, wl.seq_offsets, wl.keep)
+    np.testing.assert_array_equal(r["koff"], sel_g["kept_offsets"])
+    kt = int(r["koff"][-1])
+    kept = r["kidx"][:kt]
+    np.testing.assert_array_equal(kept, sel_g["kept_idx"])
+    # and agrees with the oracle's own selection up to near-threshold swaps
+    sel_r = oracle.select(l32, wl.flags, wl.seq_offsets, wl.keep)
+    scale = max(1.0, float(np.max(np.abs(l64[np.isfinite(l64)]))) if np.isfinite(l64).any() else 1.0)
+    swaps = selection_swaps_ok(kept, l32, sel_r, wl.flags, wl.seq_offsets, eps * scale + 1e-30)
+    # outputs against the oracle block on the GPU's selection
+    ref = oracle.routed_block(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.keep, wl.scorer, wl.ffn,
+                              kept_override=kept)
+    err = rel_err(r["y"][kept], ref["y"][kept])
+    dropped = np.ones(wl.T, bool)
+    dropped[kept] = False
+    np.testing.assert_array_equal(r["y"][dropped], wl.hidden[dropped])
+    assert err <= OUT_TOL[wl.dtype], err
+    return err, swaps

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -312,3 +312,42 @@ def test_attention_validation(kw, ptrs, code):
     at = _attn(**kw)
     assert ce.lib.ce_routed_attention(ctypes.byref(at), p["q"], p["k"], p["v"], p["o"], None) == code
     assert ce.lib.ce_routed_attention(None, FAKE, FAKE, FAKE, FAKE, None) == ce.CE_ERR_INVALID_ARG
+
+
+def tiling(B, T, d, r_c, r_e, dtype=ce.CE_BF16):
+    out = (ctypes.c_int32 * 2)()
+    r = ce.lib.ce_score_tiling(ctypes.byref(_batch(B=B, T=T)), ctypes.byref(_scorer(d=d, r_c=r_c, r_e=r_e,
+                                                                                   dtype=dtype)), out)
+    return r if r < 0 else (r, int(out[0]), int(out[1]))
+
+
+@pytest.mark.parametrize("i,expect", [(1, (0, 32, 0)), (2, (0, 32, 0)), (3, (0, 128, 0)),
+                                      (4, (1, 128, 128)), (5, (1, 128, 128))])
+def test_score_tiling_of_named_workloads(i, expect):
+    """Single-launch scorer with 32-token tiles for the tiny fp32 and the
+    understanding workloads, with 128-token tiles for the generation workload
+    (one round of workgroups instead of three), rank tiles of 128 x 128 for
+    the 7B-width and MoT workloads (where 32-token tiles would each stream up
+    to 2.8 MB of W1)."""
+    from ce_workloads import config_params
+    p = config_params(i)
+    offs, flags = build_layout(config_layout(i))
+    dt = ce.CE_F32 if i == 1 else ce.CE_BF16
+    assert tiling(len(offs) - 1, len(flags), p["d"], p["r_c"], p["r_e"], dt) == expect
+
+
+@pytest.mark.parametrize("T,r_c,r_e,expect", [(1024, 128, 32, (1, 64, 64)), (2176, 384, 96, (1, 64, 128)),
+                                              (4224, 320, 32, (1, 128, 64)), (4224, 384, 96, (1, 128, 128)),
+                                              (8320, 32, 64, (0, 128, 0)), (1024, 32, 32, (0, 32, 0))])
+def test_score_tiling_shapes(T, r_c, r_e, expect):
+    """Batch sizes that pick each scorer variant (the GPU parity tests use them)."""
+    assert tiling(3, T, 192, r_c, r_e) == expect
+    assert tiling(3, T, 192, r_c, r_e, dtype=ce.CE_F32) == (0, 32, 0)  # fp32: 32-token single launch
+
+
+def test_score_tiling_validation():
+    assert ce.lib.ce_score_tiling(None, ctypes.byref(_scorer()), None) == ce.CE_ERR_INVALID_ARG
+    assert ce.lib.ce_score_tiling(ctypes.byref(_batch()), None, None) == ce.CE_ERR_INVALID_ARG
+    assert tiling(0, 100, 256, 64, 32) == ce.CE_ERR_INVALID_ARG
+    assert tiling(2, 100, 100, 64, 32) == ce.CE_ERR_UNSUPPORTED
+    assert tiling(2, 100, 256, 64, 32) == (0, 32, 0)

@@ -1,0 +1,103 @@
+"""The fused block's rank-tiled scorer: tiles of tm tokens x tn ranks write
+per-token partial logits (section 3.2, Eq. 4, split over the ranks) that the
+TopK step assembles in a fixed order. At batch sizes that select each of the
+four tile shapes, against the oracle: logits, TopK exact on the GPU's own
+logits and near-threshold swaps only against the oracle's, block outputs,
+dropped rows bitwise, run-to-run determinism; plus one sequence longer than the
+TopK step's LDS key buffer (the assembled logits go through memory there).
+Sequences hold runs of understanding, generation and always-kept tokens, so
+tiles straddle token kinds, and the expansion ranks (r_e = 32 or 96) fill only
+part of their rank tile. The single-launch scorer's 128-token tiles are checked
+through ce_score and the block at a batch size that selects them."""
+import numpy as np
+import pytest
+
+from ce_workloads import TOK_GEN, TOK_KEEP, make_workload
+
+pytestmark = pytest.mark.gpu
+
+U, G, K = 0, TOK_GEN, TOK_KEEP
+
+
+@pytest.fixture(scope="module")
+def GU():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import gpu_util
+    return gpu_util
+
+
+def mixed_layout(T, n_seq, seed):
+    """n_seq ragged sequences summing to T, each a series of kind runs."""
+    rng = np.random.default_rng([seed, T])
+    cuts = np.sort(rng.choice(np.arange(1, T), size=n_seq - 1, replace=False))
+    lens = np.diff(np.concatenate([[0], cuts, [T]]))
+    kinds = [U, G, K, K | G]
+    seqs = []
+    for L in lens:
+        runs, left = [], int(L)
+        while left > 0:
+            n = int(min(left, rng.integers(1, 300)))
+            runs.append((n, int(rng.choice(kinds, p=[0.35, 0.45, 0.12, 0.08]))))
+            left -= n
+        seqs.append(runs)
+    return seqs
+
+
+CASES = [((64, 64), 1024, 128, 32), ((64, 128), 2176, 384, 96),
+         ((128, 64), 4224, 320, 32), ((128, 128), 4224, 384, 96)]
+
+
+@pytest.mark.parametrize("tile,T,r_c,r_e", CASES)
+def test_tiled_scorer_block(GU, tile, T, r_c, r_e):
+    import paper_2608_29291_amd as ce
+    wl = make_workload(f"tiles-{tile[0]}x{tile[1]}", mixed_layout(T, 3, sum(tile)), d=192, F=128,
+                       r_c=r_c, r_e=r_e, keep=0.45, dtype="bf16", seed=tile[0] + tile[1], biases=True)
+    dw = GU.DevWorkload(wl)
+    assert ce.ce_score_tiling(dw.batch, dw.scorer) == tile
+    print(f"[tiles {tile}] T={T} r_c={r_c} r_e={r_e}", flush=True)
+    r = GU.run_block(wl)
+    err, swaps = GU.check_block(wl, r)
+    r2 = GU.run_block(wl)
+    for k in ("y", "logits", "kidx", "koff"):
+        np.testing.assert_array_equal(r[k], r2[k])
+    print(f"[tiles {tile}] out err {err:.2e} swaps {swaps}", flush=True)
+
+
+def test_tiled_scorer_long_sequence(GU):
+    """One 17000-token sequence: the TopK step assembles the logits into
+    memory and reads them back on every radix pass."""
+    import paper_2608_29291_amd as ce
+    wl = make_workload("tiles-long", [[(9000, G), (300, K), (7700, U)]], d=64, F=64, r_c=384, r_e=96,
+                       keep=0.3, dtype="bf16", seed=5, biases=True)
+    dw = GU.DevWorkload(wl)
+    assert ce.ce_score_tiling(dw.batch, dw.scorer)[1] > 0
+    print(f"[tiles long] T={wl.T} tile={ce.ce_score_tiling(dw.batch, dw.scorer)}", flush=True)
+    r = GU.run_block(wl)
+    err, swaps = GU.check_block(wl, r)
+    print(f"[tiles long] out err {err:.2e} swaps {swaps}", flush=True)
+
+
+def test_single_launch_128_token_tiles(GU):
+    """ce_score and the block with the single-launch scorer's 128-token tiles."""
+    import torch
+    import oracle
+    import paper_2608_29291_amd as ce
+    wl = make_workload("tok128", mixed_layout(8320, 4, 77), d=128, F=64, r_c=32, r_e=64, keep=0.4,
+                       dtype="bf16", seed=77, biases=True)
+    dw = GU.DevWorkload(wl)
+    assert ce.ce_score_tiling(dw.batch, dw.scorer) == (128, 0)
+    logits = torch.empty(wl.T, device="cuda")
+    probs = torch.empty(wl.T, device="cuda")
+    ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits, probs)
+    torch.cuda.synchronize()
+    l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    eps = GU.logit_err(GU.host(logits), l64)
+    assert eps <= GU.LOGIT_TOL["bf16"], eps
+    from oracle.score import sigmoid
+    p64 = sigmoid(l64)
+    assert np.max(np.abs(GU.host(probs) - p64)) <= 1e-4
+    r = GU.run_block(wl)
+    err, swaps = GU.check_block(wl, r)
+    print(f"[tok128] logit err {eps:.2e} out err {err:.2e} swaps {swaps}", flush=True)
+
