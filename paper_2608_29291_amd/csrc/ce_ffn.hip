@@ -347,13 +347,12 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int tt = rem / gsz;
   const int ft = grp * kGroup + (rem - tt * gsz);
 
+  // both sizes loaded back to back (one latency, not two)
+  const bool two_sets = a.n_sets == 2 && a.n0_ptr;
   int kt = *a.kt_ptr;
+  int n0 = *(two_sets ? a.n0_ptr : a.kt_ptr);
   kt = kt < 0 ? 0 : (kt > a.cap ? a.cap : kt);
-  int n0 = kt;
-  if (a.n_sets == 2 && a.n0_ptr) {
-    n0 = *a.n0_ptr;
-    n0 = n0 < 0 ? 0 : (n0 > kt ? kt : n0);
-  }
+  n0 = two_sets ? (n0 < 0 ? 0 : (n0 > kt ? kt : n0)) : kt;
   const int tiles0 = (n0 + kTR - 1) / kTR;
   int set, row_lo, row_hi;
   if (tt < tiles0) {
@@ -382,21 +381,48 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   // Token rows past the tile's last packed row (the final token tile is
   // partial) are fetched from past the resource's end: zeros and no memory
   // traffic. Their MFMAs then multiply zeros, which draws less power than
-  // real data, and the clock is power-bound under MFMA load.
+  // real data.
   const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, (uint32_t)(a.tok_rows * a.tok_ld));
   uint32_t voff[8];
+  if (is_w) {
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int r = 64 * (wave & 3) + 8 * q + r8;
-    const int c = pch ^ ((r >> 1) & 7);
-    if (is_w) {
+    for (int q = 0; q < 8; ++q) {
+      const int r = 64 * (wave & 3) + 8 * q + r8;
+      const int c = pch ^ ((r >> 1) & 7);
       int feat;
       if constexpr (kMode == 0) feat = f0 + 32 * ((r >> 5) >> 1) + (r & 31);
       else feat = f0 + r;
       voff[q] = (uint32_t)((int64_t)feat * a.w_ld + c * 16);
-    } else {
-      const int j = row_lo + r;
-      voff[q] = j < row_hi ? (uint32_t)((int64_t)map_row(j, a.map1, a.map2) * a.tok_ld + c * 16) : 0x80000000u;
+    }
+  } else {
+    // source rows through the index maps: clamped, branch-free loads, so the
+    // eight of a level are in flight together (per-row branches made the
+    // compiler wait after each one)
+    int src[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int j = row_lo + 64 * (wave & 3) + 8 * q + r8;
+      src[q] = j < row_hi ? j : -1;
+    }
+    if (a.map1) {
+      int v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = a.map1[src[q] < 0 ? 0 : src[q]];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) src[q] = src[q] < 0 ? -1 : v[q];
+    }
+    if (a.map2) {
+      int v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = a.map2[src[q] < 0 ? 0 : src[q]];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) src[q] = src[q] < 0 ? -1 : v[q];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int r = 64 * (wave & 3) + 8 * q + r8;
+      const int c = pch ^ ((r >> 1) & 7);
+      voff[q] = src[q] < 0 ? 0x80000000u : (uint32_t)((int64_t)src[q] * a.tok_ld + c * 16);
     }
   }
   // weight row block (64 w + 8 q) / 32 has the parity of q / 4: the gate / up
