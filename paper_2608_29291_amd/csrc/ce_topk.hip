@@ -9,9 +9,12 @@
 // The same sweep assigns packed positions with wavefront ballot / popcount
 // prefix sums, so kept_idx comes out ascending within each sequence.
 //
-// One 1024-thread workgroup per sequence; sequences of up to 16384 tokens keep
-// their keys and KEEP bits in LDS, longer ones re-read logits and flags from
-// global memory on every pass.
+// One 1024-thread workgroup per sequence. Sequences of up to 16384 tokens keep
+// their keys and KEEP bits in LDS: the loads of four 1024-token chunks are in
+// flight together, one wave sums the packed offset meanwhile, each radix pass
+// takes two barriers (alternating histograms) and the sweep ranks all chunks
+// with one scan. Longer sequences re-read logits and flags from global memory
+// on every pass.
 #include "ce_device.hpp"
 #include "ce_launch.hpp"
 
@@ -21,7 +24,7 @@ namespace {
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kLdsKeys = 16384;
+constexpr int kMaxChunks = 16;  // keys held in LDS: up to 16 x 1024 tokens
 
 __global__ __launch_bounds__(256) void seq_info_kernel(const int32_t* __restrict__ offs,
                                                        const uint8_t* __restrict__ flags, int B,
@@ -31,80 +34,348 @@ __global__ __launch_bounds__(256) void seq_info_kernel(const int32_t* __restrict
 }
 
 struct SelShared {
-  uint32_t keys[kLdsKeys];
-  uint64_t keepmask[kLdsKeys / 64];
-  uint32_t hist[256];
+  uint32_t keys[kMaxChunks * kSelThreads];
+  uint64_t keepmask[kMaxChunks * kSelWaves];
+  uint32_t hist[256];         // global-memory path
+  uint32_t hist2[2][256];     // LDS path: one histogram per pass parity
+  uint32_t slot_cnt[kMaxChunks * kSelWaves];  // LDS path sweep: per (chunk, wave) counts
   int32_t wsum_s[kSelWaves];
   int32_t wsum_e[kSelWaves];
   int64_t scratch[kSelWaves];
+  int64_t off_b;
   uint32_t sel_digit;
   int32_t sel_above;
 };
 
-template <bool kLds>
-__device__ void select_body(const SelectArgs& a, SelShared& sh, int lo, int len, int nkeep,
-                            int64_t off_b) {
+// Retained rows of sequence s: its always-kept tokens plus ceil(keep * routable).
+__device__ __forceinline__ int64_t seq_kept(const SelectArgs& a, int len, int w) {
+  const int nk = w & 0x7fffffff;
+  return nk + num_keep_dev(a.keep, len - nk);
+}
+
+// Packed offset of sequence b (sum of K_b' over b' < b) by one wave, given
+// the sizes of sequence `lane` (loaded early by the caller, zero past b).
+__device__ __forceinline__ int64_t seq_offset_wave(const SelectArgs& a, int b, int lane, int len0, int w0) {
+  int64_t part = lane < b ? seq_kept(a, len0, w0) : 0;
+  for (int s = lane + 64; s < b; s += 64) part += seq_kept(a, a.info[3 * s + 1], a.info[3 * s + 2]);
+  for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
+  return part;
+}
+
+// Batch status by one wave: bit 0 = offsets out of order or not covering
+// [0, T), bit 1 = more retained rows than the capacity. len0 / w0: the sizes
+// of sequence `lane` (loaded early by the caller when lane < B).
+__device__ __forceinline__ void batch_status_wave(const SelectArgs& a, int lane, int len0, int w0) {
+  int64_t tot = 0;
+  int bad = 0;
+  for (int s = lane; s < a.B; s += 64) {
+    const int l2 = s == lane ? len0 : a.info[3 * s + 1];
+    const int w = s == lane ? w0 : a.info[3 * s + 2];
+    bad |= (w < 0) ? 1 : 0;
+    tot += seq_kept(a, l2, w);
+  }
+  for (int off = 32; off > 0; off >>= 1) tot += __shfl_xor(tot, off);
+  const bool any_bad = __ballot(bad != 0) != 0ull;
+  if (lane == 0) {
+    uint32_t st = 0;
+    if (any_bad) st |= 1u;
+    if (tot > a.cap) st |= 2u;
+    *a.status = st;
+  }
+}
+
+// Wave 0: the digit of the krem-th largest key in histogram h (lane l owns
+// digits 4l .. 4l+3) and the number of keys with a larger digit.
+__device__ __forceinline__ void find_digit(const uint32_t* h, int krem, int lane, SelShared& sh) {
+  const uint32_t h0 = h[4 * lane + 0], h1 = h[4 * lane + 1];
+  const uint32_t h2 = h[4 * lane + 2], h3 = h[4 * lane + 3];
+  const int s = (int)(h0 + h1 + h2 + h3);
+  int incl = s;  // inclusive suffix sum over lanes >= lane
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_down(incl, o);
+    if (lane + o < 64) incl += y;
+  }
+  int cum = incl - s;  // keys with a larger digit (higher lanes)
+  const uint32_t hh[4] = {h0, h1, h2, h3};
+#pragma unroll
+  for (int dd = 3; dd >= 0; --dd) {
+    const int hv = (int)hh[dd];
+    if (cum < krem && cum + hv >= krem) {
+      sh.sel_digit = (uint32_t)(4 * lane + dd);
+      sh.sel_above = cum;
+    }
+    cum += hv;
+  }
+}
+
+// Sequences of at most kMaxChunks * kSelThreads tokens: keys and KEEP bits
+// in LDS. The loops stay loops: each workgroup runs this code once on a cold
+// instruction cache, and fully unrolled versions spent more time fetching
+// instructions than they saved.
+__device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& sh, int b, int lo, int len,
+                                                int nkeep) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int nc = (len + kSelThreads - 1) / kSelThreads;  // chunks of 1024 tokens (wave-uniform)
+
+  // wave 15 sums the packed offset of this sequence and wave 14 (sequence 0)
+  // the batch status; the sizes of sequence `lane` are loaded now, so that
+  // their latency overlaps the key loads below
+  const bool off_wave = wave == kSelWaves - 1, st_wave = wave == kSelWaves - 2 && b == 0;
+  int len0 = 0, w0 = 0;
+  if ((off_wave && lane < b) || (st_wave && lane < a.B)) {
+    len0 = a.info[3 * lane + 1];
+    w0 = a.info[3 * lane + 2];
+  }
+
+  // ---- keys: token c * 1024 + tid of chunk c; four chunks per round with
+  //      their loads in flight together (clamped into the sequence) ----
+  if (!a.part) {
+#pragma unroll 1
+    for (int c0 = 0; c0 < nc; c0 += 4) {
+      uint32_t f4[4];
+      float l4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = min((c0 + j) * kSelThreads + tid, len - 1);
+        f4[j] = a.flags[lo + i];
+        l4[j] = a.logits[lo + i];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = (c0 + j) * kSelThreads + tid;
+        const bool kp = (f4[j] & 2u) != 0 && i < len;
+        if (i < len) sh.keys[i] = logit_key(kp ? __builtin_inff() : l4[j]);
+        const uint64_t bal = __ballot(kp);
+        if (lane == 0 && c0 + j < nc) sh.keepmask[(c0 + j) * kSelWaves + wave] = bal;
+      }
+    }
+  } else {
+    // logits from the rank-tiled scorer's partial sums, tile by tile so that
+    // a tile's loads for the round's chunks are in flight together; fixed
+    // order: core tiles, b2c, then (generation tokens) the expansion tiles and
+    // b2e[m]
+    float b2e_m = 0.0f;
+    if (a.r_exp > 0 && a.b2e) {
+      const double mf = floor((double)a.n_seg * (double)a.t[b]);
+      const int m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
+      b2e_m = a.b2e[m];
+    }
+    const int64_t T = a.T;
+    const float* pp = a.part + lo;
+    const bool has_exp = a.r_exp > 0 && a.n_rt > a.n_ct;
+#pragma unroll 1
+    for (int c0 = 0; c0 < nc; c0 += 4) {
+      int i4[4];
+      uint32_t f4[4];
+      float l4[4], v4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        i4[j] = min((c0 + j) * kSelThreads + tid, len - 1);
+        f4[j] = a.flags[lo + i4[j]];
+        l4[j] = pp[i4[j]];
+      }
+#pragma unroll 1
+      for (int q = 1; q < a.n_ct; ++q) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v4[j] = pp[q * T + i4[j]];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) l4[j] += v4[j];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) l4[j] += a.b2c;
+      if (has_exp) {
+        float e4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) e4[j] = pp[a.n_ct * T + i4[j]];
+#pragma unroll 1
+        for (int q = a.n_ct + 1; q < a.n_rt; ++q) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v4[j] = pp[q * T + i4[j]];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) e4[j] += v4[j];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (f4[j] & 1u) l4[j] += e4[j] + b2e_m;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = (c0 + j) * kSelThreads + tid;
+        const bool kp = (f4[j] & 2u) != 0 && i < len;
+        const float l = kp ? __builtin_inff() : l4[j];
+        if (i < len) {
+          sh.keys[i] = logit_key(l);
+          a.logits_w[lo + i] = l;
+        }
+        const uint64_t bal = __ballot(kp);
+        if (lane == 0 && c0 + j < nc) sh.keepmask[(c0 + j) * kSelWaves + wave] = bal;
+      }
+    }
+  }
+
+  if (off_wave) {
+    const int64_t off = seq_offset_wave(a, b, lane, len0, w0);
+    if (lane == 0) sh.off_b = off;
+  } else if (st_wave) {
+    batch_status_wave(a, lane, len0, w0);
+  }
+  if (tid < 512) (&sh.hist2[0][0])[tid] = 0u;
+  __syncthreads();
+
+  auto keep_of = [&](int i) -> bool { return (sh.keepmask[i >> 6] >> (i & 63)) & 1ull; };
+  const int n_r = len - nkeep;
+  const int k = num_keep_dev(a.keep, n_r);
+  // mode: 0 = none of the routable tokens, 1 = all of them, 2 = threshold
+  const int mode = (k <= 0) ? 0 : (k >= n_r ? 1 : 2);
+
+  uint32_t theta = 0;
+  int krem = k;
+  if (mode == 2) {
+    uint32_t prefix = 0, pmask = 0;
+    // two histograms alternate: wave 1 clears the next pass's while wave 0
+    // scans this one, so a pass takes two barriers
+#pragma unroll 1
+    for (int p = 0; p < 4; ++p) {
+      const int shift = 24 - 8 * p;
+      uint32_t* h = sh.hist2[p & 1];
+#pragma unroll 1
+      for (int i = tid; i < len; i += kSelThreads) {
+        const uint32_t key = sh.keys[i];
+        if (!keep_of(i) && (key & pmask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
+      }
+      lds_barrier();
+      if (wave == 0) {
+        find_digit(h, krem, lane, sh);
+      } else if (wave == 1 && p < 3) {
+        uint32_t* hn = sh.hist2[(p + 1) & 1];  // scanned in the previous pass
+#pragma unroll
+        for (int j = 0; j < 4; ++j) hn[4 * lane + j] = 0u;
+      }
+      lds_barrier();
+      prefix |= sh.sel_digit << shift;
+      pmask |= 255u << shift;
+      krem -= sh.sel_above;
+    }
+    theta = prefix;
+  }
+  // krem = number of theta-equal routable tokens to retain (lowest indices first)
+
+  // ---- sweep: strong (always kept) and tie tokens counted per (chunk, wave)
+  //      in token order, one scan over those counts, then packed positions ----
+  auto classify = [&](int i, bool& st, bool& eq) {
+    st = false;
+    eq = false;
+    if (i < len) {
+      if (keep_of(i) || mode == 1) {
+        st = true;
+      } else if (mode == 2) {
+        const uint32_t key = sh.keys[i];
+        st = key > theta;
+        eq = key == theta;
+      }
+    }
+  };
+#pragma unroll 1
+  for (int c = 0; c < nc; ++c) {
+    bool st, eq;
+    classify(c * kSelThreads + tid, st, eq);
+    const uint64_t bs = __ballot(st), be = __ballot(eq);
+    // strong count in the low 16 bits, ties in the high 16 (each at most 16384)
+    if (lane == 0) sh.slot_cnt[c * kSelWaves + wave] = (uint32_t)__popcll(bs) | ((uint32_t)__popcll(be) << 16);
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // exclusive prefix over the (chunk, wave) entries in token order; lane l
+    // owns entries 4l .. 4l+3
+    const int n_ent = nc * kSelWaves;
+    uint32_t v4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v4[j] = (4 * lane + j < n_ent) ? sh.slot_cnt[4 * lane + j] : 0u;
+    const uint32_t tot = v4[0] + v4[1] + v4[2] + v4[3];
+    uint32_t incl = tot;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    uint32_t run = incl - tot;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (4 * lane + j < n_ent) sh.slot_cnt[4 * lane + j] = run;
+      run += v4[j];
+    }
+  }
+  __syncthreads();
+  const int64_t off_b = sh.off_b;
+#pragma unroll 1
+  for (int c = 0; c < nc; ++c) {
+    const int i = c * kSelThreads + tid;
+    bool st, eq;
+    classify(i, st, eq);
+    const uint64_t bs = __ballot(st), be = __ballot(eq);
+    const uint32_t pre = sh.slot_cnt[c * kSelWaves + wave];
+    const int s_before = (int)(pre & 0xffffu) + __popcll(bs & lt_mask);
+    const int e_before = (int)(pre >> 16) + __popcll(be & lt_mask);
+    const bool kept = st || (eq && e_before < krem);
+    const int64_t pos = off_b + s_before + (e_before < krem ? e_before : krem);
+    if (i < len) {
+      if (kept && pos < a.cap) a.kept_idx[pos] = lo + i;
+      if (a.token_pos) a.token_pos[lo + i] = kept ? (int32_t)(pos < 0x7fffffff ? pos : 0x7fffffff) : -1;
+    }
+  }
+  if (tid == 0) {
+    const int64_t k_b = nkeep + k;
+    a.kept_offsets[b] = (int32_t)(off_b < 0x7fffffff ? off_b : 0x7fffffff);
+    if (b == a.B - 1) {
+      const int64_t tot = off_b + k_b;
+      a.kept_offsets[a.B] = (int32_t)(tot < 0x7fffffff ? tot : 0x7fffffff);
+    }
+  }
+}
+
+// Sequences longer than the LDS key buffer holds: keys and KEEP bits are
+// re-read from global memory on every pass.
+__device__ __forceinline__ void select_body_global(const SelectArgs& a, SelShared& sh, int lo, int len, int nkeep,
+                                   int64_t off_b) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
   // ---- logits from the rank-tiled scorer's partial sums (fixed order) ----
-  float b2e_m = 0.0f;
-  if (a.part && a.r_exp > 0 && a.b2e) {
-    const double mf = floor((double)a.n_seg * (double)a.t[blockIdx.x]);
-    const int m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
-    b2e_m = a.b2e[m];
-  }
-  auto assemble = [&](int i) -> float {
-    const uint8_t f = a.flags[lo + i];
-    if (f & 2) return __builtin_inff();
-    const float* pp = a.part + lo + i;
-    float l = pp[0];
-    for (int qq = 1; qq < a.n_ct; ++qq) l += pp[(int64_t)qq * a.T];
-    l += a.b2c;
-    if ((f & 1) && a.r_exp > 0) {
-      float e = pp[(int64_t)a.n_ct * a.T];
-      for (int qq = a.n_ct + 1; qq < a.n_rt; ++qq) e += pp[(int64_t)qq * a.T];
-      l += e + b2e_m;
+  if (a.part) {
+    float b2e_m = 0.0f;
+    if (a.r_exp > 0 && a.b2e) {
+      const double mf = floor((double)a.n_seg * (double)a.t[blockIdx.x]);
+      const int m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
+      b2e_m = a.b2e[m];
     }
-    return l;
-  };
-  if (!kLds && a.part) {
-    for (int i = tid; i < len; i += kSelThreads) a.logits_w[lo + i] = assemble(i);
+    for (int i = tid; i < len; i += kSelThreads) {
+      const uint8_t f = a.flags[lo + i];
+      float l;
+      if (f & 2) {
+        l = __builtin_inff();
+      } else {
+        const float* pp = a.part + lo + i;
+        l = pp[0];
+        for (int qq = 1; qq < a.n_ct; ++qq) l += pp[(int64_t)qq * a.T];
+        l += a.b2c;
+        if ((f & 1) && a.r_exp > 0 && a.n_rt > a.n_ct) {
+          float e = pp[(int64_t)a.n_ct * a.T];
+          for (int qq = a.n_ct + 1; qq < a.n_rt; ++qq) e += pp[(int64_t)qq * a.T];
+          l += e + b2e_m;
+        }
+      }
+      a.logits_w[lo + i] = l;
+    }
     __threadfence_block();
     __syncthreads();
   }
-
-  // ---- keys ----
-  if constexpr (kLds) {
-    for (int base = 0; base < len; base += kSelThreads) {
-      const int i = base + tid;
-      bool kp = false;
-      if (i < len) {
-        kp = (a.flags[lo + i] & 2) != 0;
-        float l;
-        if (a.part) {
-          l = assemble(i);
-          a.logits_w[lo + i] = l;
-        } else {
-          l = a.logits[lo + i];
-        }
-        sh.keys[i] = logit_key(l);
-      }
-      const uint64_t bal = __ballot(kp);
-      if (lane == 0 && base + wave * 64 < len) sh.keepmask[(base >> 6) + wave] = bal;
-    }
-    __syncthreads();
-  }
-  auto key_of = [&](int i) -> uint32_t {
-    if constexpr (kLds) return sh.keys[i];
-    else return logit_key(a.logits[lo + i]);
-  };
-  auto keep_of = [&](int i) -> bool {
-    if constexpr (kLds) return (sh.keepmask[i >> 6] >> (i & 63)) & 1ull;
-    else return (a.flags[lo + i] & 2) != 0;
-  };
+  const float* logits = a.part ? a.logits_w : a.logits;
+  auto key_of = [&](int i) -> uint32_t { return logit_key(logits[lo + i]); };
+  auto keep_of = [&](int i) -> bool { return (a.flags[lo + i] & 2) != 0; };
 
   const int n_r = len - nkeep;
   const int k = num_keep_dev(a.keep, n_r);
@@ -124,28 +395,7 @@ __device__ void select_body(const SelectArgs& a, SelShared& sh, int lo, int len,
         if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
       }
       __syncthreads();
-      if (wave == 0) {
-        // lane l owns digits 4l .. 4l+3; find the digit holding the krem-th largest
-        const uint32_t h0 = sh.hist[4 * lane + 0], h1 = sh.hist[4 * lane + 1];
-        const uint32_t h2 = sh.hist[4 * lane + 2], h3 = sh.hist[4 * lane + 3];
-        const int s = (int)(h0 + h1 + h2 + h3);
-        int incl = s;  // inclusive suffix sum over lanes >= lane
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_down(incl, o);
-          if (lane + o < 64) incl += y;
-        }
-        int cum = incl - s;  // keys with a larger digit (higher lanes)
-        const uint32_t hh[4] = {h0, h1, h2, h3};
-#pragma unroll
-        for (int dd = 3; dd >= 0; --dd) {
-          const int h = (int)hh[dd];
-          if (cum < krem && cum + h >= krem) {
-            sh.sel_digit = (uint32_t)(4 * lane + dd);
-            sh.sel_above = cum;
-          }
-          cum += h;
-        }
-      }
+      if (wave == 0) find_digit(sh.hist, krem, lane, sh);
       __syncthreads();
       prefix |= sh.sel_digit << shift;
       pmask |= 255u << shift;
@@ -214,19 +464,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   __shared__ SelShared sh;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
-
-  // ---- packed offset of this sequence: sum of K_b' over b' < b ----
-  int64_t part = 0;
-  for (int s = tid; s < b; s += kSelThreads) {
-    const int len = a.info[3 * s + 1];
-    const int nk = a.info[3 * s + 2] & 0x7fffffff;
-    part += nk + num_keep_dev(a.keep, len - nk);
-  }
-  const int64_t off_b = block_sum_i64(part, sh.scratch);
-
   const int lo = a.info[3 * b + 0];
   const int len = a.info[3 * b + 1];
   const int nkeep = a.info[3 * b + 2] & 0x7fffffff;
+  if (len <= kMaxChunks * kSelThreads) {
+    select_body_lds(a, sh, b, lo, len, nkeep);
+    return;
+  }
+
+  // ---- long sequence: packed offset of this sequence first ----
+  int64_t part = 0;
+  for (int s = tid; s < b; s += kSelThreads) part += seq_kept(a, a.info[3 * s + 1], a.info[3 * s + 2]);
+  const int64_t off_b = block_sum_i64(part, sh.scratch);
   const int64_t k_b = nkeep + num_keep_dev(a.keep, len - nkeep);
   if (tid == 0) {
     a.kept_offsets[b] = (int32_t)(off_b < 0x7fffffff ? off_b : 0x7fffffff);
@@ -235,29 +484,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
       a.kept_offsets[a.B] = (int32_t)(tot < 0x7fffffff ? tot : 0x7fffffff);
     }
   }
-  if (b == 0) {
-    // status: one writer, no atomics; covers every sequence
-    int64_t tot = 0;
-    int bad = 0;
-    for (int s = tid; s < a.B; s += kSelThreads) {
-      const int l2 = a.info[3 * s + 1];
-      const int w = a.info[3 * s + 2];
-      const int nk = w & 0x7fffffff;
-      bad |= (w < 0) ? 1 : 0;
-      tot += nk + num_keep_dev(a.keep, l2 - nk);
-    }
-    const int any_bad = __syncthreads_or(bad);
-    tot = block_sum_i64(tot, sh.scratch);
-    if (tid == 0) {
-      uint32_t st = 0;
-      if (any_bad) st |= 1u;
-      if (tot > a.cap) st |= 2u;
-      *a.status = st;
-    }
+  if (b == 0 && (tid >> 6) == 0) {
+    const int l0 = (tid < a.B) ? a.info[3 * tid + 1] : 0, w0 = (tid < a.B) ? a.info[3 * tid + 2] : 0;
+    batch_status_wave(a, tid & 63, l0, w0);
   }
-
-  if (len <= kLdsKeys) select_body<true>(a, sh, lo, len, nkeep, off_b);
-  else select_body<false>(a, sh, lo, len, nkeep, off_b);
+  select_body_global(a, sh, lo, len, nkeep, off_b);
 }
 
 // Stable partition of packed rows by FFN set: grp_rows lists set-0 rows first

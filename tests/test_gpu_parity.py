@@ -156,6 +156,26 @@ def test_topk_long_sequence_global_path(G):
     check_topk_exact(G, wl, l32)
 
 
+@pytest.mark.parametrize("lens", [(1023, 1024, 1025), (4097, 3), (16384,), (16385, 1)])
+@pytest.mark.parametrize("mode", ["normal", "ints"])
+def test_topk_register_slots(G, lens, mode):
+    """Sequences over several 1024-token register slots, up to the 16384-token
+    limit of the register path and one token past it (global-memory path);
+    always-kept tokens sit inside the sequences, across slot boundaries."""
+    seqs = []
+    for n in lens:
+        h = n // 2
+        seqs.append([(h - 20, 0), (41, TOK_KEEP), (n - h - 21, 0)] if n > 64 else [(n, 0)])
+    wl = make_workload("slots", seqs, d=64, F=64, r_c=32, r_e=32, keep=0.41, dtype="bf16", seed=9)
+    rng = np.random.default_rng(sum(lens))
+    if mode == "ints":
+        l32 = rng.integers(-20, 20, size=wl.T).astype(np.float32)  # many ties across slots
+    else:
+        l32 = rng.standard_normal(wl.T).astype(np.float32)
+    print(f"[topk slots] lens={lens} mode={mode}", flush=True)
+    check_topk_exact(G, wl, l32)
+
+
 def test_topk_empty_and_all_kept(G):
     wl = make_workload("empty", [[(0, 0)], [(10, TOK_KEEP)], [(0, 0)], [(5, 0), (3, TOK_KEEP)], [(1, 0)]],
                        d=64, F=64, r_c=32, r_e=32, keep=0.5, dtype="bf16", seed=7)

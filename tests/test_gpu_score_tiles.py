@@ -3,8 +3,9 @@ per-token partial logits (section 3.2, Eq. 4, split over the ranks) that the
 TopK step assembles in a fixed order. At batch sizes that select each of the
 four tile shapes, against the oracle: logits, TopK exact on the GPU's own
 logits and near-threshold swaps only against the oracle's, block outputs,
-dropped rows bitwise, run-to-run determinism; plus one sequence longer than the
-TopK step's LDS key buffer (the assembled logits go through memory there).
+dropped rows bitwise, run-to-run determinism; plus one sequence at the TopK
+step's 16384-token register limit and one longer (the assembled logits go
+through memory there).
 Sequences hold runs of understanding, generation and always-kept tokens, so
 tiles straddle token kinds, and the expansion ranks (r_e = 32 or 96) fill only
 part of their rank tile. The single-launch scorer's 128-token tiles are checked
@@ -101,3 +102,20 @@ def test_single_launch_128_token_tiles(GU):
     err, swaps = GU.check_block(wl, r)
     print(f"[tok128] logit err {eps:.2e} out err {err:.2e} swaps {swaps}", flush=True)
 
+
+
+def test_tiled_scorer_register_limit(GU):
+    """One 16384-token sequence (all 16 register slots of the TopK step, the
+    partial sums assembled tile by tile) and a short one."""
+    import paper_2608_29291_amd as ce
+    wl = make_workload("tiles-16k", [[(7000, G), (300, K), (6000, U), (3084, G)], [(700, U), (60, K)]],
+                       d=64, F=64, r_c=384, r_e=96, keep=0.35, dtype="bf16", seed=12, biases=True)
+    dw = GU.DevWorkload(wl)
+    assert ce.ce_score_tiling(dw.batch, dw.scorer)[1] > 0
+    print(f"[tiles 16k] T={wl.T} tile={ce.ce_score_tiling(dw.batch, dw.scorer)}", flush=True)
+    r = GU.run_block(wl)
+    err, swaps = GU.check_block(wl, r)
+    r2 = GU.run_block(wl)
+    for k in ("y", "logits", "kidx", "koff"):
+        np.testing.assert_array_equal(r[k], r2[k])
+    print(f"[tiles 16k] out err {err:.2e} swaps {swaps}", flush=True)
