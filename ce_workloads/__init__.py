@@ -306,11 +306,18 @@ def make_config(i: int, seed=None, step: Optional[int] = None) -> Workload:
         t_values = [config3_t(s)] * B
     w = make_workload(CONFIG_NAMES[i], layout, seed=seed, t_values=t_values, **p)
     if i == 3 and step is not None and step > 0:
-        xi = np.random.default_rng([2, int(step)]).standard_normal(
-            size=w.hidden.shape, dtype=np.float32)
-        w.hidden = bf16_round(w.hidden + np.float32(0.25) * xi)
+        w.hidden = config3_step_hidden(w.hidden, int(step))
         w.meta["step"] = int(step)
     return w
+
+
+def config3_step_hidden(hidden0: np.ndarray, step: int) -> np.ndarray:
+    """Hidden states of config 3's denoising step s from those of step 0:
+    bf16(h_0 + 0.25 * xi_s), xi_s standard normal from seed (2, s)."""
+    if step == 0:
+        return hidden0
+    xi = np.random.default_rng([2, int(step)]).standard_normal(size=hidden0.shape, dtype=np.float32)
+    return bf16_round(hidden0 + np.float32(0.25) * xi)
 
 
 def small_workload(kind: str, seed: int = 0, dtype: str = "bf16", **kw) -> Workload:
