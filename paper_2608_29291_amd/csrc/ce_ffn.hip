@@ -778,9 +778,11 @@ hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
 // Kernel and tile choice, from timing every variant on the five named workloads:
 //   gate/up: the full-line ping-pong kernel (128 output features x 256 tokens,
 //            groups of 8 feature tiles); fallback 8-wave 256 x 256 register-staged;
-//   down:    the full-line ping-pong kernel when its 256 x 256 tiles number
-//            >= 200 (enough to fill the chip; groups of 8 feature tiles), else
-//            the same kernel over two K halves (groups of 6), else 256 x 128 (4 x 2 waves)
+//   down:    the full-line ping-pong kernel over two K halves (groups of 6)
+//            when the cost model of down_split_tiles prefers it (uneven
+//            rounds: 108 tiles at the understanding workload, 294 at the 7B
+//            width), else the same kernel over whole tiles when they number
+//            >= 200 (groups of 8 feature tiles), else 256 x 128 (4 x 2 waves)
 //            for d < 3072 and 128 x 128 (2 x 2 waves) for the 7B width,
 //            token-tile-major order (every weight tile of a token tile stays in
 //            one XCD's L2).
@@ -803,18 +805,17 @@ hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream
 int ffn_down_split_tiles(const FfnGemmArgs& a, bool bf16) {
   if (!bf16 || !a.part || !a.tile_cnt || !pp2_ok(a)) return 0;
   const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
-  if (big_tiles >= 200) return 0;
   const int t = down_split_tiles(a.cap, a.n_feat, a.k_bytes / 2, a.n_sets, 2);
   return t == big_tiles ? t : 0;
 }
 
 hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear) {
   if (bf16) {
+    // tiles that fill the chip's rounds unevenly: two K halves per tile, when
+    // the workspace holds their partial sums
+    if (ffn_down_split_tiles(a, bf16) > 0) return launch_pp2<1, 6, true, 2>(a, stream, counters_clear);
     const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
     if (big_tiles >= 200 && pp2_ok(a)) return launch_pp2<1, 8, true>(a, stream);
-    // too few tiles to fill the chip: two K halves per tile, when the
-    // workspace holds their partial sums
-    if (ffn_down_split_tiles(a, bf16) > 0) return launch_pp2<1, 6, true, 2>(a, stream, counters_clear);
     if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2, 1, 64>(a, stream);
     return launch_cfg<true, 1, 128, 128, 2, 2, 2, 1, 64>(a, stream);
   }

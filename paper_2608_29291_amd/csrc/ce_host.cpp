@@ -24,7 +24,16 @@ int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem) {
   if (k_bytes % 128 != 0 || k_bytes < 6 * 128) return 0;
   if ((int64_t)cap * k_bytes >= lim || (int64_t)d * k_bytes >= lim) return 0;
   const int64_t tiles = (int64_t)((cap + 255) / 256 + n_sets - 1) * ((d + 255) / 256);
-  return tiles <= kSplitMaxTiles ? (int)tiles : 0;
+  if (tiles > kSplitMaxTiles) return 0;
+  // Launch cost in units of the K-loop time of one 128-byte superslab (one
+  // workgroup per CU, rounds of 256), from measured per-workgroup timelines:
+  // a whole tile adds its prologue and residual epilogue (~5.6 superslabs), a
+  // half adds the partial sums written and read back besides (~14.1).
+  const int64_t ns = k_bytes / 128;
+  auto rounds = [](int64_t n) { return (n + 255) / 256; };
+  const double whole = (double)rounds(tiles) * ((double)ns + 5.6);
+  const double halves = (double)rounds(2 * tiles) * ((double)ns / 2.0 + 14.1);
+  return halves < whole ? (int)tiles : 0;
 }
 
 int score_token_tile(int B, int T, int d, int r_core, int r_exp, int elem) {

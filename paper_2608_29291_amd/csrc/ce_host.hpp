@@ -36,10 +36,12 @@ struct WsLayout {
 WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem);
 
 // The down GEMM (d outputs, contraction d_ff) runs as two K halves when its
-// 256 x 256 tiles are too few to fill the chip; returns that tile count, or 0
-// when the down GEMM is not split. Shared by the launcher and the workspace
-// layout so both agree.
-constexpr int kSplitMaxTiles = 128;
+// 256 x 256 tiles fill the chip's rounds of 256 workgroups so unevenly that
+// twice the workgroups, each with half of K plus the partial-sum exchange,
+// finish sooner (a cost model); returns that tile count, or 0 when the down
+// GEMM is not split. Shared by the launcher and the workspace layout so both
+// agree. At most kSplitMaxTiles tiles (512 MB of partial sums).
+constexpr int kSplitMaxTiles = 1024;
 // The FFN-saliency reduction splits each sequence's rows over at most this
 // many workgroups (partial sums in the workspace, summed in a fixed order).
 constexpr int kSalSplits = 16;

@@ -351,3 +351,25 @@ def test_score_tiling_validation():
     assert tiling(0, 100, 256, 64, 32) == ce.CE_ERR_INVALID_ARG
     assert tiling(2, 100, 100, 64, 32) == ce.CE_ERR_UNSUPPORTED
     assert tiling(2, 100, 256, 64, 32) == (0, 32, 0)
+
+
+@pytest.mark.parametrize("i,split", [(1, False), (2, True), (3, False), (4, True), (5, True)])
+def test_down_split_policy_of_named_workloads(i, split):
+    """The down GEMM runs as two K halves where its 256 x 256 tiles fill the
+    rounds of 256 workgroups unevenly: 108 tiles (understanding) and 294 (7B
+    width, MoT); whole tiles for 204 (generation: one round) and for the tiny
+    fp32 workload. The split shows in the FFN workspace as the partial-sum
+    region, two fp32 256 x 256 tiles per output tile."""
+    from ce_workloads import config_params
+    p = config_params(i)
+    offs, flags = build_layout(config_layout(i))
+    keep = {1: 0.5, 2: 0.35, 3: 0.5, 4: 0.4, 5: 0.3}[i]
+    cap = ce.ce_kept_count_host(offs, flags, keep)
+    n_sets = 2 if i == 5 else 1
+    dt = ce.CE_F32 if i == 1 else ce.CE_BF16
+    elem = 4 if i == 1 else 2
+    b = _batch(B=len(offs) - 1, T=len(flags), keep=keep, cap=cap)
+    need = ce.lib.ce_workspace_size(ce.CE_WS_FFN, ctypes.byref(b), p["d"], p["F"], dt)
+    tiles = ((cap + 255) // 256 + n_sets - 1) * ((p["d"] + 255) // 256)
+    act = cap * p["F"] * elem
+    assert (need >= act + tiles * 2 * 256 * 256 * 4) == split

@@ -317,6 +317,22 @@ def test_block(G, kind, dtype, inplace):
     print(f"[block {kind} {dtype} inplace={inplace}] rel err {err:.3e} swaps {swaps}")
 
 
+@pytest.mark.parametrize("kind", ["und", "mot", "interleaved"])
+def test_block_ping_pong_split_down(G, kind):
+    """Shapes on the ping-pong GEMMs (d and d_ff multiples of 256, 32
+    superslabs of K): gate/up with the SwiGLU epilogue, and the down GEMM in
+    two K halves that meet through the workspace (the cost model splits at
+    this K), ragged last token tile, MoT groups; run twice, bitwise equal (two
+    addends: the sum does not depend on which half arrives last)."""
+    wl = small_workload(kind, seed=21, dtype="bf16", d=512, F=2048)
+    print(f"[block ping-pong {kind}] T={wl.T}", flush=True)
+    r = run_block(G, wl)
+    err, swaps = check_block(G, wl, r)
+    r2 = run_block(G, wl)
+    np.testing.assert_array_equal(r["y"], r2["y"])
+    print(f"[block ping-pong {kind}] rel err {err:.3e} swaps {swaps}", flush=True)
+
+
 def test_block_keep_one_is_dense(G):
     wl = small_workload("mot", seed=10, dtype="bf16", keep=1.0)
     wl.flags = (wl.flags & ~np.uint8(TOK_KEEP)).astype(np.uint8)
