@@ -463,6 +463,10 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     return v;
   };
   const uint32_t rkey = (uint32_t)((lrow >> 1) & 7);  // fragment rows start at multiples of 32
+  // A wave whose 64 token rows all lie past the tile's last packed row (the
+  // final token tile is partial) reads no fragments and issues no MFMAs: its
+  // accumulators stay zero, and the epilogue stores none of its rows.
+  const bool mfma_on = __builtin_amdgcn_readfirstlane((int)(row_lo + wt * 64 < row_hi)) != 0;
   const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kRow);
   const uint32_t rowb = (uint32_t)((wt * 64 + lrow) * kRow);
   u32x4_t fa[2][kMW], fb[2][kMT];
@@ -489,18 +493,21 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   if (late) lds_barrier();
   int wb = 0, tb = 0;  // ring slots of superslab s
   // one memory phase and one compute phase over K half H of superslab s
-  auto half = [&](int s, auto hc) __attribute__((always_inline)) {
+  auto half = [&](int s, auto hc, auto on) __attribute__((always_inline)) {
     constexpr int H = decltype(hc)::value;
+    constexpr bool kOn = decltype(on)::value;
     // ---- memory phase: fragments of K half H of superslab s ----
     const char* sa = wsm + wb * kSlab;
     const char* sb = tsm + tb * kSlab;
+    if constexpr (kOn) {
 #pragma unroll
-    for (int step = 0; step < 2; ++step) {
-      const uint32_t off = (((uint32_t)(4 * H + 2 * step + lhalf)) ^ opaque(rkey)) << 4;
+      for (int step = 0; step < 2; ++step) {
+        const uint32_t off = (((uint32_t)(4 * H + 2 * step + lhalf)) ^ opaque(rkey)) << 4;
 #pragma unroll
-      for (int i = 0; i < kMW; ++i) fa[step][i] = *reinterpret_cast<const u32x4_t*>(sa + rowa + off + 32 * i * kRow);
+        for (int i = 0; i < kMW; ++i) fa[step][i] = *reinterpret_cast<const u32x4_t*>(sa + rowa + off + 32 * i * kRow);
 #pragma unroll
-      for (int j = 0; j < kMT; ++j) fb[step][j] = *reinterpret_cast<const u32x4_t*>(sb + rowb + off + 32 * j * kRow);
+        for (int j = 0; j < kMT; ++j) fb[step][j] = *reinterpret_cast<const u32x4_t*>(sb + rowb + off + 32 * j * kRow);
+      }
     }
     // superslab s - 1 is consumed by both groups: its slot receives superslab
     // s + kBufs - 1, either half of this wave's rows in each phase (spread) or
@@ -531,12 +538,14 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     __builtin_amdgcn_sched_barrier(0);
     // ---- compute phase ----
     if constexpr (kPrio) __builtin_amdgcn_s_setprio(1);
+    if constexpr (kOn) {
 #pragma unroll
-    for (int step = 0; step < 2; ++step)
+      for (int step = 0; step < 2; ++step)
 #pragma unroll
-      for (int i = 0; i < kMW; ++i)
+        for (int i = 0; i < kMW; ++i)
 #pragma unroll
-        for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[step][i], fb[step][j]);
+          for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[step][i], fb[step][j]);
+    }
     if constexpr (kPrio) __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_sched_barrier(0);
     if (H == 1 && !late && s + 1 < ns) {
@@ -546,12 +555,19 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  for (int s = s0; s < ns; ++s) {
-    half(s, I0{});
-    half(s, I1{});
-    wb = wb + 1 == kBufs0 ? 0 : wb + 1;
-    tb = tb + 1 == kBufs1 ? 0 : tb + 1;
-  }
+  // two instances of the K loop, picked once per tile: with MFMAs, and
+  // without them for a wave whose rows are all past the tile's end (same DMA
+  // and barriers); a branch inside the loop cost 1-1.5% on full tiles
+  auto kloop = [&](auto on) __attribute__((always_inline)) {
+    for (int s = s0; s < ns; ++s) {
+      half(s, I0{}, on);
+      half(s, I1{}, on);
+      wb = wb + 1 == kBufs0 ? 0 : wb + 1;
+      tb = tb + 1 == kBufs1 ? 0 : tb + 1;
+    }
+  };
+  if (mfma_on) kloop(std::true_type{});
+  else kloop(std::false_type{});
 
   if constexpr (kSplit == 2) {
     if (!late) lds_barrier();  // both groups in step from here on
