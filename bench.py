@@ -385,18 +385,38 @@ def main():
         return float(np.mean([a.elapsed_time(b) for a, b in evs])) * 1e3  # us
 
     reps = max(args.steps, 10)
-    gemm_warm = 20  # untimed GEMM calls after the delay, before the timed ones
-    stages = {
-        "score": timed(lambda i: ce.ce_score(batch, h0, wsets[i % n_sets][0], logits,
-                                             stream=stream), reps),
-        "topk_compact": timed(lambda i: ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk,
-                                                           stream=stream), reps),
-        "ffn_gateup": timed(lambda i: ce.ce_ffn_gateup(batch, compact, kept_idx, kept_off,
-                                                       wsets[i % n_sets][1], act, ws_ffn, stream=stream),
-                            reps, gemm_warm),
-        "ffn_down": timed(lambda i: ce.ce_ffn_down(batch, act, kept_idx, kept_off, wsets[i % n_sets][1],
-                                                   ffn_out, ws_ffn, stream=stream), reps, gemm_warm),
-    }
+    gemm_warm = 20  # untimed rounds after the delay, before the timed ones
+
+    def timed_pipeline(fns, reps, warm):
+        """Mean GPU time per call of each of `fns`, called in turn (the staged
+        entry points in the order ce_routed_block runs them), one event pair
+        around every call: each kernel runs under the same mix of load as in
+        the fused block (a GEMM timed back to back against itself draws more
+        power and gets a lower clock). Same device-side delay first as timed()."""
+        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in fns] for _ in range(reps)]
+        torch.cuda._sleep(20_000_000)
+        for i in range(warm):
+            for fn in fns:
+                fn(i)
+        for i in range(reps):
+            for f, fn in enumerate(fns):
+                evs[i][f][0].record(stream)
+                fn(i)
+                evs[i][f][1].record(stream)
+        torch.cuda.synchronize()
+        return [float(np.mean([evs[i][f][0].elapsed_time(evs[i][f][1]) for i in range(reps)])) * 1e3
+                for f in range(len(fns))]
+
+    stage_names = ("score", "topk_compact", "ffn_gateup", "ffn_down")
+    stage_fns = (
+        lambda i: ce.ce_score(batch, h0, wsets[i % n_sets][0], logits, stream=stream),
+        lambda i: ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk, stream=stream),
+        lambda i: ce.ce_ffn_gateup(batch, compact, kept_idx, kept_off, wsets[i % n_sets][1], act, ws_ffn,
+                                   stream=stream),
+        lambda i: ce.ce_ffn_down(batch, act, kept_idx, kept_off, wsets[i % n_sets][1], ffn_out, ws_ffn,
+                                 stream=stream))
+    stages = dict(zip(stage_names, timed_pipeline(stage_fns, reps, gemm_warm)))
     log("stages (us): " + ", ".join(f"{k}={v:.1f}" for k, v in stages.items()))
 
     # FFN-pruning signal (section 3.4, Eq. 8-9) on this step's activations: one
