@@ -339,8 +339,12 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int per = (total + kXcds - 1) / kXcds;
   const int wk = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
   if (wk >= total) return;
-  const int w = wk / kSplit;   // tile; both K halves of a tile are adjacent in the XCD order
-  const int kz = wk - w * kSplit;
+  // K half kz of tile w: the first halves of all tiles, then the second
+  // halves, so each XCD streams one half of K of its tiles (a third fewer
+  // distinct operand bytes through its L2 than both halves of half as many
+  // tiles); the two halves meet through device-coherent memory wherever they run
+  const int kz = kSplit == 1 ? 0 : wk / (total / kSplit);
+  const int w = wk - kz * (total / kSplit);
   const int grp = w / (kGroup * n_tt);
   const int rem = w - grp * (kGroup * n_tt);
   const int gsz = min(kGroup, n_ft - grp * kGroup);
