@@ -233,7 +233,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the routed block shards by sequence with no exchange; see the design notes)",
+              "(the routed block shards by sequence with no exchange between GPUs)",
               file=sys.stderr)
         sys.exit(2)
 
