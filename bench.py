@@ -35,7 +35,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0
 MALL_BYTES = 256 << 20
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_gateup_showo2_understanding_traffic.txt")
+# HBM traffic of the gate/up GEMM per workload, from rocprofv3 counter runs
+TRAFFIC_FILES = {2: "ffn_gateup_showo2_understanding_traffic.txt", 4: "ffn_gateup_7b_mixed_varlen_traffic.txt"}
 KERNEL_SOURCES = ["paper_2608_29291_amd/csrc/ce_ffn.hip", "paper_2608_29291_amd/csrc/ce_device.hpp"]
 
 
@@ -51,11 +52,13 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic():
-    """HBM bytes per gate/up launch from the committed counter summary, if it
-    was taken on the current kernel source (else None)."""
+def load_traffic(wid: int):
+    """HBM bytes per gate/up launch from the committed counter summary of this
+    workload, if it was taken on the current kernel source (else None)."""
+    if wid not in TRAFFIC_FILES:
+        return None
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(ROOT, "profiles", TRAFFIC_FILES[wid])) as f:
             kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith(" "))
     except OSError:
         return None
@@ -212,11 +215,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", type=int, default=2, help="named workload 1..5 (default 2)")
+    ap.add_argument("--workload", type=int, default=4,
+                    help="named workload 1..5 (default 4, the largest: 7B width, mixed varlen batch)")
     ap.add_argument("--step3", type=int, default=-1,
                     help="workload 3: one denoising step s (0..49), or -1 (default) for all 50 in turn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seqs", type=int, default=0, help="sequences in the oracle sample (0 = auto)")
+    ap.add_argument("--cpu-seqs", type=int, default=0,
+                    help="sequences in the oracle sample (0 = every sequence of the batch)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (reference kernel of "
                          "known traffic for the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -459,7 +464,7 @@ def main():
     peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
     achieved = gateup_flops / (stages["ffn_gateup"] * 1e-6) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": load_traffic(),
+                "frac": round(achieved / peak, 4), "traffic": load_traffic(wid),
                 "kernel": "ffn_gemm_pp2_kernel gate/up + SwiGLU (ce_ffn_gateup)",
                 "flops_per_launch": gateup_flops, "timed_launches": reps, "warm_launches": gemm_warm}
 
@@ -498,7 +503,7 @@ def main():
     result["routed_attention"] = time_attention(ce, stream, max(args.steps, 10))
     result["achievable_peaks"] = (achievable_peaks(cap, d, F) if bf16 else None)
     if not args.no_cpu_baseline:
-        n_seq = args.cpu_seqs or {1: 1, 2: 8, 3: 1, 4: 1, 5: 1}[wid]
+        n_seq = args.cpu_seqs or wl.B
         log(f"oracle CPU baseline on {n_seq} sequence(s)...")
         result["cpu_baseline"] = cpu_baseline(wl, n_seq)
     print(json.dumps(result), flush=True)

@@ -39,17 +39,18 @@ N_SEGMENTS = 4  # M, number of generation expansion scorers
 def bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 -> bf16 bit patterns (uint16), round to nearest, ties to even.
 
-    NaN inputs map to a quiet NaN pattern. Used to store drawn inputs.
+    NaN inputs map to a quiet NaN pattern. Used to store drawn inputs. The
+    rounding add stays in uint32: it can carry past 2^32 only for NaN bit
+    patterns, which are replaced afterwards.
     """
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
-    r = r.astype(np.uint32) & np.uint32(0xFFFF)
+    u = x.view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
     nan = np.isnan(x)
     if nan.any():
-        r = np.where(nan, (x.view(np.uint32) >> np.uint32(16)) | np.uint32(0x40), r)
-    return r.astype(np.uint16)
+        r = np.where(nan, ((u >> np.uint32(16)) | np.uint32(0x40)).astype(np.uint16), r)
+    return r
 
 
 def bf16_to_f32(bits: np.ndarray) -> np.ndarray:

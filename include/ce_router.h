@@ -8,7 +8,9 @@
  *   1. score     core + expansion routing logits per token       (section 3.2, Eq. 4)
  *   2. topk      per-sequence TopK of the logits -> retained set  (section 3.4, Eq. 6)
  *   3. compact   retained tokens packed into a shorter sequence   (section 3.4, after Eq. 6)
- *   4. ffn       SwiGLU FFN on the packed rows only
+ *   4. ffn       SwiGLU FFN on the packed rows only              (section 3.4, after Eq. 6:
+ *                the retained tokens form a shorter sequence for the layer's
+ *                attention and FFN)
  *   5. scatter   residual merge; dropped tokens take the bypass   (section 3.4, after Eq. 6)
  *
  * Conventions shared by every entry point
@@ -20,8 +22,11 @@
  *   returns. All work is enqueued on `stream` (a hipStream_t; NULL = the
  *   default stream); calls return without waiting for it. There are no
  *   device-to-host copies and no synchronisation on the hot path.
- * - Arguments are validated on the host before anything is launched; a
- *   negative status means nothing was enqueued.
+ * - Arguments are validated on the host before anything is launched: a
+ *   validation error (CE_ERR_INVALID_ARG, CE_ERR_UNSUPPORTED,
+ *   CE_ERR_WORKSPACE) means nothing was enqueued. CE_ERR_HIP reports a failed
+ *   launch; entry points with several launches may already have enqueued the
+ *   earlier ones, so after CE_ERR_HIP the outputs and workspace are undefined.
  * - Values known only on the device (how many tokens each sequence keeps,
  *   the packed row count Kt, MoT group sizes) never leave the device. Grids
  *   are sized from host-known upper bounds (kept_capacity); surplus tiles
@@ -214,7 +219,10 @@ int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidd
                     void* stream);
 
 /*
- * Step 4 -- SwiGLU FFN on the packed rows.
+ * Step 4 -- SwiGLU FFN on the packed rows (section 3.4, after Eq. 6: the
+ * retained tokens are packed into a shorter sequence and only that sequence
+ * runs through the layer's FFN; in a mixture-of-transformers backbone, section
+ * 4.1, each retained token uses the FFN weight set of its task).
  *   compact      device dtype [kept_capacity x d]: packed rows (row j is token kept_idx[j])
  *   kept_idx     device int32 [kept_capacity] (needed for the MoT set choice)
  *   kept_offsets device int32 [B+1]: Kt = kept_offsets[B] rows are processed
@@ -227,7 +235,8 @@ int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kep
                   void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Step 4 in two launches (same result as ce_routed_ffn):
+ * Step 4 in two launches (same result as ce_routed_ffn; section 3.4, FFN over
+ * the packed retained rows):
  *   ce_ffn_gateup  act[j] = SiLU(W_gate x_j) * (W_up x_j), x_j = compact[j]; act is the
  *                  intermediate activation z of the FFN (section 3.4, Eq. 8 scores FFN
  *                  channels from it). act: device dtype [kept_capacity x d_ff], packed order.
@@ -254,8 +263,11 @@ int ce_scatter_residual(const ce_batch* batch, const void* ffn_out, const int32_
                         const void* hidden_in, void* hidden_out, void* stream);
 
 /*
- * Steps 1-5 fused: score -> TopK -> SwiGLU FFN over the retained rows
- * (gathered directly from hidden_in) -> residual scatter into hidden_out.
+ * Steps 1-5 fused (section 3.2 Eq. 4, section 3.4 Eq. 6 and the packing /
+ * bypass rule after it): score -> TopK -> SwiGLU FFN over the retained rows
+ * (gathered directly from hidden_in) -> residual scatter into hidden_out;
+ * dropped tokens take the bypass path (their rows are never written in place,
+ * copied unchanged out of place).
  *   hidden_in / hidden_out  device dtype [T x d] (may alias: in place)
  *   logits_out       device float32 [T] or NULL
  *   kept_idx_out     device int32 [kept_capacity] or NULL

@@ -126,6 +126,12 @@ _sig("ce_layer_gap", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_in
 # ----------------------------------------------------------------------------
 # marshalling helpers
 # ----------------------------------------------------------------------------
+#
+# The library sees only pointers, so the binding checks what a pointer cannot
+# carry before every call: dtype, shape or element count, contiguity, 16-byte
+# alignment and the device. A wrong size or a sliced, misaligned tensor would
+# otherwise become an out-of-bounds or misaligned access on the GPU. These are
+# argument checks only; the routed block's arithmetic all runs in the library.
 
 def _ptr(t) -> Optional[int]:
     if t is None:
@@ -150,6 +156,50 @@ def _dtype_code(t) -> int:
     if t.dtype == torch.float32:
         return CE_F32
     raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _torch_dtype(code: int):
+    import torch
+    return {CE_BF16: torch.bfloat16, CE_F32: torch.float32}[code]
+
+
+def _chk(t, name: str, dtype=None, numel: Optional[int] = None, shape=None, rows_min: Optional[int] = None,
+         optional: bool = False):
+    """Validate one device tensor argument; returns its pointer (None for an
+    absent optional argument).
+
+    dtype     required torch dtype
+    numel     minimum element count
+    shape     exact shape (a tuple; None entries match any size)
+    rows_min  for matrices given by `shape` with a None row count: at least
+              this many rows
+    """
+    import torch
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name}: required tensor is missing")
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: tensor must live in GPU memory")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name}: tensor is on {t.device}, the current device is "
+                         f"cuda:{torch.cuda.current_device()}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: tensor must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if t.numel() > 0 and t.data_ptr() % 16 != 0:
+        raise ValueError(f"{name}: data pointer is not 16-byte aligned")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, need at least {numel}")
+    if shape is not None:
+        if t.dim() != len(shape) or any(s is not None and int(d) != int(s) for d, s in zip(t.shape, shape)):
+            raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+        if rows_min is not None and t.shape[0] < rows_min:
+            raise ValueError(f"{name}: {t.shape[0]} rows, need at least {rows_min}")
+    return t.data_ptr()
 
 
 def _stream(stream) -> Optional[int]:
@@ -182,8 +232,17 @@ class Batch:
         return int(self.flags.numel())
 
     def c(self) -> CEBatch:
-        return CEBatch(self.B, self.T, _dev_ptr(self.seq_offsets), _dev_ptr(self.flags),
-                       _dev_ptr(self.t), float(self.keep), int(self.kept_capacity))
+        import torch
+        so = _chk(self.seq_offsets, "seq_offsets", torch.int32, numel=2)
+        if self.seq_offsets.dim() != 1:
+            raise ValueError("seq_offsets must be 1-D [B+1]")
+        if self.flags is None or self.flags.dim() != 1:
+            raise ValueError("flags must be a 1-D uint8 tensor [T]")
+        fl = _chk(self.flags, "flags", torch.uint8)
+        tp = _chk(self.t, "t", torch.float32, numel=self.B, optional=True)
+        if int(self.kept_capacity) < 0:
+            raise ValueError("kept_capacity must be >= 0")
+        return CEBatch(self.B, self.T, so, fl, tp, float(self.keep), int(self.kept_capacity))
 
 
 @dataclass
@@ -198,13 +257,37 @@ class Scorer:
     b1_exp: "object" = None
     b2_exp: "object" = None
 
+    @property
+    def d(self) -> int:
+        return int(self.w1_core.shape[1])
+
+    @property
+    def dtype(self) -> int:
+        return _dtype_code(self.w1_core)
+
     def c(self) -> CEScorerW:
-        r_c, d = self.w1_core.shape
-        n_seg, r_e = (self.w1_exp.shape[0], self.w1_exp.shape[1]) if self.w1_exp is not None else (1, 0)
-        return CEScorerW(int(d), int(r_c), int(r_e), int(n_seg), _dtype_code(self.w1_core),
-                         _dev_ptr(self.w1_core), _dev_ptr(self.b1_core), _dev_ptr(self.w2_core),
-                         float(self.b2_core), _dev_ptr(self.w1_exp), _dev_ptr(self.b1_exp),
-                         _dev_ptr(self.w2_exp), _dev_ptr(self.b2_exp))
+        import torch
+        if self.w1_core is None or self.w1_core.dim() != 2:
+            raise ValueError("w1_core must be a matrix [r_core, d]")
+        r_c, d = (int(x) for x in self.w1_core.shape)
+        tdt = self.w1_core.dtype
+        _dtype_code(self.w1_core)
+        if self.w1_exp is not None:
+            if self.w1_exp.dim() != 3:
+                raise ValueError("w1_exp must be [n_seg, r_exp, d]")
+            n_seg, r_e = int(self.w1_exp.shape[0]), int(self.w1_exp.shape[1])
+        else:
+            n_seg, r_e = 1, 0
+        f32 = torch.float32
+        ptrs = (_chk(self.w1_core, "w1_core", tdt, shape=(r_c, d)),
+                _chk(self.b1_core, "b1_core", f32, shape=(r_c,), optional=True),
+                _chk(self.w2_core, "w2_core", f32, shape=(r_c,)),
+                _chk(self.w1_exp, "w1_exp", tdt, shape=(n_seg, r_e, d), optional=r_e == 0),
+                _chk(self.b1_exp, "b1_exp", f32, shape=(n_seg, r_e), optional=True),
+                _chk(self.w2_exp, "w2_exp", f32, shape=(n_seg, r_e), optional=r_e == 0),
+                _chk(self.b2_exp, "b2_exp", f32, shape=(n_seg,), optional=True))
+        return CEScorerW(d, r_c, r_e, n_seg, _dtype_code(self.w1_core), ptrs[0], ptrs[1], ptrs[2],
+                         float(self.b2_core), ptrs[3], ptrs[4], ptrs[5], ptrs[6])
 
 
 @dataclass
@@ -214,15 +297,41 @@ class FFN:
     w_up: Sequence
     w_down: Sequence
 
+    @property
+    def d(self) -> int:
+        return int(self.w_gate[0].shape[1])
+
+    @property
+    def d_ff(self) -> int:
+        return int(self.w_gate[0].shape[0])
+
     def c(self) -> CEFFNW:
         n = len(self.w_gate)
-        F, d = self.w_gate[0].shape
-        s = CEFFNW(int(d), int(F), int(n), _dtype_code(self.w_gate[0]))
+        if n not in (1, 2) or len(self.w_up) != n or len(self.w_down) != n:
+            raise ValueError("an FFN has 1 or 2 weight sets, each with gate, up and down")
+        if self.w_gate[0] is None or self.w_gate[0].dim() != 2:
+            raise ValueError("w_gate must be a matrix [d_ff, d]")
+        F, d = (int(x) for x in self.w_gate[0].shape)
+        tdt = self.w_gate[0].dtype
+        s = CEFFNW(d, F, n, _dtype_code(self.w_gate[0]))
         for i in range(n):
-            s.w_gate[i] = _dev_ptr(self.w_gate[i])
-            s.w_up[i] = _dev_ptr(self.w_up[i])
-            s.w_down[i] = _dev_ptr(self.w_down[i])
+            s.w_gate[i] = _chk(self.w_gate[i], f"w_gate[{i}]", tdt, shape=(F, d))
+            s.w_up[i] = _chk(self.w_up[i], f"w_up[{i}]", tdt, shape=(F, d))
+            s.w_down[i] = _chk(self.w_down[i], f"w_down[{i}]", tdt, shape=(d, F))
         return s
+
+
+def _ws_ptr(ws, need: int):
+    """Workspace pointer and size in bytes (any dtype; the library checks the size)."""
+    p = _chk(ws, "ws")
+    nbytes = ws.numel() * ws.element_size()
+    if nbytes < need:
+        raise ValueError(f"ws: {nbytes} bytes, need {need}")
+    return p, nbytes
+
+
+def _hidden(h, name, T, d, tdt):
+    return _chk(h, name, tdt, shape=(T, d))
 
 
 # ----------------------------------------------------------------------------
@@ -260,65 +369,117 @@ def alloc_workspace(which: int, batch: Batch, d: int, d_ff: int, dtype: int, dev
 
 def ce_workspace_status(ws, stream=None) -> int:
     out = ctypes.c_uint32(0)
-    _check(lib.ce_workspace_status(_dev_ptr(ws), ctypes.byref(out), _stream(stream)),
+    _check(lib.ce_workspace_status(_chk(ws, "ws", numel=4), ctypes.byref(out), _stream(stream)),
            "ce_workspace_status")
     return int(out.value)
 
 
 def ce_score(batch: Batch, hidden, scorer: Scorer, logits, probs=None, stream=None):
+    import torch
     cb, sw = batch.c(), scorer.c()
-    _check(lib.ce_score(ctypes.byref(cb), _dev_ptr(hidden), ctypes.byref(sw), _dev_ptr(logits),
-                        _dev_ptr(probs), _stream(stream)), "ce_score")
+    T = batch.T
+    h = _hidden(hidden, "hidden", T, sw.d, _torch_dtype(sw.dtype) if sw.dtype in (0, 1) else None)
+    _check(lib.ce_score(ctypes.byref(cb), h, ctypes.byref(sw),
+                        _chk(logits, "logits", torch.float32, numel=T),
+                        _chk(probs, "probs", torch.float32, numel=T, optional=True), _stream(stream)),
+           "ce_score")
 
 
 def ce_topk_compact(batch: Batch, logits, kept_idx, kept_offsets, ws, token_pos=None,
                     hidden=None, compact=None, stream=None):
+    import torch
     cb = batch.c()
+    T, B, cap = batch.T, batch.B, int(batch.kept_capacity)
     dtype = _dtype_code(hidden) if hidden is not None else CE_F32
-    d = int(hidden.shape[1]) if hidden is not None else 0
-    _check(lib.ce_topk_compact(ctypes.byref(cb), _dev_ptr(logits), _dev_ptr(hidden), dtype, d,
-                               _dev_ptr(kept_idx), _dev_ptr(kept_offsets), _dev_ptr(token_pos),
-                               _dev_ptr(compact), _dev_ptr(ws), ws.numel(), _stream(stream)),
+    d = int(hidden.shape[1]) if hidden is not None and hidden.dim() == 2 else 0
+    hp = cp = None
+    if compact is not None:
+        if hidden is None:
+            raise ValueError("compact needs hidden")
+        hp = _hidden(hidden, "hidden", T, d, hidden.dtype)
+        cp = _chk(compact, "compact", hidden.dtype, shape=(None, d), rows_min=cap)
+    i32 = torch.int32
+    wp, wn = _ws_ptr(ws, ce_workspace_size(CE_WS_TOPK, batch, d if compact is not None else 0, 0,
+                                           dtype if compact is not None else CE_F32))
+    _check(lib.ce_topk_compact(ctypes.byref(cb), _chk(logits, "logits", torch.float32, numel=T), hp, dtype, d,
+                               _chk(kept_idx, "kept_idx", i32, numel=cap),
+                               _chk(kept_offsets, "kept_offsets", i32, numel=B + 1),
+                               _chk(token_pos, "token_pos", i32, numel=T, optional=True), cp,
+                               wp, wn, _stream(stream)),
            "ce_topk_compact")
 
 
-def ce_routed_ffn(batch: Batch, compact, kept_idx, kept_offsets, ffn: FFN, ffn_out, ws, stream=None):
+def _ffn_common(batch: Batch, ffn: FFN, kept_idx, kept_offsets):
+    import torch
     cb, fw = batch.c(), ffn.c()
-    _check(lib.ce_routed_ffn(ctypes.byref(cb), _dev_ptr(compact), _dev_ptr(kept_idx),
-                             _dev_ptr(kept_offsets), ctypes.byref(fw), _dev_ptr(ffn_out),
-                             _dev_ptr(ws), ws.numel(), _stream(stream)), "ce_routed_ffn")
+    cap = int(batch.kept_capacity)
+    ki = _chk(kept_idx, "kept_idx", torch.int32, numel=cap)
+    ko = _chk(kept_offsets, "kept_offsets", torch.int32, numel=batch.B + 1)
+    tdt = ffn.w_gate[0].dtype
+    need = ce_workspace_size(CE_WS_FFN, batch, fw.d, fw.d_ff, fw.dtype)
+    return cb, fw, cap, ki, ko, tdt, need
+
+
+def ce_routed_ffn(batch: Batch, compact, kept_idx, kept_offsets, ffn: FFN, ffn_out, ws, stream=None):
+    cb, fw, cap, ki, ko, tdt, need = _ffn_common(batch, ffn, kept_idx, kept_offsets)
+    wp, wn = _ws_ptr(ws, need)
+    _check(lib.ce_routed_ffn(ctypes.byref(cb), _chk(compact, "compact", tdt, shape=(None, fw.d), rows_min=cap),
+                             ki, ko, ctypes.byref(fw),
+                             _chk(ffn_out, "ffn_out", tdt, shape=(None, fw.d), rows_min=cap),
+                             wp, wn, _stream(stream)), "ce_routed_ffn")
 
 
 def ce_ffn_gateup(batch: Batch, compact, kept_idx, kept_offsets, ffn: FFN, act, ws, stream=None):
-    cb, fw = batch.c(), ffn.c()
-    _check(lib.ce_ffn_gateup(ctypes.byref(cb), _dev_ptr(compact), _dev_ptr(kept_idx),
-                             _dev_ptr(kept_offsets), ctypes.byref(fw), _dev_ptr(act),
-                             _dev_ptr(ws), ws.numel(), _stream(stream)), "ce_ffn_gateup")
+    cb, fw, cap, ki, ko, tdt, need = _ffn_common(batch, ffn, kept_idx, kept_offsets)
+    wp, wn = _ws_ptr(ws, need)
+    _check(lib.ce_ffn_gateup(ctypes.byref(cb), _chk(compact, "compact", tdt, shape=(None, fw.d), rows_min=cap),
+                             ki, ko, ctypes.byref(fw),
+                             _chk(act, "act", tdt, shape=(None, fw.d_ff), rows_min=cap),
+                             wp, wn, _stream(stream)), "ce_ffn_gateup")
 
 
 def ce_ffn_down(batch: Batch, act, kept_idx, kept_offsets, ffn: FFN, ffn_out, ws, stream=None):
-    cb, fw = batch.c(), ffn.c()
-    _check(lib.ce_ffn_down(ctypes.byref(cb), _dev_ptr(act), _dev_ptr(kept_idx),
-                           _dev_ptr(kept_offsets), ctypes.byref(fw), _dev_ptr(ffn_out),
-                           _dev_ptr(ws), ws.numel(), _stream(stream)), "ce_ffn_down")
+    cb, fw, cap, ki, ko, tdt, need = _ffn_common(batch, ffn, kept_idx, kept_offsets)
+    wp, wn = _ws_ptr(ws, need)
+    _check(lib.ce_ffn_down(ctypes.byref(cb), _chk(act, "act", tdt, shape=(None, fw.d_ff), rows_min=cap),
+                           ki, ko, ctypes.byref(fw),
+                           _chk(ffn_out, "ffn_out", tdt, shape=(None, fw.d), rows_min=cap),
+                           wp, wn, _stream(stream)), "ce_ffn_down")
 
 
 def ce_scatter_residual(batch: Batch, ffn_out, kept_idx, kept_offsets, hidden_in, hidden_out,
                         stream=None):
+    import torch
     cb = batch.c()
-    _check(lib.ce_scatter_residual(ctypes.byref(cb), _dev_ptr(ffn_out), _dev_ptr(kept_idx),
-                                   _dev_ptr(kept_offsets), _dtype_code(hidden_in),
-                                   int(hidden_in.shape[1]), _dev_ptr(hidden_in),
-                                   _dev_ptr(hidden_out), _stream(stream)), "ce_scatter_residual")
+    cap, T = int(batch.kept_capacity), batch.T
+    if hidden_in is None or hidden_in.dim() != 2:
+        raise ValueError("hidden_in must be a matrix [T, d]")
+    d, tdt = int(hidden_in.shape[1]), hidden_in.dtype
+    _check(lib.ce_scatter_residual(ctypes.byref(cb), _chk(ffn_out, "ffn_out", tdt, shape=(None, d), rows_min=cap),
+                                   _chk(kept_idx, "kept_idx", torch.int32, numel=cap),
+                                   _chk(kept_offsets, "kept_offsets", torch.int32, numel=batch.B + 1),
+                                   _dtype_code(hidden_in), d, _hidden(hidden_in, "hidden_in", T, d, tdt),
+                                   _hidden(hidden_out, "hidden_out", T, d, tdt), _stream(stream)),
+           "ce_scatter_residual")
 
 
 def ce_routed_block(batch: Batch, hidden_in, hidden_out, scorer: Scorer, ffn: FFN, ws,
                     logits_out=None, kept_idx_out=None, kept_offsets_out=None, stream=None):
+    import torch
     cb, sw, fw = batch.c(), scorer.c(), ffn.c()
-    _check(lib.ce_routed_block(ctypes.byref(cb), _dev_ptr(hidden_in), _dev_ptr(hidden_out),
-                               ctypes.byref(sw), ctypes.byref(fw), _dev_ptr(logits_out),
-                               _dev_ptr(kept_idx_out), _dev_ptr(kept_offsets_out), _dev_ptr(ws),
-                               ws.numel(), _stream(stream)), "ce_routed_block")
+    T, cap = batch.T, int(batch.kept_capacity)
+    if sw.d != fw.d or sw.dtype != fw.dtype:
+        raise ValueError("scorer and FFN must agree on d and dtype")
+    tdt = ffn.w_gate[0].dtype
+    wp, wn = _ws_ptr(ws, ce_workspace_size(CE_WS_BLOCK, batch, fw.d, fw.d_ff, fw.dtype))
+    _check(lib.ce_routed_block(ctypes.byref(cb), _hidden(hidden_in, "hidden_in", T, fw.d, tdt),
+                               _hidden(hidden_out, "hidden_out", T, fw.d, tdt),
+                               ctypes.byref(sw), ctypes.byref(fw),
+                               _chk(logits_out, "logits_out", torch.float32, numel=T, optional=True),
+                               _chk(kept_idx_out, "kept_idx_out", torch.int32, numel=cap, optional=True),
+                               _chk(kept_offsets_out, "kept_offsets_out", torch.int32, numel=batch.B + 1,
+                                    optional=True),
+                               wp, wn, _stream(stream)), "ce_routed_block")
 
 
 def ce_score_tiling(batch: Batch, scorer: Scorer):
@@ -334,52 +495,91 @@ def ce_score_tiling(batch: Batch, scorer: Scorer):
 
 def ce_drop_stability(batch: Batch, token_pos_t, token_pos_ref, jaccard, j_rand=None, rda=None,
                       stream=None):
+    import torch
     cb = batch.c()
-    _check(lib.ce_drop_stability(ctypes.byref(cb), _dev_ptr(token_pos_t), _dev_ptr(token_pos_ref),
-                                 _dev_ptr(jaccard), _dev_ptr(j_rand), _dev_ptr(rda), _stream(stream)),
+    T, B = batch.T, batch.B
+    i32, f32 = torch.int32, torch.float32
+    _check(lib.ce_drop_stability(ctypes.byref(cb), _chk(token_pos_t, "token_pos_t", i32, numel=T),
+                                 _chk(token_pos_ref, "token_pos_ref", i32, numel=T),
+                                 _chk(jaccard, "jaccard", f32, numel=B),
+                                 _chk(j_rand, "j_rand", f32, numel=B, optional=True),
+                                 _chk(rda, "rda", f32, numel=B, optional=True), _stream(stream)),
            "ce_drop_stability")
 
 
 def ce_ffn_down_colnorms(ffn: FFN, norms, stream=None):
+    import torch
     fw = ffn.c()
-    _check(lib.ce_ffn_down_colnorms(ctypes.byref(fw), _dev_ptr(norms), _stream(stream)), "ce_ffn_down_colnorms")
+    _check(lib.ce_ffn_down_colnorms(ctypes.byref(fw),
+                                    _chk(norms, "norms", torch.float32, numel=fw.n_sets * fw.d_ff),
+                                    _stream(stream)), "ce_ffn_down_colnorms")
 
 
 def ce_ffn_saliency(batch: Batch, act, kept_idx, kept_offsets, ffn: FFN, norms, prune_mask, delta,
                     saliency, leakage, ws, use_pruned=None, stream=None):
-    cb, fw = batch.c(), ffn.c()
-    _check(lib.ce_ffn_saliency(ctypes.byref(cb), _dev_ptr(act), _dev_ptr(kept_idx), _dev_ptr(kept_offsets),
-                               ctypes.byref(fw), _dev_ptr(norms), _dev_ptr(prune_mask), float(delta),
-                               _dev_ptr(saliency), _dev_ptr(leakage), _dev_ptr(use_pruned), _dev_ptr(ws),
-                               ws.numel(), _stream(stream)), "ce_ffn_saliency")
+    import torch
+    cb, fw, cap, ki, ko, tdt, need = _ffn_common(batch, ffn, kept_idx, kept_offsets)
+    B, F = batch.B, fw.d_ff
+    f32, u8 = torch.float32, torch.uint8
+    wp, wn = _ws_ptr(ws, need)
+    _check(lib.ce_ffn_saliency(ctypes.byref(cb), _chk(act, "act", tdt, shape=(None, F), rows_min=cap), ki, ko,
+                               ctypes.byref(fw), _chk(norms, "norms", f32, numel=fw.n_sets * F),
+                               _chk(prune_mask, "prune_mask", u8, numel=F), float(delta),
+                               _chk(saliency, "saliency", f32, numel=B * F), _chk(leakage, "leakage", f32, numel=B),
+                               _chk(use_pruned, "use_pruned", u8, numel=B, optional=True), wp, wn,
+                               _stream(stream)), "ce_ffn_saliency")
 
 
 def ce_ffn_mask_channels(batch: Batch, act, kept_offsets, prune_mask, use_pruned, stream=None):
+    import torch
     cb = batch.c()
-    _check(lib.ce_ffn_mask_channels(ctypes.byref(cb), _dev_ptr(act), _dev_ptr(kept_offsets), _dtype_code(act),
-                                    int(act.shape[1]), _dev_ptr(prune_mask), _dev_ptr(use_pruned),
-                                    _stream(stream)), "ce_ffn_mask_channels")
-
+    cap, B = int(batch.kept_capacity), batch.B
+    if act is None or act.dim() != 2:
+        raise ValueError("act must be a matrix [kept_capacity, d_ff]")
+    F = int(act.shape[1])
+    _check(lib.ce_ffn_mask_channels(ctypes.byref(cb), _chk(act, "act", act.dtype, shape=(None, F), rows_min=cap),
+                                    _chk(kept_offsets, "kept_offsets", torch.int32, numel=B + 1), _dtype_code(act),
+                                    F, _chk(prune_mask, "prune_mask", torch.uint8, numel=F),
+                                    _chk(use_pruned, "use_pruned", torch.uint8, numel=B), _stream(stream)),
+           "ce_ffn_mask_channels")
 
 
 def ce_layer_gap(batch: Batch, x_in, x_out, token_pos, delta, cos, rho_all, rho_ret, gap, skip=None,
                  stream=None):
+    import torch
     cb = batch.c()
-    _check(lib.ce_layer_gap(ctypes.byref(cb), _dev_ptr(x_in), _dev_ptr(x_out), _dtype_code(x_in),
-                            int(x_in.shape[1]), _dev_ptr(token_pos), float(delta), _dev_ptr(cos),
-                            _dev_ptr(rho_all), _dev_ptr(rho_ret), _dev_ptr(gap), _dev_ptr(skip),
-                            _stream(stream)), "ce_layer_gap")
-
+    T, B = batch.T, batch.B
+    if x_in is None or x_in.dim() != 2:
+        raise ValueError("x_in must be a matrix [T, d]")
+    d, tdt = int(x_in.shape[1]), x_in.dtype
+    f32 = torch.float32
+    _check(lib.ce_layer_gap(ctypes.byref(cb), _hidden(x_in, "x_in", T, d, tdt), _hidden(x_out, "x_out", T, d, tdt),
+                            _dtype_code(x_in), d, _chk(token_pos, "token_pos", torch.int32, numel=T), float(delta),
+                            _chk(cos, "cos", f32, numel=T), _chk(rho_all, "rho_all", f32, numel=B),
+                            _chk(rho_ret, "rho_ret", f32, numel=B), _chk(gap, "gap", f32, numel=B),
+                            _chk(skip, "skip", torch.uint8, numel=B, optional=True), _stream(stream)),
+           "ce_layer_gap")
 
 
 def ce_routed_attention(q, k, v, o, q_offsets, kv_offsets, causal, scale, stream=None):
     """q, o [rows, H, head_dim], k, v [rows, H_kv, head_dim] bf16 device tensors;
     q_offsets / kv_offsets int32 device tensors [B+1]."""
-    at = CEAttn(int(q_offsets.numel() - 1), int(q.shape[1]), int(k.shape[1]), int(q.shape[2]),
-                _dev_ptr(q_offsets), _dev_ptr(kv_offsets), int(q.shape[0]), int(k.shape[0]),
-                int(bool(causal)), float(scale), _dtype_code(q))
-    _check(lib.ce_routed_attention(ctypes.byref(at), _dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o),
-                                   _stream(stream)), "ce_routed_attention")
+    import torch
+    for name, x in (("q", q), ("k", k)):
+        if x is None or x.dim() != 3:
+            raise ValueError(f"{name} must be [rows, heads, head_dim]")
+    if q_offsets is None or q_offsets.dim() != 1 or kv_offsets is None or kv_offsets.numel() != q_offsets.numel():
+        raise ValueError("q_offsets and kv_offsets must be 1-D [B+1] of equal length")
+    tdt = q.dtype
+    qs, ks = tuple(int(x) for x in q.shape), tuple(int(x) for x in k.shape)
+    B = int(q_offsets.numel() - 1)
+    ptrs = (_chk(q, "q", tdt, shape=qs), _chk(k, "k", tdt, shape=ks), _chk(v, "v", tdt, shape=ks),
+            _chk(o, "o", tdt, shape=qs), _chk(q_offsets, "q_offsets", torch.int32, numel=2),
+            _chk(kv_offsets, "kv_offsets", torch.int32, numel=2))
+    at = CEAttn(B, qs[1], ks[1], qs[2], ptrs[4], ptrs[5], qs[0], ks[0], int(bool(causal)), float(scale),
+                _dtype_code(q))
+    _check(lib.ce_routed_attention(ctypes.byref(at), ptrs[0], ptrs[1], ptrs[2], ptrs[3], _stream(stream)),
+           "ce_routed_attention")
 
 
 __all__ = [

@@ -373,3 +373,22 @@ def test_down_split_policy_of_named_workloads(i, split):
     tiles = ((cap + 255) // 256 + n_sets - 1) * ((p["d"] + 255) // 256)
     act = cap * p["F"] * elem
     assert (need >= act + tiles * 2 * 256 * 256 * 4) == split
+
+
+def test_binding_rejects_host_tensors_before_any_call():
+    """The binding checks what a pointer cannot carry (device, dtype, size,
+    alignment) before calling the library; host tensors never reach it."""
+    import torch
+    wl = small_workload("und", seed=0, dtype="bf16", d=64, F=64, r_c=32, r_e=32)
+    t = lambda x, dt=None: torch.from_numpy(np.ascontiguousarray(x)) if dt is None else \
+        torch.from_numpy(np.ascontiguousarray(x)).to(dt)
+    batch = ce.Batch(t(wl.seq_offsets), t(wl.flags), t(wl.t), float(wl.keep), wl.T)
+    with pytest.raises(ValueError, match="GPU memory"):
+        batch.c()
+    sw = wl.scorer
+    scorer = ce.Scorer(t(sw.w1_core, torch.bfloat16), t(sw.w2_core), t(sw.w1_exp, torch.bfloat16), t(sw.w2_exp))
+    with pytest.raises(ValueError):
+        scorer.c()
+    with pytest.raises(ValueError):
+        ce.ce_score(batch, t(wl.hidden, torch.bfloat16), scorer, torch.empty(wl.T))
+

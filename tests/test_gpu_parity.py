@@ -369,3 +369,32 @@ def test_block_without_optional_outputs(G):
     torch.cuda.synchronize()
     full = run_block(G, wl)
     np.testing.assert_array_equal(G.host(h), full["y"])
+
+
+# ---------------------------------------------------------------- binding checks
+def test_binding_rejects_bad_tensors(G):
+    """Wrong dtype, too few elements, a misaligned slice or a wrong shape is a
+    ValueError in the binding; nothing reaches the device."""
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = small_workload("und", seed=9, dtype="bf16", d=64, F=64, r_c=32, r_e=32)
+    dw = G.DevWorkload(wl)
+    logits = torch.empty(wl.T, device="cuda")
+    kept_idx, kept_off = dw.new_idx()
+    ws = dw.ws(ce.CE_WS_TOPK)
+    bad_calls = [
+        lambda: ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits[: wl.T - 1]),               # too small
+        lambda: ce.ce_score(dw.batch, dw.hidden, dw.scorer, logits.double()),                 # dtype
+        lambda: ce.ce_score(dw.batch, dw.hidden[:, :32].contiguous(), dw.scorer, logits),     # shape
+        lambda: ce.ce_score(dw.batch, dw.hidden.float(), dw.scorer, logits),                  # dtype
+        lambda: ce.ce_topk_compact(dw.batch, logits, kept_idx[: dw.cap - 1], kept_off, ws),   # capacity
+        lambda: ce.ce_topk_compact(dw.batch, logits, kept_idx.long(), kept_off, ws),          # int64 idx
+        lambda: ce.ce_topk_compact(dw.batch, logits, kept_idx, kept_off[1:], ws),             # misaligned
+        lambda: ce.ce_topk_compact(dw.batch, logits, kept_idx, kept_off, ws[:64]),            # workspace
+        lambda: ce.ce_topk_compact(ce.Batch(dw.seq_offsets.long(), dw.flags, dw.t, wl.keep, dw.cap),
+                                   logits, kept_idx, kept_off, ws),                            # int64 offsets
+    ]
+    for i, call in enumerate(bad_calls):
+        with pytest.raises(ValueError):
+            call()
+        print(f"[binding] bad call {i} rejected", flush=True)
