@@ -219,6 +219,25 @@ int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidd
                     void* stream);
 
 /*
+ * ce_topk_compact without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, serving loops or harnesses that forbid
+ * hipMalloc). Same arguments and results as ce_topk_compact, except:
+ *   - no ws / ws_bytes: the per-sequence summaries live in a fixed array of
+ *     786,688 bytes in device memory that the library holds on each GPU it
+ *     runs on until the process ends (looked up on the first call on a
+ *     device); calls that overlap on one GPU share it and race;
+ *   - status  device uint32 [1] out, or NULL: the status word (CE_DEV_* bits)
+ *             that ce_topk_compact writes into its workspace;
+ *   - at most CE_NOALLOC_MAX_B sequences: larger batches return
+ *     CE_ERR_UNSUPPORTED before anything is enqueued.
+ * Allocates nothing: no hipMalloc, no hipFree, no allocating library call.
+ */
+enum { CE_NOALLOC_MAX_B = 65536 };
+int ce_topk_compact_noalloc(const ce_batch* batch, const float* logits, const void* hidden,
+                            int dtype, int32_t d, int32_t* kept_idx, int32_t* kept_offsets,
+                            int32_t* token_pos, void* compact, uint32_t* status, void* stream);
+
+/*
  * Step 4 -- SwiGLU FFN on the packed rows (section 3.4, after Eq. 6: the
  * retained tokens are packed into a shorter sequence and only that sequence
  * runs through the layer's FFN; in a mixture-of-transformers backbone, section

@@ -38,7 +38,7 @@ EXPORTED = [
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
-    "ce_routed_attention", "ce_score_tiling",
+    "ce_routed_attention", "ce_score_tiling", "ce_topk_compact_noalloc",
 ]
 
 
@@ -102,6 +102,8 @@ _sig("ce_workspace_status", ctypes.c_int, [_p, ctypes.POINTER(ctypes.c_uint32), 
 _sig("ce_score", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, ctypes.POINTER(CEScorerW), _p, _p, _p])
 _sig("ce_topk_compact", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p,
                                        _p, _p, ctypes.c_size_t, _p])
+_sig("ce_topk_compact_noalloc", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p,
+                                               _p, _p, _p, _p])
 _sig("ce_routed_ffn", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
                                      ctypes.c_size_t, _p])
 _sig("ce_ffn_gateup", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
@@ -409,6 +411,33 @@ def ce_topk_compact(batch: Batch, logits, kept_idx, kept_offsets, ws, token_pos=
            "ce_topk_compact")
 
 
+def ce_topk_compact_noalloc(batch: Batch, logits, kept_idx, kept_offsets, token_pos=None, hidden=None,
+                            compact=None, status=None, stream=None):
+    """ce_topk_compact without a workspace (the library's fixed per-GPU
+    scratch holds the summaries; calls overlapping on one GPU race). status:
+    optional uint32-sized device tensor (int32 is accepted) for the status word."""
+    import torch
+    cb = batch.c()
+    T, B, cap = batch.T, batch.B, int(batch.kept_capacity)
+    dtype = _dtype_code(hidden) if hidden is not None else CE_F32
+    d = int(hidden.shape[1]) if hidden is not None and hidden.dim() == 2 else 0
+    hp = cp = None
+    if compact is not None:
+        if hidden is None:
+            raise ValueError("compact needs hidden")
+        hp = _hidden(hidden, "hidden", T, d, hidden.dtype)
+        cp = _chk(compact, "compact", hidden.dtype, shape=(None, d), rows_min=cap)
+    if status is not None and status.dtype not in (torch.int32, torch.uint32):
+        raise ValueError("status must be a 4-byte integer tensor")
+    i32 = torch.int32
+    _check(lib.ce_topk_compact_noalloc(ctypes.byref(cb), _chk(logits, "logits", torch.float32, numel=T), hp,
+                                       dtype, d, _chk(kept_idx, "kept_idx", i32, numel=cap),
+                                       _chk(kept_offsets, "kept_offsets", i32, numel=B + 1),
+                                       _chk(token_pos, "token_pos", i32, numel=T, optional=True), cp,
+                                       _chk(status, "status", numel=1, optional=True), _stream(stream)),
+           "ce_topk_compact_noalloc")
+
+
 def _ffn_common(batch: Batch, ffn: FFN, kept_idx, kept_offsets):
     import torch
     cb, fw = batch.c(), ffn.c()
@@ -585,7 +614,7 @@ def ce_routed_attention(q, k, v, o, q_offsets, kv_offsets, causal, scale, stream
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
-    "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
+    "ce_score", "ce_topk_compact", "ce_topk_compact_noalloc", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "ce_routed_attention", "CEAttn",

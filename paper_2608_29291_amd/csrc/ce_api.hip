@@ -152,6 +152,45 @@ int ffn_prologue(const ce_batch* batch, const void* in, const int32_t* kept_idx,
   return CE_OK;
 }
 
+// Arguments of ce_topk_compact / ce_topk_compact_noalloc shared by both (the
+// workspace and the scratch are checked by the callers).
+int topk_args_ok(const ce_batch* batch, const float* logits, const void* hidden, int dtype, int32_t d,
+                 const int32_t* kept_idx, const int32_t* kept_offsets, const void* compact) {
+  CE_CHECK(check_batch(batch, false));
+  if (!kept_offsets) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && !logits) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && !kept_idx) return CE_ERR_INVALID_ARG;
+  if (compact) {
+    CE_CHECK(check_dtype_d(dtype, d));
+    if (batch->T > 0 && !hidden) return CE_ERR_INVALID_ARG;
+  }
+  return CE_OK;
+}
+
+// The TopK launches: per-sequence summaries into `info` [3 B], selection and
+// index maps (status word into `status`), optional gather.
+int topk_launch(const ce_batch* batch, const float* logits, const void* hidden, int dtype, int32_t d,
+                int32_t* kept_idx, int32_t* kept_offsets, int32_t* token_pos, void* compact, int32_t* info,
+                uint32_t* status, hipStream_t s) {
+  CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));
+  SelectArgs sa{};
+  sa.logits = logits;
+  sa.flags = batch->flags;
+  sa.info = info;
+  sa.B = batch->B;
+  sa.keep = batch->keep;
+  sa.cap = batch->kept_capacity;
+  sa.kept_idx = kept_idx;
+  sa.kept_offsets = kept_offsets;
+  sa.token_pos = token_pos;
+  sa.status = status;
+  CE_TRY(launch_select(sa, s));
+  if (compact)
+    CE_TRY(launch_gather(static_cast<const char*>(hidden), (int64_t)d * elem_size(dtype), kept_idx, kept_offsets,
+                         batch->B, batch->kept_capacity, static_cast<char*>(compact), s));
+  return CE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -177,36 +216,12 @@ int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w, fl
 int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidden, int dtype,
                     int32_t d, int32_t* kept_idx, int32_t* kept_offsets, int32_t* token_pos,
                     void* compact, void* ws, size_t ws_bytes, void* stream) {
-  CE_CHECK(check_batch(batch, false));
-  if (!kept_offsets) return CE_ERR_INVALID_ARG;
-  if (batch->T > 0 && !logits) return CE_ERR_INVALID_ARG;
-  if (batch->kept_capacity > 0 && !kept_idx) return CE_ERR_INVALID_ARG;
-  if (compact) {
-    CE_CHECK(check_dtype_d(dtype, d));
-    if (batch->T > 0 && !hidden) return CE_ERR_INVALID_ARG;
-  }
+  CE_CHECK(topk_args_ok(batch, logits, hidden, dtype, d, kept_idx, kept_offsets, compact));
   const int elem = compact ? elem_size(dtype) : 4;
   const WsLayout L = ws_layout(CE_WS_TOPK, batch->B, batch->T, batch->kept_capacity, 0, 0, elem);
   CE_CHECK(check_ws(ws, ws_bytes, L.total));
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  int32_t* info = at<int32_t>(ws, L.seq_info);
-  CE_TRY(launch_seq_info(batch->seq_offsets, batch->flags, batch->B, batch->T, info, s));
-  SelectArgs sa{};
-  sa.logits = logits;
-  sa.flags = batch->flags;
-  sa.info = info;
-  sa.B = batch->B;
-  sa.keep = batch->keep;
-  sa.cap = batch->kept_capacity;
-  sa.kept_idx = kept_idx;
-  sa.kept_offsets = kept_offsets;
-  sa.token_pos = token_pos;
-  sa.status = at<uint32_t>(ws, L.status);
-  CE_TRY(launch_select(sa, s));
-  if (compact)
-    CE_TRY(launch_gather(static_cast<const char*>(hidden), (int64_t)d * elem, kept_idx, kept_offsets,
-                         batch->B, batch->kept_capacity, static_cast<char*>(compact), s));
-  return CE_OK;
+  return topk_launch(batch, logits, hidden, dtype, d, kept_idx, kept_offsets, token_pos, compact,
+                     at<int32_t>(ws, L.seq_info), at<uint32_t>(ws, L.status), static_cast<hipStream_t>(stream));
 }
 
 int ce_ffn_gateup(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
@@ -471,3 +486,63 @@ int ce_routed_attention(const ce_attn* at, const void* q, const void* k, const v
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// TopK and packing without a workspace, for callers that cannot allocate
+// (code under HIP graph capture, serving loops that forbid hipMalloc). The
+// summaries and the status word live in a fixed array in device memory instead
+// of the caller's workspace; every call on a GPU shares that GPU's copy, so
+// calls that overlap on one GPU race.
+// ---------------------------------------------------------------------------
+#include <atomic>
+#include <mutex>
+
+namespace {
+
+// Layout of `scratch`: the status word (padded to 256 bytes), then the
+// per-sequence summaries, 3 int32 per sequence, for at most CE_NOALLOC_MAX_B
+// sequences: 786,688 bytes per GPU, held until the process ends.
+constexpr size_t kScratchStatusBytes = 256;
+constexpr size_t kScratchBytes = kScratchStatusBytes + (size_t)3 * CE_NOALLOC_MAX_B * sizeof(int32_t);
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address is looked up once per device (with that device current) and
+// only that address is passed to kernels.
+constexpr int kMaxDevices = 64;
+std::atomic<char*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+int scratch_of_current_device(char** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CE_ERR_HIP;
+  char* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      void* addr = nullptr;
+      if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return CE_ERR_HIP;
+      p = static_cast<char*>(addr);
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return CE_OK;
+}
+
+}  // namespace
+
+extern "C" int ce_topk_compact_noalloc(const ce_batch* batch, const float* logits, const void* hidden,
+                                       int dtype, int32_t d, int32_t* kept_idx, int32_t* kept_offsets,
+                                       int32_t* token_pos, void* compact, uint32_t* status, void* stream) {
+  CE_CHECK(topk_args_ok(batch, logits, hidden, dtype, d, kept_idx, kept_offsets, compact));
+  if (batch->B > CE_NOALLOC_MAX_B) return CE_ERR_UNSUPPORTED;
+  char* sc = nullptr;
+  CE_CHECK(scratch_of_current_device(&sc));
+  // the summaries are written in full by the first launch and the status
+  // word by the second, so nothing left by an earlier call is read
+  uint32_t* st = status ? status : reinterpret_cast<uint32_t*>(sc);
+  return topk_launch(batch, logits, hidden, dtype, d, kept_idx, kept_offsets, token_pos, compact,
+                     reinterpret_cast<int32_t*>(sc + kScratchStatusBytes), st, static_cast<hipStream_t>(stream));
+}

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 21
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -392,3 +392,15 @@ def test_binding_rejects_host_tensors_before_any_call():
     with pytest.raises(ValueError):
         ce.ce_score(batch, t(wl.hidden, torch.bfloat16), scorer, torch.empty(wl.T))
 
+
+def test_noalloc_topk_validation():
+    """ce_topk_compact_noalloc rejects bad arguments and batches beyond its
+    fixed scratch before any HIP call (so these run without a GPU)."""
+    f = ce.lib.ce_topk_compact_noalloc
+    b = _batch()
+    assert f(None, FAKE, None, 0, 0, FAKE, FAKE, None, None, None, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), FAKE, None, 0, 0, FAKE, None, None, None, None, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), None, None, 0, 0, FAKE, FAKE, None, None, None, None) == ce.CE_ERR_INVALID_ARG
+    assert f(ctypes.byref(b), FAKE, FAKE, ce.CE_BF16, 100, FAKE, FAKE, None, FAKE, None, None) == ce.CE_ERR_UNSUPPORTED
+    big = _batch(B=65537, T=70000, cap=70000)
+    assert f(ctypes.byref(big), FAKE, None, 0, 0, FAKE, FAKE, None, None, None, None) == ce.CE_ERR_UNSUPPORTED
