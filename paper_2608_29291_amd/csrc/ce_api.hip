@@ -122,10 +122,12 @@ FfnGemmArgs down_args(const ce_ffn_w* w, const ce_batch* b, const char* act, con
   return a;
 }
 
-// Split-K scratch of the down GEMM (present when the layout reserved it).
-void set_down_split(FfnGemmArgs& a, void* ws, const WsLayout& L) {
-  a.part = L.down_part ? at<float>(ws, L.down_part) : nullptr;
-  a.tile_cnt = L.down_cnt ? at<int32_t>(ws, L.down_cnt) : nullptr;
+// Partial sums and arrival counters of a GEMM launch's split tail tiles
+// (present when the layout reserved them); mode 0 = gate/up, 1 = down.
+void set_split(FfnGemmArgs& a, void* ws, const WsLayout& L, int mode) {
+  a.part = L.gemm_part ? at<float>(ws, L.gemm_part) : nullptr;
+  const size_t cnt = mode == 0 ? L.gu_cnt : L.dn_cnt;
+  a.tile_cnt = (L.gemm_part && cnt) ? at<int32_t>(ws, cnt) : nullptr;
 }
 
 // Shared argument checks of the staged FFN calls; on success fills the
@@ -231,8 +233,11 @@ int ce_ffn_gateup(const ce_batch* batch, const void* compact, const int32_t* kep
   int32_t *grp, *n0;
   CE_CHECK(ffn_prologue(batch, compact, kept_idx, kept_offsets, w, act, ws, ws_bytes, s, &grp, &n0));
   if (batch->kept_capacity == 0) return CE_OK;
-  const FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr,
-                                    static_cast<char*>(act), grp, kept_offsets + batch->B, n0);
+  const WsLayout L = ws_layout(CE_WS_FFN, batch->B, batch->T, batch->kept_capacity, w->d, w->d_ff,
+                               elem_size(w->dtype));
+  FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr,
+                              static_cast<char*>(act), grp, kept_offsets + batch->B, n0);
+  set_split(g, ws, L, 0);
   CE_TRY(launch_ffn_gateup(g, w->dtype == CE_BF16, s));
   return CE_OK;
 }
@@ -249,7 +254,7 @@ int ce_ffn_down(const ce_batch* batch, const void* act, const int32_t* kept_idx,
   FfnGemmArgs dn = down_args(w, batch, static_cast<const char*>(act), grp,
                              static_cast<char*>(ffn_out), grp, nullptr, nullptr,
                              kept_offsets + batch->B, n0);
-  set_down_split(dn, ws, L);
+  set_split(dn, ws, L, 1);
   CE_TRY(launch_ffn_down(dn, w->dtype == CE_BF16, s));
   return CE_OK;
 }
@@ -270,10 +275,11 @@ int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kep
   char* act = at<char>(ws, L.act);
   FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr,
                              nullptr, kt, n0);
-  set_down_split(dn, ws, L);
+  set_split(dn, ws, L, 1);
   FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr, act,
                               nullptr, kt, n0);
-  g.clear_n = ffn_down_split_tiles(dn, bf16);
+  set_split(g, ws, L, 0);
+  g.clear_n = ffn_split_counters(dn, 1, bf16);
   g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
   CE_TRY(launch_ffn_gateup(g, bf16, s));
   CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
@@ -333,7 +339,23 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   } else {
     CE_TRY(launch_score(sa, bf16, s));
   }
-  // 2-3. per-sequence TopK + packed index maps (Eq. 6)
+  // FFN launch arguments (host-known; the row counts stay on the device)
+  const int32_t* kt = kept_off + batch->B;
+  int32_t* grp = ffn->n_sets == 2 ? at<int32_t>(ws, L.grp_rows) : nullptr;
+  int32_t* n0 = ffn->n_sets == 2 ? at<int32_t>(ws, L.grp_n0) : nullptr;
+  char* act = at<char>(ws, L.act);
+  FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
+                             kept_idx, static_cast<const char*>(hidden_in), kt, n0);
+  set_split(dn, ws, L, 1);
+  FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx, act,
+                              nullptr, kt, n0);
+  set_split(g, ws, L, 0);
+  g.clear_n = ffn_split_counters(dn, 1, bf16);
+  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
+  const int gu_counters = ffn_split_counters(g, 0, bf16);
+
+  // 2-3. per-sequence TopK + packed index maps (Eq. 6); the select launch
+  //      also clears the gate/up launch's arrival counters
   SelectArgs sel{};
   sel.logits = logits;
   if (tiled) {
@@ -357,6 +379,8 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
   sel.kept_offsets = kept_off;
   sel.token_pos = token_pos;
   sel.status = at<uint32_t>(ws, L.status);
+  sel.clear_cnt = gu_counters > 0 ? g.tile_cnt : nullptr;
+  sel.clear_n = gu_counters;
   CE_TRY(launch_select(sel, s));
   // bypass path for a separate output buffer: dropped rows copied unchanged
   if (hidden_in != hidden_out)
@@ -364,24 +388,10 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                             (int64_t)ffn->d * elem, batch->T, token_pos, s));
   if (batch->kept_capacity == 0) return CE_OK;
   // 4. SwiGLU FFN on the retained rows, gathered straight from hidden_in
-  const int32_t* kt = kept_off + batch->B;
-  int32_t* grp = nullptr;
-  int32_t* n0 = nullptr;
-  if (ffn->n_sets == 2) {
-    grp = at<int32_t>(ws, L.grp_rows);
-    n0 = at<int32_t>(ws, L.grp_n0);
+  if (ffn->n_sets == 2)
     CE_TRY(launch_group(kept_idx, kept_off, batch->B, batch->kept_capacity, batch->T, batch->flags,
                         grp, n0, s));
-  }
-  char* act = at<char>(ws, L.act);
-  FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
-                             kept_idx, static_cast<const char*>(hidden_in), kt, n0);
-  set_down_split(dn, ws, L);
-  FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx, act,
-                              nullptr, kt, n0);
-  g.clear_n = ffn_down_split_tiles(dn, bf16);
-  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
-  CE_TRY(launch_ffn_gateup(g, bf16, s));
+  CE_TRY(launch_ffn_gateup(g, bf16, s, gu_counters > 0));
   // 5. down projection + residual, scattered straight into the token rows
   CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
   return CE_OK;

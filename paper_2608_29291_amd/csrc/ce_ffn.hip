@@ -310,10 +310,13 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
 // bank line, so the 8 rows of each parity need 8 distinct keys for the 16
 // lanes to cover all 64 banks (a key of r & 7 repeats every 8 rows: 2-way
 // conflicts, measured as half of the LDS busy time).
+// kSplit: 1 = whole tiles only; 2 = tail tiles in two K pieces; 0 = tail
+// tiles in sp.pieces > 2 K pieces (separate instances keep the whole-tile and
+// two-piece code free of the general merge).
 template <int kMode, int kGroup, bool kPrio, int kSplit, int kWBufs = 2, bool kSpreadW = true,
           bool kSpreadT = true>
 __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) void ffn_gemm_pp2_kernel(
-    FfnGemmArgs a, int n_tt, int n_ft) {
+    FfnGemmArgs a, int n_tt, int n_ft, GemmSplit sp) {
   constexpr int kWR = 256, kTR = 256;
   constexpr int kMW = 4, kMT = 2;
   constexpr int kRow = 128;                  // bytes of K per staged row
@@ -333,18 +336,28 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int wt = wave >> 1;
   const bool late = wave >= 4;  // group B
 
-  static_assert(kSplit == 1 || kSplit == 2, "two K halves at most (their sum is order-free)");
-  static_assert(kSplit == 1 || kMode == 1, "only the down GEMM splits K");
-  const int total = n_tt * n_ft * kSplit;
-  const int per = (total + kXcds - 1) / kXcds;
-  const int wk = (int)(blockIdx.x % kXcds) * per + (int)(blockIdx.x / kXcds);
-  if (wk >= total) return;
-  // K half kz of tile w: the first halves of all tiles, then the second
-  // halves, so each XCD streams one half of K of its tiles (a third fewer
-  // distinct operand bytes through its L2 than both halves of half as many
-  // tiles); the two halves meet through device-coherent memory wherever they run
-  const int kz = kSplit == 1 ? 0 : wk / (total / kSplit);
-  const int w = wk - kz * (total / kSplit);
+  // ---- work item of this workgroup (see GemmSplit): the first whole_x
+  //      workgroups of XCD x = blockIdx % 8 take whole tiles of its range
+  //      [x per_x, (x + 1) per_x); the other workgroups of all XCDs take the
+  //      K pieces of the tail tiles, numbered piece-major, so that each XCD
+  //      streams one or two K ranges of many tail tiles (fewer distinct
+  //      operand bytes through its L2 than every range of a few tiles) ----
+  const int total = n_tt * n_ft;
+  const int xcd = (int)(blockIdx.x % kXcds);
+  const int loc = (int)(blockIdx.x / kXcds);
+  int w, piece = 0, pieces = 1, slot = 0;
+  if (kSplit == 1 || loc < sp.whole_x) {
+    w = xcd * sp.per_x + loc;
+  } else {
+    const int n_tail = kXcds * sp.tail_x;  // tail tiles of the launch
+    pieces = kSplit == 2 ? 2 : sp.pieces;
+    const int g = xcd * (sp.tail_x * pieces) + (loc - sp.whole_x);
+    piece = g / n_tail;
+    slot = g - piece * n_tail;  // partial-sum tiles [slot x pieces, + pieces), counter [slot]
+    const int sx = slot / sp.tail_x;
+    w = sx * sp.per_x + sp.whole_x + (slot - sx * sp.tail_x);
+  }
+  if (w >= total) return;
   const int grp = w / (kGroup * n_tt);
   const int rem = w - grp * (kGroup * n_tt);
   const int gsz = min(kGroup, n_ft - grp * kGroup);
@@ -475,11 +488,11 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const uint32_t rowb = (uint32_t)((wt * 64 + lrow) * kRow);
   u32x4_t fa[2][kMW], fb[2][kMT];
 
-  // superslabs [s0, ns) of K: all of them, or one half when K is split
-  // (>= 3 per range, checked by the launcher)
+  // superslabs [s0, ns) of K: all of them, or this piece's range when the
+  // tile is split (>= 3 per range, checked by the launcher)
   const int ns_all = a.k_bytes / kRow;
-  const int s0 = ns_all * kz / kSplit;
-  const int ns = ns_all * (kz + 1) / kSplit;
+  const int s0 = ns_all * piece / pieces;
+  const int ns = ns_all * (piece + 1) / pieces;
   // each ring starts with all but one of its slots in flight; the first
   // superslab must have landed
   constexpr int kBufs0 = kWBufs;  // waves 0-3 (weights)
@@ -573,70 +586,95 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   if (mfma_on) kloop(std::true_type{});
   else kloop(std::false_type{});
 
-  if constexpr (kSplit == 2) {
+  // K pieces of a tail tile meet through the workspace: each writes its
+  // sums, then bumps the tile's arrival counter; the last to arrive adds the
+  // pieces up and finishes the tile. Nobody waits on anybody. The sums move
+  // with device-coherent (sc1) stores and loads, so no L2 write-back or
+  // invalidation is needed; the counter is an agent-scope atomic issued after
+  // this workgroup's stores have completed. Two pieces: the last adds the
+  // other's sums to its own (two addends commute, so the result does not
+  // depend on which came last); more: the last re-reads all of them and adds
+  // them in piece order, so the result is the same whichever came last.
+  constexpr int kSC1 = 16;  // cache-policy operand: sc1
+  // register order: per lane 32 float4, one wave instruction = 1 KB contiguous
+  auto part_off = [&](int i, int j, int v4) __attribute__((always_inline)) {
+    return (uint32_t)((((wave * 32 + (i * kMT + j) * 4 + v4) * 64) + lane) * 16);
+  };
+  if (kSplit != 1 && pieces > 1) {
     if (!late) lds_barrier();  // both groups in step from here on
-    // The two K halves of a tile meet through the workspace: each writes its
-    // sums, then bumps the tile's arrival counter; the second to arrive adds
-    // the other's sums and finishes the tile. Nobody waits on anybody. The
-    // sums move with device-coherent (sc1) stores and loads, so no L2
-    // write-back or invalidation is needed; the counter is an agent-scope
-    // atomic issued after this workgroup's stores have completed.
-    constexpr int kSC1 = 16;  // cache-policy operand: sc1
-    const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.part + (int64_t)w * 2 * (256 * 256), 2 * 256 * 256 * 4);
-    const uint32_t mine = (uint32_t)kz * (256 * 256 * 4);
-    // register order: per lane 32 float4, one store instruction = 1 KB contiguous
+    const __amdgpu_buffer_rsrc_t prs =
+        make_rsrc(a.part + (int64_t)slot * pieces * (256 * 256), (uint32_t)pieces * (256 * 256 * 4));
+    const uint32_t mine = (uint32_t)piece * (256 * 256 * 4);
 #pragma unroll
     for (int i = 0; i < kMW; ++i)
 #pragma unroll
       for (int j = 0; j < kMT; ++j)
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
-          const uint32_t o = (uint32_t)((((wave * 32 + (i * kMT + j) * 4 + v4) * 64) + lane) * 16);
           const u32x4_t x = {__float_as_uint(acc[i][j][4 * v4]), __float_as_uint(acc[i][j][4 * v4 + 1]),
                              __float_as_uint(acc[i][j][4 * v4 + 2]), __float_as_uint(acc[i][j][4 * v4 + 3])};
-          __builtin_amdgcn_raw_buffer_store_b128(x, prs, (int)(mine + o), 0, kSC1);
+          __builtin_amdgcn_raw_buffer_store_b128(x, prs, (int)(mine + part_off(i, j, v4)), 0, kSC1);
         }
     wait_vmcnt<0>();  // this wave's sums have reached the coherence point
     __syncthreads();
     int* const arrived = reinterpret_cast<int*>(smem);  // the rings are no longer read
     if (tid == 0)
-      arrived[0] = __hip_atomic_fetch_add(a.tile_cnt + w, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      arrived[0] = __hip_atomic_fetch_add(a.tile_cnt + slot, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    if (arrived[0] == 0) return;  // first half done: the other finishes the tile
-    // the other half's sums are added row block by row block in the epilogue
+    const int order = arrived[0];
+    __syncthreads();  // read by every wave before the epilogue reuses the LDS
+    if (order != pieces - 1) return;  // another piece finishes the tile
+    // the sums are added row block by row block in the epilogue (merge_block)
   }
-  // adds the other K half's sums to row block j, in batches of 8 loads (32
-  // registers next to the 128 accumulators)
+  // row block j of the tile: adds the other pieces' sums (see above), one
+  // 32-row block at a time, 4 float4 loads per piece and two pieces in flight
+  // (32 registers next to the 128 accumulators and the residual values)
   auto merge_block = [&](int j) __attribute__((always_inline)) {
-    if constexpr (kSplit == 2) {
-      const __amdgpu_buffer_rsrc_t prs = make_rsrc(a.part + (int64_t)w * 2 * (256 * 256), 2 * 256 * 256 * 4);
-      const uint32_t other = (uint32_t)(kz ^ 1) * (256 * 256 * 4);
+    if (kSplit == 1 || pieces <= 1) return;
+    const __amdgpu_buffer_rsrc_t prs =
+        make_rsrc(a.part + (int64_t)slot * pieces * (256 * 256), (uint32_t)pieces * (256 * 256 * 4));
+    auto load4 = [&](u32x4_t (&y)[4], int p, int i) __attribute__((always_inline)) {
+      const uint32_t base = (uint32_t)p * (256 * 256 * 4);
 #pragma unroll
-      for (int i0 = 0; i0 < kMW; i0 += 2) {
-        u32x4_t y[2][4];
+      for (int v4 = 0; v4 < 4; ++v4)
+        y[v4] = __builtin_bit_cast(
+            u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, (int)(base + part_off(i, j, v4)), 0, kSC1));
+    };
+    auto add4 = [&](const u32x4_t (&y)[4], int i, bool first) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const f32x4_t v = {__uint_as_float(y[v4].x), __uint_as_float(y[v4].y), __uint_as_float(y[v4].z),
+                           __uint_as_float(y[v4].w)};
 #pragma unroll
-          for (int v4 = 0; v4 < 4; ++v4) {
-            const uint32_t o = (uint32_t)((((wave * 32 + ((i0 + i) * kMT + j) * 4 + v4) * 64) + lane) * 16);
-            y[i][v4] = __builtin_bit_cast(u32x4_t,
-                                          __builtin_amdgcn_raw_buffer_load_b128(prs, (int)(other + o), 0, 16 /* sc1 */));
-          }
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int v4 = 0; v4 < 4; ++v4) {
-            // two addends: the sum does not depend on which half came last
-            acc[i0 + i][j][4 * v4] += __uint_as_float(y[i][v4].x);
-            acc[i0 + i][j][4 * v4 + 1] += __uint_as_float(y[i][v4].y);
-            acc[i0 + i][j][4 * v4 + 2] += __uint_as_float(y[i][v4].z);
-            acc[i0 + i][j][4 * v4 + 3] += __uint_as_float(y[i][v4].w);
-          }
-        // the sums are materialized here: otherwise the compiler sinks the
-        // adds to the epilogue's stores and keeps every loaded value live
-        // (spilling) until then
-        asm volatile("" : "+v"(acc[i0][j]), "+v"(acc[i0 + 1][j])::"memory");
+        for (int e = 0; e < 4; ++e) acc[i][j][4 * v4 + e] = first ? v[e] : acc[i][j][4 * v4 + e] + v[e];
       }
+    };
+    // two pieces: the other piece's sums, two 32-row feature blocks per
+    // batch; more: acc = p_0 + p_1 + ... + p_{S-1}, one feature block per
+    // batch and two pieces' loads in flight. Both use 32 registers.
+    const bool two = kSplit == 2;
+#pragma unroll
+    for (int i = 0; i < kMW; i += 2) {
+      u32x4_t y[2][4];
+      if (two) {
+        load4(y[0], piece ^ 1, i);
+        load4(y[1], piece ^ 1, i + 1);
+        add4(y[0], i, false);
+        add4(y[1], i + 1, false);
+      } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          for (int p = 0; p < pieces; p += 2) {
+            load4(y[0], p, i + h);
+            if (p + 1 < pieces) load4(y[1], p + 1, i + h);
+            add4(y[0], i + h, p == 0);
+            if (p + 1 < pieces) add4(y[1], i + h, false);
+          }
+      }
+      // the sums are materialized here: otherwise the compiler sinks the
+      // adds to the epilogue's stores and keeps every loaded value live
+      // (spilling) until then
+      asm volatile("" : "+v"(acc[i][j]), "+v"(acc[i + 1][j])::"memory");
     }
   };
 
@@ -666,7 +704,13 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
           }
       }
     };
-    if (!late) {
+    if (kSplit != 1 && pieces > 1) {
+      // last piece of a split tile: every wave is in step and past the rings
+      merge_block(0);
+      merge_block(1);
+      stage();
+      lds_barrier();
+    } else if (!late) {
       stage();
       lds_barrier();
       lds_barrier();
@@ -739,34 +783,52 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   }
   // group A's extra barrier at the end matches group B's at the start (the
   // gate/up path above already ends in step)
-  if (kMode == 1 && kSplit == 1 && !late) lds_barrier();
+  if (kMode == 1 && (kSplit == 1 || pieces == 1) && !late) lds_barrier();
 }
 
 __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, int n) {
   for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
 }
 
-template <int kMode, int kGroup, bool kPrio, int kSplit = 1, int kWBufs = 2, bool kSpreadW = true,
-          bool kSpreadT = true>
-hipError_t launch_pp2(const FfnGemmArgs& a, hipStream_t stream, bool counters_clear = false) {
+// Split plan of a ping-pong launch: whole tiles in full rounds per XCD, the
+// partial last round as K pieces when the workspace holds their partial sums
+// (see GemmSplit).
+template <int kMode>
+GemmSplit pp2_plan(const FfnGemmArgs& a, int* n_tt, int* n_ft) {
   constexpr int kFTile = (kMode == 0) ? 128 : 256;
-  const int n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
-  const int n_ft = (a.n_feat + kFTile - 1) / kFTile;
+  *n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
+  *n_ft = (a.n_feat + kFTile - 1) / kFTile;
+  const int64_t items = (int64_t)*n_tt * *n_ft;
+  if (a.part && a.tile_cnt) return gemm_split(items, a.k_bytes / 128);
+  GemmSplit sp;
+  sp.per_x = (int)((items + kXcds - 1) / kXcds);
+  sp.whole_x = sp.per_x;
+  sp.tail_x = 0;
+  sp.pieces = 1;
+  return sp;
+}
+
+template <int kMode, int kGroup, bool kPrio, int kWBufs = 2, bool kSpreadW = true, bool kSpreadT = true>
+hipError_t launch_pp2(const FfnGemmArgs& a, const GemmSplit& sp, int n_tt, int n_ft, hipStream_t stream,
+                      bool counters_clear) {
   if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
-  if (kSplit > 1) {
-    if (!a.part || !a.tile_cnt) return hipErrorInvalidValue;
-    // arrival counters start at zero: cleared by the preceding gate/up launch,
-    // else by a fill kernel (no memset nodes in a captured stream)
-    if (!counters_clear) {
-      hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(256), 0, stream, a.tile_cnt, n_tt * n_ft);
-      const hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
+  if (sp.pieces > 1 && !counters_clear) {
+    // arrival counters start at zero: cleared by the preceding kernel, else
+    // by a fill kernel (no memset nodes in a captured stream)
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(1), dim3(256), 0, stream, a.tile_cnt, kXcds * sp.tail_x);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  const int total = n_tt * n_ft * kSplit;
-  const int grid = ((total + kXcds - 1) / kXcds) * kXcds;
-  hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, kSplit, kWBufs, kSpreadW, kSpreadT>),
-                     dim3(grid), dim3(512), 0, stream, a, n_tt, n_ft);
+  const int grid = kXcds * (sp.whole_x + sp.tail_x * sp.pieces);
+  if (sp.pieces == 1)
+    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 1, kWBufs, kSpreadW, kSpreadT>), dim3(grid),
+                       dim3(512), 0, stream, a, n_tt, n_ft, sp);
+  else if (sp.pieces == 2)
+    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 2, kWBufs, kSpreadW, kSpreadT>), dim3(grid),
+                       dim3(512), 0, stream, a, n_tt, n_ft, sp);
+  else
+    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 0, kWBufs, kSpreadW, kSpreadT>), dim3(grid),
+                       dim3(512), 0, stream, a, n_tt, n_ft, sp);
   return hipGetLastError();
 }
 
@@ -798,14 +860,15 @@ hipError_t launch_cfg(const FfnGemmArgs& a, hipStream_t stream) {
 // Kernel and tile choice, from timing every variant on the five named workloads:
 //   gate/up: the full-line ping-pong kernel (128 output features x 256 tokens,
 //            groups of 8 feature tiles); fallback 8-wave 256 x 256 register-staged;
-//   down:    the full-line ping-pong kernel over two K halves (groups of 6)
-//            when the cost model of down_split_tiles prefers it (uneven
-//            rounds: 108 tiles at the understanding workload, 294 at the 7B
-//            width), else the same kernel over whole tiles when they number
-//            >= 200 (groups of 8 feature tiles), else 256 x 128 (4 x 2 waves)
-//            for d < 3072 and 128 x 128 (2 x 2 waves) for the 7B width,
-//            token-tile-major order (every weight tile of a token tile stays in
-//            one XCD's L2).
+//   down:    the full-line ping-pong kernel (256 x 256, groups of 8 feature
+//            tiles) when its plan splits the last round or the tiles number
+//            >= 200, else 256 x 128 (4 x 2 waves) for d < 3072 and 128 x 128
+//            (2 x 2 waves) for the 7B width, token-tile-major order (every
+//            weight tile of a token tile stays in one XCD's L2).
+// Both ping-pong launches split the tiles of their last, partial round over K
+// (GemmSplit) when the workspace holds the partial sums: 3108 gate/up tiles at
+// the 7B width are 12 full rounds plus 36 tiles, 294 down tiles one round plus
+// 38, the 108 down tiles of the understanding workload less than one round.
 // fp32 data (tiny workloads) uses 128 x 128 tiles, or smaller ones when those
 // would leave most of the chip idle (fp32 MFMAs run at 1/16 of the bf16 rate,
 // so a handful of large tiles would each take tens of microseconds).
@@ -813,29 +876,37 @@ inline int64_t grid_tiles(const FfnGemmArgs& a, int feat_tile, int tok_tile) {
   return (int64_t)((a.cap + tok_tile - 1) / tok_tile + a.n_sets - 1) * ((a.n_feat + feat_tile - 1) / feat_tile);
 }
 
-hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream) {
+hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear) {
   if (bf16) {
-    if (pp2_ok(a)) return launch_pp2<0, 8, true>(a, stream);
+    if (pp2_ok(a)) {
+      int n_tt, n_ft;
+      const GemmSplit sp = pp2_plan<0>(a, &n_tt, &n_ft);
+      return launch_pp2<0, 8, true>(a, sp, n_tt, n_ft, stream, counters_clear);
+    }
     return launch_cfg<true, 0, 256, 256, 4, 2, 1, 1, 4>(a, stream);
   }
   if (grid_tiles(a, 64, 128) < 128) return launch_cfg<false, 0, 64, 64, 1, 2, 2>(a, stream);
   return launch_cfg<false, 0, 128, 128, 2, 2, 2>(a, stream);
 }
 
-int ffn_down_split_tiles(const FfnGemmArgs& a, bool bf16) {
-  if (!bf16 || !a.part || !a.tile_cnt || !pp2_ok(a)) return 0;
-  const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
-  const int t = down_split_tiles(a.cap, a.n_feat, a.k_bytes / 2, a.n_sets, 2);
-  return t == big_tiles ? t : 0;
+// the down GEMM runs on the ping-pong kernel when it splits or has >= 200 tiles
+inline bool down_on_pp2(const FfnGemmArgs& a, const GemmSplit& sp, int n_tt, int n_ft) {
+  return pp2_ok(a) && (sp.pieces > 1 || (int64_t)n_tt * n_ft >= 200);
+}
+
+int ffn_split_counters(const FfnGemmArgs& a, int mode, bool bf16) {
+  if (!bf16 || !pp2_ok(a) || !a.part || !a.tile_cnt) return 0;
+  int n_tt, n_ft;
+  const GemmSplit sp = mode == 0 ? pp2_plan<0>(a, &n_tt, &n_ft) : pp2_plan<1>(a, &n_tt, &n_ft);
+  if (mode == 1 && !down_on_pp2(a, sp, n_tt, n_ft)) return 0;
+  return sp.pieces > 1 ? kXcds * sp.tail_x : 0;
 }
 
 hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear) {
   if (bf16) {
-    // tiles that fill the chip's rounds unevenly: two K halves per tile, when
-    // the workspace holds their partial sums
-    if (ffn_down_split_tiles(a, bf16) > 0) return launch_pp2<1, 6, true, 2>(a, stream, counters_clear);
-    const int64_t big_tiles = (int64_t)((a.cap + 255) / 256 + a.n_sets - 1) * ((a.n_feat + 255) / 256);
-    if (big_tiles >= 200 && pp2_ok(a)) return launch_pp2<1, 8, true>(a, stream);
+    int n_tt, n_ft;
+    const GemmSplit sp = pp2_plan<1>(a, &n_tt, &n_ft);
+    if (down_on_pp2(a, sp, n_tt, n_ft)) return launch_pp2<1, 8, true>(a, sp, n_tt, n_ft, stream, counters_clear);
     if (a.n_feat < 3072) return launch_cfg<true, 1, 256, 128, 4, 2, 2, 1, 64>(a, stream);
     return launch_cfg<true, 1, 128, 128, 2, 2, 2, 1, 64>(a, stream);
   }

@@ -15,25 +15,52 @@ int elem_size(int dtype) {
   return 0;
 }
 
-int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem) {
-  if (elem != 2 || cap <= 0 || d <= 0 || d_ff <= 0 || n_sets < 1) return 0;
-  const int64_t k_bytes = (int64_t)d_ff * 2;
+GemmSplit gemm_split(int64_t items, int ns) {
+  GemmSplit sp;
+  sp.per_x = (int)((items + kXcdCount - 1) / kXcdCount);
+  sp.whole_x = sp.per_x;
+  sp.tail_x = 0;
+  sp.pieces = 1;
+  if (items <= 0 || ns < 6) return sp;
+  const int full = sp.per_x / kCusPerXcd * kCusPerXcd;
+  const int tail = sp.per_x - full;
+  // after more than two full rounds the workgroups' finishing times spread
+  // out enough that the dispatcher fills the last round's gaps by itself
+  // (measured: splitting the 7B-width gate/up tail, 12 rounds + 5 tiles per
+  // XCD, gained nothing)
+  if (tail == 0 || full > 2 * kCusPerXcd) return sp;
+  const double whole = (double)ns + 3.5;
+  double best = whole;
+  int best_s = 1;
+  for (int s = 2; s * tail <= kCusPerXcd && s * 3 <= ns; ++s) {
+    const double cost = (double)ns / s + 2.0 + 2.5 * (s == 2 ? 1 : s);
+    if (cost < best) {
+      best = cost;
+      best_s = s;
+    }
+  }
+  if (best_s == 1) return sp;
+  sp.whole_x = full;
+  sp.tail_x = tail;
+  sp.pieces = best_s;
+  return sp;
+}
+
+void gemm_items(int mode, int cap, int d, int d_ff, int n_sets, int elem, int64_t* items, int* ns) {
+  *items = 0;
+  *ns = 0;
+  if (elem != 2 || cap <= 0 || d <= 0 || d_ff <= 0 || n_sets < 1) return;
+  const int64_t k_bytes = (int64_t)(mode == 0 ? d : d_ff) * 2;
+  const int n_feat = mode == 0 ? d_ff : d;
   const int64_t lim = (int64_t)1 << 31;
-  // the ping-pong kernel's limits: whole 128-byte K superslabs, at least 3 of
-  // them per K half, 32-bit buffer offsets
-  if (k_bytes % 128 != 0 || k_bytes < 6 * 128) return 0;
-  if ((int64_t)cap * k_bytes >= lim || (int64_t)d * k_bytes >= lim) return 0;
-  const int64_t tiles = (int64_t)((cap + 255) / 256 + n_sets - 1) * ((d + 255) / 256);
-  if (tiles > kSplitMaxTiles) return 0;
-  // Launch cost in units of the K-loop time of one 128-byte superslab (one
-  // workgroup per CU, rounds of 256), from measured per-workgroup timelines:
-  // a whole tile adds its prologue and residual epilogue (~5.6 superslabs), a
-  // half adds the partial sums written and read back besides (~14.1).
-  const int64_t ns = k_bytes / 128;
-  auto rounds = [](int64_t n) { return (n + 255) / 256; };
-  const double whole = (double)rounds(tiles) * ((double)ns + 5.6);
-  const double halves = (double)rounds(2 * tiles) * ((double)ns / 2.0 + 14.1);
-  return halves < whole ? (int)tiles : 0;
+  if (k_bytes % 128 != 0 || k_bytes < 3 * 128) return;
+  // rows of the token operand: the hidden states (T rows, gate/up on the
+  // block path) or the packed rows; cap bounds the packed ones, and the
+  // launcher checks the actual operand before it relies on this
+  if ((int64_t)cap * k_bytes >= lim || (int64_t)n_feat * k_bytes >= lim) return;
+  const int ftile = mode == 0 ? 128 : 256;
+  *items = (int64_t)((cap + 255) / 256 + n_sets - 1) * ((n_feat + ftile - 1) / ftile);
+  *ns = (int)(k_bytes / 128);
 }
 
 int score_token_tile(int B, int T, int d, int r_core, int r_exp, int elem) {
@@ -113,14 +140,22 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
     L.grp_rows = take(sC * 4);
     L.grp_n0 = take(4);
     L.act = take(sC * sF * (size_t)elem);
-    int tiles = 0;
-    for (int n_sets = 1; n_sets <= 2; ++n_sets) {
-      const int t = down_split_tiles(cap, d, d_ff, n_sets, elem);
-      tiles = t > tiles ? t : tiles;
-    }
-    if (tiles > 0) {
-      L.down_part = take((size_t)tiles * 2 * 256 * 256 * 4);
-      L.down_cnt = take((size_t)tiles * 4);
+    // partial-sum tiles of the split tails of both GEMMs (they run one after
+    // the other, so they share the region), for either number of weight sets
+    int slots = 0;
+    for (int n_sets = 1; n_sets <= 2; ++n_sets)
+      for (int mode = 0; mode <= 1; ++mode) {
+        int64_t items;
+        int ns;
+        gemm_items(mode, cap, d, d_ff, n_sets, elem, &items, &ns);
+        const GemmSplit sp = gemm_split(items, ns);
+        const int n = kXcdCount * sp.tail_x * sp.pieces;
+        slots = n > slots ? n : slots;
+      }
+    if (slots > 0) {
+      L.gemm_part = take((size_t)slots * 256 * 256 * 4);
+      L.gu_cnt = take((size_t)kSplitMaxSlots * 4);
+      L.dn_cnt = take((size_t)kSplitMaxSlots * 4);
     }
     L.sal_part = take(((size_t)kSalSplits * sB * sF + sB * ((sF + 255) / 256) * 2) * 4);
   }

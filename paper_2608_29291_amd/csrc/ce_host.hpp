@@ -26,8 +26,9 @@ struct WsLayout {
   size_t grp_rows;   // int32 [cap]    (MoT grouping)
   size_t grp_n0;     // int32          (MoT group size)
   size_t act;        // dtype [cap * d_ff] SwiGLU activations
-  size_t down_part;  // float [2 x tiles x 256 x 256] split-K partial sums of the down GEMM
-  size_t down_cnt;   // int32 [tiles] arrival counters of the split-K down GEMM
+  size_t gemm_part;  // float [slots x 256 x 256] K-piece partial sums of the FFN GEMMs' tail tiles
+  size_t gu_cnt;     // int32 [kSplitMaxSlots] arrival counters of the gate/up tail tiles
+  size_t dn_cnt;     // int32 [kSplitMaxSlots] arrival counters of the down tail tiles
   size_t sal_part;   // float [kSalSplits x B x d_ff] FFN-saliency partial sums, then
                      // float [B x ceil(d_ff / 256) x 2] per-chunk totals
   size_t total;
@@ -35,17 +36,39 @@ struct WsLayout {
 
 WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem);
 
-// The down GEMM (d outputs, contraction d_ff) runs as two K halves when its
-// 256 x 256 tiles fill the chip's rounds of 256 workgroups so unevenly that
-// twice the workgroups, each with half of K plus the partial-sum exchange,
-// finish sooner (a cost model); returns that tile count, or 0 when the down
-// GEMM is not split. Shared by the launcher and the workspace layout so both
-// agree. At most kSplitMaxTiles tiles (512 MB of partial sums).
-constexpr int kSplitMaxTiles = 1024;
+// Work split of one 256 x 256-tile FFN GEMM launch (the ping-pong kernel) over
+// the chip's 8 XCDs of 32 CUs, one workgroup per CU at a time. Work item w
+// (a tile) runs on XCD w / per_x. On each XCD the first whole_x items run as
+// whole tiles, in full rounds of 32; the remaining tail_x items (the last,
+// partial round) run as `pieces` workgroups each, over equal ranges of the
+// K superslabs, whose fp32 partial sums meet through the workspace: the last
+// piece to arrive adds them up in piece order and runs the epilogue.
+// pieces == 1: no split (whole_x = per_x, tail_x = 0).
+constexpr int kXcdCount = 8;
+constexpr int kCusPerXcd = 32;
+constexpr int kSplitMaxSlots = kXcdCount * kCusPerXcd;  // partial-sum tiles: 256 x 256 KB = 64 MB
+struct GemmSplit {
+  int per_x;    // items per XCD (the last XCD may have fewer)
+  int whole_x;  // whole items per XCD
+  int tail_x;   // split items per XCD
+  int pieces;   // workgroups per split item
+};
+// Chosen by a cost model in units of one superslab's K-loop time: a whole
+// tile costs ns + 3.5 (prologue, epilogue); a piece ns / S + 2 (its partial
+// sums written) + the last arriver's reads (2.5 per partial tile read: one for
+// S = 2, whose two addends commute; all S otherwise, summed in piece order).
+// Splits only when that beats running the tail as whole tiles, after at most
+// two full rounds; S * tail_x <= 32 and at least 3 superslabs per piece.
+GemmSplit gemm_split(int64_t items, int ns);
+// Item and superslab counts of the gate/up (mode 0: 128 output features per
+// tile) and down (mode 1: 256) launches over kept_capacity rows, or 0 items
+// when the ping-pong kernel does not apply (fp32, K not in whole 128-byte
+// superslabs, fewer than 3 of them, or 32-bit offsets overflowing).
+void gemm_items(int mode, int cap, int d, int d_ff, int n_sets, int elem, int64_t* items, int* ns);
+
 // The FFN-saliency reduction splits each sequence's rows over at most this
 // many workgroups (partial sums in the workspace, summed in a fixed order).
 constexpr int kSalSplits = 16;
-int down_split_tiles(int cap, int d, int d_ff, int n_sets, int elem);
 
 // Token tile of the single-launch scorer: 32, or (bf16, r_core + r_exp <=
 // 384) 128 when that takes fewer rounds of 256 workgroups x rows of K each

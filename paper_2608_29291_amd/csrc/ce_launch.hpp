@@ -33,23 +33,24 @@ struct FfnGemmArgs {
   int cap;
   const int32_t* n0_ptr;  // rows in the first weight set (MoT), or NULL
   int n_sets;
-  // down GEMM split over two K halves (both NULL: no split): fp32 partial sums
-  // [2 x tiles x 256 x 256] and per-tile arrival counters [tiles]
+  // tail tiles split over K (see GemmSplit): fp32 partial sums [slots x 256 x
+  // 256] and this launch's arrival counters, zero on entry (both NULL: no split)
   float* part;
   int32_t* tile_cnt;
-  // gate/up only: the following down GEMM's arrival counters, cleared by the
-  // first workgroup (NULL: none), so the down launch needs no fill kernel
+  // the following GEMM launch's arrival counters, cleared by the first
+  // workgroup (NULL: none), so that launch needs no fill kernel
   int32_t* clear_cnt;
   int clear_n;
 };
 
-hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream);
-// counters_clear: the arrival counters of a split down GEMM were already
-// cleared on this stream (by the gate/up launch through clear_cnt).
-hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream,
-                           bool counters_clear = false);
-// Number of arrival counters the down GEMM with these arguments uses (0: no split).
-int ffn_down_split_tiles(const FfnGemmArgs& a, bool bf16);
+// counters_clear: this launch's arrival counters (tile_cnt) were already
+// cleared on this stream (by the previous kernel through clear_cnt); else a
+// fill kernel clears them first when the launch splits.
+hipError_t launch_ffn_gateup(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear = false);
+hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear = false);
+// Number of arrival counters a GEMM launch with these arguments uses (0: no
+// split); mode 0 = gate/up, 1 = down.
+int ffn_split_counters(const FfnGemmArgs& a, int mode, bool bf16);
 
 struct ScoreArgs {
   const char* hidden;
@@ -105,6 +106,9 @@ struct SelectArgs {
   int32_t* kept_offsets;
   int32_t* token_pos;  // or NULL
   uint32_t* status;
+  // counters of the following gate/up launch, cleared by workgroup 0 (or NULL)
+  int32_t* clear_cnt;
+  int clear_n;
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 

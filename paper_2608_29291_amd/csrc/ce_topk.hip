@@ -464,6 +464,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   __shared__ SelShared sh;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
+  // the following gate/up launch's arrival counters start at zero
+  if (a.clear_cnt && b == 0)
+    for (int i = tid; i < a.clear_n; i += kSelThreads) a.clear_cnt[i] = 0;
   const int lo = a.info[3 * b + 0];
   const int len = a.info[3 * b + 1];
   const int nkeep = a.info[3 * b + 2] & 0x7fffffff;

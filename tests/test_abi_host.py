@@ -353,26 +353,36 @@ def test_score_tiling_validation():
     assert tiling(2, 100, 256, 64, 32) == (0, 32, 0)
 
 
-@pytest.mark.parametrize("i,split", [(1, False), (2, True), (3, False), (4, True), (5, True)])
-def test_down_split_policy_of_named_workloads(i, split):
-    """The down GEMM runs as two K halves where its 256 x 256 tiles fill the
-    rounds of 256 workgroups unevenly: 108 tiles (understanding) and 294 (7B
-    width, MoT); whole tiles for 204 (generation: one round) and for the tiny
-    fp32 workload. The split shows in the FFN workspace as the partial-sum
-    region, two fp32 256 x 256 tiles per output tile."""
+# Partial-sum tiles the FFN workspace reserves for the split tail tiles of the
+# two GEMM launches (the largest plan over gate/up, down and one or two weight
+# sets), worked by hand from the plan's rule: per XCD (8) the items past full
+# rounds of 32 run as S pieces each, when there are at most two full rounds.
+# Understanding workload: down 108 tiles -> 14 per XCD, S = 2 (224 slots);
+# two sets: 114 -> 15, S = 2 (240); gate/up 1260 / 1330 tiles: 4-5 full rounds,
+# no split. Generation workload: gate/up 2380 tiles (9 rounds), down 204 (26 per
+# XCD: S = 1), no split. 7B width: down 294 -> 37 = 32 + 5, S = 6 (240); MoT
+# (two sets, the same tile counts): 240. fp32: none.
+SPLIT_SLOTS = {1: 0, 2: 240, 3: 0, 4: 240, 5: 240}
+
+
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 5])
+def test_gemm_split_workspace_of_named_workloads(i):
     from ce_workloads import config_params
     p = config_params(i)
     offs, flags = build_layout(config_layout(i))
     keep = {1: 0.5, 2: 0.35, 3: 0.5, 4: 0.4, 5: 0.3}[i]
     cap = ce.ce_kept_count_host(offs, flags, keep)
-    n_sets = 2 if i == 5 else 1
     dt = ce.CE_F32 if i == 1 else ce.CE_BF16
     elem = 4 if i == 1 else 2
-    b = _batch(B=len(offs) - 1, T=len(flags), keep=keep, cap=cap)
-    need = ce.lib.ce_workspace_size(ce.CE_WS_FFN, ctypes.byref(b), p["d"], p["F"], dt)
-    tiles = ((cap + 255) // 256 + n_sets - 1) * ((p["d"] + 255) // 256)
-    act = cap * p["F"] * elem
-    assert (need >= act + tiles * 2 * 256 * 256 * 4) == split
+    B, F = len(offs) - 1, p["F"]
+    b = _batch(B=B, T=len(flags), keep=keep, cap=cap)
+    need = ce.lib.ce_workspace_size(ce.CE_WS_FFN, ctypes.byref(b), p["d"], F, dt)
+    al = lambda x: (max(x, 1) + 255) // 256 * 256
+    slots = SPLIT_SLOTS[i]
+    want = (al(16) + al(cap * 4) + al(4) + al(cap * F * elem)
+            + (al(slots * 256 * 256 * 4) + 2 * al(256 * 4) if slots else 0)
+            + al((16 * B * F + B * ((F + 255) // 256) * 2) * 4))
+    assert need == want
 
 
 def test_binding_rejects_host_tensors_before_any_call():

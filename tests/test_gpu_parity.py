@@ -317,20 +317,65 @@ def test_block(G, kind, dtype, inplace):
     print(f"[block {kind} {dtype} inplace={inplace}] rel err {err:.3e} swaps {swaps}")
 
 
+# (d, d_ff) on the ping-pong GEMMs whose few tiles make both launches split
+# every tile over K (partial sums meeting through the workspace): 512 / 2048
+# splits gate/up tiles in 2 pieces (8 superslabs of K) and down tiles in 4 (32
+# superslabs, summed in piece order); 2048 / 1024 the other way round (gate/up
+# in 4, down in 2)
+SPLIT_SHAPES = [(512, 2048), (2048, 1024)]
+
+
+@pytest.mark.parametrize("d,F", SPLIT_SHAPES)
 @pytest.mark.parametrize("kind", ["und", "mot", "interleaved"])
-def test_block_ping_pong_split_down(G, kind):
-    """Shapes on the ping-pong GEMMs (d and d_ff multiples of 256, 32
-    superslabs of K): gate/up with the SwiGLU epilogue, and the down GEMM in
-    two K halves that meet through the workspace (the cost model splits at
-    this K), ragged last token tile, MoT groups; run twice, bitwise equal (two
-    addends: the sum does not depend on which half arrives last)."""
-    wl = small_workload(kind, seed=21, dtype="bf16", d=512, F=2048)
-    print(f"[block ping-pong {kind}] T={wl.T}", flush=True)
+def test_block_ping_pong_split(G, kind, d, F):
+    """Fused block on the ping-pong GEMMs with split tail tiles: gate/up with
+    the SwiGLU epilogue after the pieces meet, down with the residual scatter,
+    ragged last token tile, MoT groups; run twice, bitwise equal (two pieces
+    commute, more are added in piece order, so the sum does not depend on
+    which piece arrives last)."""
+    wl = small_workload(kind, seed=21, dtype="bf16", d=d, F=F)
+    print(f"[block ping-pong {kind} d={d} F={F}] T={wl.T}", flush=True)
     r = run_block(G, wl)
     err, swaps = check_block(G, wl, r)
     r2 = run_block(G, wl)
     np.testing.assert_array_equal(r["y"], r2["y"])
     print(f"[block ping-pong {kind}] rel err {err:.3e} swaps {swaps}", flush=True)
+
+
+@pytest.mark.parametrize("d,F", SPLIT_SHAPES)
+@pytest.mark.parametrize("kind", ["und", "mot"])
+def test_staged_ffn_split(G, kind, d, F):
+    """The staged FFN entry points with split tail tiles: ce_routed_ffn equals
+    ce_ffn_gateup + ce_ffn_down bit for bit (each clears its own counters),
+    both equal the oracle's FFN, and a second ce_routed_ffn call on the same
+    workspace repeats the first bit for bit."""
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = small_workload(kind, seed=22, dtype="bf16", d=d, F=F)
+    _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    dw, kidx, koff, _, comp, st = run_topk(G, wl, l32, compact=True)
+    assert st == 0
+    kt = int(koff[-1])
+    ki, ko = G.to_dev(kidx.astype(np.int32)), G.to_dev(koff.astype(np.int32))
+    ws = dw.ws(ce.CE_WS_FFN)
+    outs = []
+    for _ in range(2):
+        o = torch.full_like(comp, float("nan"))
+        ce.ce_routed_ffn(dw.batch, comp, ki, ko, dw.ffn, o, ws)
+        outs.append(o)
+    act = torch.full((max(dw.cap, 1), F), float("nan"), dtype=torch.bfloat16, device="cuda")
+    o2 = torch.full_like(comp, float("nan"))
+    ce.ce_ffn_gateup(dw.batch, comp, ki, ko, dw.ffn, act, ws)
+    ce.ce_ffn_down(dw.batch, act, ki, ko, dw.ffn, o2, ws)
+    torch.cuda.synchronize()
+    f = G.host(outs[0])[:kt]
+    np.testing.assert_array_equal(G.host(outs[1])[:kt], f)
+    np.testing.assert_array_equal(G.host(o2)[:kt], f)
+    rows = kidx[:kt]
+    f_ref = oracle.routed_rows(wl.hidden, wl.flags, rows, wl.ffn) - wl.hidden[rows].astype(np.float64)
+    err = G.rel_err(f, f_ref)
+    print(f"[staged split {kind} d={d} F={F}] rel err {err:.3e}", flush=True)
+    assert err <= G.FFN_TOL["bf16"]
 
 
 def test_block_keep_one_is_dense(G):
