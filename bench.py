@@ -354,7 +354,39 @@ def main():
                   "min": round(min(step_us), 2), "max": round(max(step_us), 2)}
     log(f"routed block: {ms * 1e3:.1f} us/step (median {step_stats['median']}, middle 7/8 "
         f"{step_stats['mean_middle_7_8']})")
-    del pool
+
+    # The block with the layer-skipping gap (Eq. 7) from the down GEMM's
+    # epilogue (ce_routed_block_gap) against the plain block: pairs of blocks,
+    # plain then with the gap, each on its own pristine copy, an event pair
+    # around each, so that both see the same engine clock.
+    ws_gap = ce.alloc_workspace(ce.CE_WS_BLOCK_GAP, batch, d, F, dtc, device=dev)
+    cos_g = torch.empty(T, device=dev)
+    ra_g, rr_g, gp_g = (torch.empty(wl.B, device=dev) for _ in range(3))
+    sk_g = torch.empty(wl.B, dtype=torch.uint8, device=dev)
+    pool_b = [torch.empty_like(base_h) for _ in range(n_pool)]
+
+    def step_gap(i):
+        sc, ff = wsets[i % n_sets]
+        j = i % n_pool
+        ce.ce_routed_block_gap(src[j % len(src)][1], pool_b[j], pool_b[j], sc, ff, ws_gap, 0.0040, cos_g, ra_g,
+                               rr_g, gp_g, sk_g, stream=stream)
+
+    restore()
+    for j, x in enumerate(pool_b):
+        x.copy_(src[j % len(src)][0])
+    torch.cuda.synchronize()
+    pairs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        pairs[i][0].record(stream)
+        step(i)
+        pairs[i][1].record(stream)
+        step_gap(i)
+        pairs[i][2].record(stream)
+    torch.cuda.synchronize()
+    plain_us = float(np.mean([e[0].elapsed_time(e[1]) for e in pairs])) * 1e3
+    gap_block_us = float(np.mean([e[1].elapsed_time(e[2]) for e in pairs])) * 1e3
+    log(f"pairs: routed block {plain_us:.1f} us, with the fused layer gap {gap_block_us:.1f} us")
+    del pool, pool_b, ws_gap
 
     # ---- per-stage launches (staged entry points on the same data) ----
     logits = torch.empty(T, device=dev)
@@ -500,6 +532,11 @@ def main():
     result["ucs_signals"] = time_drop_stability(ce, stream, max(args.steps, 10))
     result["ucs_signals"]["ffn_saliency_leakage"] = ucs_ffn
     result["ucs_signals"]["layer_gap"] = ucs_gap
+    result["ucs_signals"]["layer_gap_fused_in_block"] = {
+        "block_with_gap_us": round(gap_block_us, 2), "block_us": round(plain_us, 2),
+        "extra_us": round(gap_block_us - plain_us, 2), "pairs": args.steps,
+        "note": "ce_routed_block_gap vs ce_routed_block in alternating pairs; the gap sums come from the "
+                "down GEMM's epilogue (no [T x d] re-read)"}
     result["routed_attention"] = time_attention(ce, stream, max(args.steps, 10))
     result["achievable_peaks"] = (achievable_peaks(cap, d, F) if bf16 else None)
     if not args.no_cpu_baseline:

@@ -80,7 +80,7 @@ enum {
 };
 
 /* ---- workspace kinds ---------------------------------------------------- */
-enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2 };
+enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2, CE_WS_BLOCK_GAP = 3 };
 
 /*
  * A ragged batch of B sequences packed back to back: sequence b owns tokens
@@ -298,6 +298,29 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                     const ce_scorer_w* scorer, const ce_ffn_w* ffn, float* logits_out,
                     int32_t* kept_idx_out, int32_t* kept_offsets_out, void* ws,
                     size_t ws_bytes, void* stream);
+
+/*
+ * ce_routed_block plus the layer-skipping redundancy gap of the block
+ * (section 3.4, UCS operator (1), Eq. 7), with x_in = hidden_in and x_out =
+ * hidden_out as ce_layer_gap defines it, without reading either [T x d]
+ * matrix again: the down GEMM's epilogue, which holds each retained row's
+ * residual and output, adds up the fp64 sums of in*out, in*in and out*out per
+ * row, and a dropped token, which bypasses the block unchanged, has cos = 1.
+ * Same arguments and results as ce_routed_block (the outputs are bit for bit
+ * those of ce_routed_block), plus
+ *   delta     skip threshold delta_LS (the paper's is 0.0040), finite
+ *   cos       device float32 [T] out: per-token cosine (NaN past an overflowing
+ *             capacity, see CE_DEV_OVERFLOW)
+ *   rho_all, rho_ret, gap  device float32 [B] out; skip device uint8 [B] out or NULL
+ *   ws        device workspace of ce_workspace_size(CE_WS_BLOCK_GAP, ...) bytes
+ * The sums add the per-row partials in a fixed order (deterministic); they
+ * differ from ce_layer_gap's only in the order of the fp64 additions.
+ */
+int ce_routed_block_gap(const ce_batch* batch, const void* hidden_in, void* hidden_out,
+                        const ce_scorer_w* scorer, const ce_ffn_w* ffn, float* logits_out,
+                        int32_t* kept_idx_out, int32_t* kept_offsets_out, float delta, float* cos,
+                        float* rho_all, float* rho_ret, float* gap, uint8_t* skip, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /*
  * Host query: how the routing logits (section 3.2, Eq. 4) are computed for

@@ -31,14 +31,14 @@ CE_OK, CE_ERR_INVALID_ARG, CE_ERR_UNSUPPORTED, CE_ERR_WORKSPACE, CE_ERR_HIP = 0,
 CE_F32, CE_BF16 = 0, 1
 CE_TOK_GEN, CE_TOK_KEEP = 1, 2
 CE_DEV_BAD_OFFSETS, CE_DEV_OVERFLOW = 1, 2
-CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK = 0, 1, 2
+CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK, CE_WS_BLOCK_GAP = 0, 1, 2, 3
 
 EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
     "ce_workspace_status", "ce_score", "ce_topk_compact", "ce_routed_ffn", "ce_ffn_gateup",
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
-    "ce_routed_attention", "ce_score_tiling", "ce_topk_compact_noalloc",
+    "ce_routed_attention", "ce_score_tiling", "ce_topk_compact_noalloc", "ce_routed_block_gap",
 ]
 
 
@@ -114,6 +114,9 @@ _sig("ce_scatter_residual", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, 
                                            _p, _p])
 _sig("ce_routed_block", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.POINTER(CEScorerW),
                                        ctypes.POINTER(CEFFNW), _p, _p, _p, _p, ctypes.c_size_t, _p])
+_sig("ce_routed_block_gap", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.POINTER(CEScorerW),
+                                           ctypes.POINTER(CEFFNW), _p, _p, _p, ctypes.c_float, _p, _p, _p, _p, _p,
+                                           _p, ctypes.c_size_t, _p])
 _sig("ce_drop_stability", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, _p, _p, _p])
 _sig("ce_ffn_down_colnorms", ctypes.c_int, [ctypes.POINTER(CEFFNW), _p, _p])
 _sig("ce_ffn_saliency", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
@@ -511,6 +514,32 @@ def ce_routed_block(batch: Batch, hidden_in, hidden_out, scorer: Scorer, ffn: FF
                                wp, wn, _stream(stream)), "ce_routed_block")
 
 
+def ce_routed_block_gap(batch: Batch, hidden_in, hidden_out, scorer: Scorer, ffn: FFN, ws, delta, cos, rho_all,
+                        rho_ret, gap, skip=None, logits_out=None, kept_idx_out=None, kept_offsets_out=None,
+                        stream=None):
+    """ce_routed_block plus the block's layer-skipping gap (Eq. 7) from its
+    down GEMM's epilogue; ws: ce_workspace_size(CE_WS_BLOCK_GAP, ...) bytes."""
+    import torch
+    cb, sw, fw = batch.c(), scorer.c(), ffn.c()
+    T, B, cap = batch.T, batch.B, int(batch.kept_capacity)
+    if sw.d != fw.d or sw.dtype != fw.dtype:
+        raise ValueError("scorer and FFN must agree on d and dtype")
+    tdt = ffn.w_gate[0].dtype
+    f32 = torch.float32
+    wp, wn = _ws_ptr(ws, ce_workspace_size(CE_WS_BLOCK_GAP, batch, fw.d, fw.d_ff, fw.dtype))
+    _check(lib.ce_routed_block_gap(ctypes.byref(cb), _hidden(hidden_in, "hidden_in", T, fw.d, tdt),
+                                   _hidden(hidden_out, "hidden_out", T, fw.d, tdt),
+                                   ctypes.byref(sw), ctypes.byref(fw),
+                                   _chk(logits_out, "logits_out", f32, numel=T, optional=True),
+                                   _chk(kept_idx_out, "kept_idx_out", torch.int32, numel=cap, optional=True),
+                                   _chk(kept_offsets_out, "kept_offsets_out", torch.int32, numel=B + 1,
+                                        optional=True),
+                                   float(delta), _chk(cos, "cos", f32, numel=T), _chk(rho_all, "rho_all", f32, numel=B),
+                                   _chk(rho_ret, "rho_ret", f32, numel=B), _chk(gap, "gap", f32, numel=B),
+                                   _chk(skip, "skip", torch.uint8, numel=B, optional=True), wp, wn, _stream(stream)),
+           "ce_routed_block_gap")
+
+
 def ce_score_tiling(batch: Batch, scorer: Scorer):
     """(tm, tn) of the rank-tiled scorer ce_routed_block uses for this batch,
     or (token_tile, 0) for the single-launch scorer (host query, no GPU work)."""
@@ -615,9 +644,9 @@ __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
     "ce_score", "ce_topk_compact", "ce_topk_compact_noalloc", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
-    "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
+    "ce_scatter_residual", "ce_routed_block", "ce_routed_block_gap", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "ce_routed_attention", "CEAttn",
-    "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK",
+    "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK", "CE_WS_BLOCK_GAP",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -193,6 +193,123 @@ int topk_launch(const ce_batch* batch, const float* logits, const void* hidden, 
   return CE_OK;
 }
 
+// Outputs of the layer-skipping gap computed with the routed block.
+struct GapOut {
+  float delta;
+  float* cos;
+  float* rho_all;
+  float* rho_ret;
+  float* gap;
+  uint8_t* skip;
+};
+
+// The routed block; with `go` also the layer-skipping gap from the down
+// GEMM's per-row sums (the caller's workspace has the CE_WS_BLOCK_GAP layout).
+int routed_block_impl(const ce_batch* batch, const void* hidden_in, void* hidden_out, const ce_scorer_w* scorer,
+                      const ce_ffn_w* ffn, float* logits_out, int32_t* kept_idx_out, int32_t* kept_offsets_out,
+                      const GapOut* go, void* ws, size_t ws_bytes, void* stream) {
+  CE_CHECK(check_batch(batch, scorer != nullptr && scorer->r_exp > 0));
+  CE_CHECK(check_scorer(scorer));
+  CE_CHECK(check_ffn(ffn));
+  if (scorer->d != ffn->d || scorer->dtype != ffn->dtype) return CE_ERR_INVALID_ARG;
+  if (batch->T > 0 && (!hidden_in || !hidden_out)) return CE_ERR_INVALID_ARG;
+  const int elem = elem_size(ffn->dtype);
+  const WsLayout L = ws_layout(go ? CE_WS_BLOCK_GAP : CE_WS_BLOCK, batch->B, batch->T, batch->kept_capacity, ffn->d,
+                               ffn->d_ff, elem);
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf16 = ffn->dtype == CE_BF16;
+  float* logits = logits_out ? logits_out : at<float>(ws, L.logits);
+  int32_t* kept_idx = kept_idx_out ? kept_idx_out : at<int32_t>(ws, L.kept_idx);
+  int32_t* kept_off = kept_offsets_out ? kept_offsets_out : at<int32_t>(ws, L.kept_off);
+  int32_t* token_pos = at<int32_t>(ws, L.token_pos);
+  int32_t* info = at<int32_t>(ws, L.seq_info);
+
+  // 1. routing logits (Eq. 4); the same launch writes the per-sequence
+  //    summaries. bf16: rank-tiled partial logits when that moves fewer
+  //    bytes per workgroup; the TopK step adds them up.
+  ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
+  sa.info = info;
+  int tm = 0, tn = 0;
+  const bool tiled = bf16 && score_tiling(batch->B, batch->T, scorer->d, scorer->r_core, scorer->r_exp, elem,
+                                          &tm, &tn, &sa.n_ct, &sa.n_rt);
+  if (tiled) {
+    sa.part = at<float>(ws, L.score_part);
+    CE_TRY(launch_score_tiles(sa, tm, tn, s));
+  } else {
+    CE_TRY(launch_score(sa, bf16, s));
+  }
+  // FFN launch arguments (host-known; the row counts stay on the device)
+  const int32_t* kt = kept_off + batch->B;
+  int32_t* grp = ffn->n_sets == 2 ? at<int32_t>(ws, L.grp_rows) : nullptr;
+  int32_t* n0 = ffn->n_sets == 2 ? at<int32_t>(ws, L.grp_n0) : nullptr;
+  char* act = at<char>(ws, L.act);
+  FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
+                             kept_idx, static_cast<const char*>(hidden_in), kt, n0);
+  set_split(dn, ws, L, 1);
+  double* gap_part = go ? at<double>(ws, L.gap_part) : nullptr;
+  if (go) {
+    dn.gap_part = gap_part;
+    dn.gap_np = ffn_down_gap_slots(dn, bf16);
+  }
+  FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx, act,
+                              nullptr, kt, n0);
+  set_split(g, ws, L, 0);
+  g.clear_n = ffn_split_counters(dn, 1, bf16);
+  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
+  const int gu_counters = ffn_split_counters(g, 0, bf16);
+
+  // 2-3. per-sequence TopK + packed index maps (Eq. 6); the select launch
+  //      also clears the gate/up launch's arrival counters
+  SelectArgs sel{};
+  sel.logits = logits;
+  if (tiled) {
+    sel.part = sa.part;
+    sel.logits_w = logits;
+    sel.n_ct = sa.n_ct;
+    sel.n_rt = sa.n_rt;
+    sel.T = batch->T;
+    sel.r_exp = scorer->r_exp;
+    sel.n_seg = scorer->n_seg;
+    sel.b2c = scorer->b2_core;
+    sel.b2e = scorer->b2_exp;
+    sel.t = batch->t;
+  }
+  sel.flags = batch->flags;
+  sel.info = info;
+  sel.B = batch->B;
+  sel.keep = batch->keep;
+  sel.cap = batch->kept_capacity;
+  sel.kept_idx = kept_idx;
+  sel.kept_offsets = kept_off;
+  sel.token_pos = token_pos;
+  sel.status = at<uint32_t>(ws, L.status);
+  sel.clear_cnt = gu_counters > 0 ? g.tile_cnt : nullptr;
+  sel.clear_n = gu_counters;
+  CE_TRY(launch_select(sel, s));
+  // bypass path for a separate output buffer: dropped rows copied unchanged
+  if (hidden_in != hidden_out)
+    CE_TRY(launch_copy_rows(static_cast<const char*>(hidden_in), static_cast<char*>(hidden_out),
+                            (int64_t)ffn->d * elem, batch->T, token_pos, s));
+  // layer gap (Eq. 7) from the down GEMM's per-row sums, after the block
+  auto finish_gap = [&]() -> int {
+    if (!go) return CE_OK;
+    CE_TRY(launch_gap_from_parts(gap_part, dn.gap_np, batch->kept_capacity, batch->seq_offsets, batch->B,
+                                 batch->T, token_pos, go->delta, go->cos, go->rho_all, go->rho_ret, go->gap,
+                                 go->skip, s));
+    return CE_OK;
+  };
+  if (batch->kept_capacity == 0) return finish_gap();
+  // 4. SwiGLU FFN on the retained rows, gathered straight from hidden_in
+  if (ffn->n_sets == 2)
+    CE_TRY(launch_group(kept_idx, kept_off, batch->B, batch->kept_capacity, batch->T, batch->flags,
+                        grp, n0, s));
+  CE_TRY(launch_ffn_gateup(g, bf16, s, gu_counters > 0));
+  // 5. down projection + residual, scattered straight into the token rows
+  CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
+  return finish_gap();
+}
+
 }  // namespace
 
 extern "C" {
@@ -309,92 +426,21 @@ int ce_routed_block(const ce_batch* batch, const void* hidden_in, void* hidden_o
                     const ce_scorer_w* scorer, const ce_ffn_w* ffn, float* logits_out,
                     int32_t* kept_idx_out, int32_t* kept_offsets_out, void* ws, size_t ws_bytes,
                     void* stream) {
-  CE_CHECK(check_batch(batch, scorer != nullptr && scorer->r_exp > 0));
-  CE_CHECK(check_scorer(scorer));
-  CE_CHECK(check_ffn(ffn));
-  if (scorer->d != ffn->d || scorer->dtype != ffn->dtype) return CE_ERR_INVALID_ARG;
-  if (batch->T > 0 && (!hidden_in || !hidden_out)) return CE_ERR_INVALID_ARG;
-  const int elem = elem_size(ffn->dtype);
-  const WsLayout L = ws_layout(CE_WS_BLOCK, batch->B, batch->T, batch->kept_capacity, ffn->d, ffn->d_ff, elem);
-  CE_CHECK(check_ws(ws, ws_bytes, L.total));
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const bool bf16 = ffn->dtype == CE_BF16;
-  float* logits = logits_out ? logits_out : at<float>(ws, L.logits);
-  int32_t* kept_idx = kept_idx_out ? kept_idx_out : at<int32_t>(ws, L.kept_idx);
-  int32_t* kept_off = kept_offsets_out ? kept_offsets_out : at<int32_t>(ws, L.kept_off);
-  int32_t* token_pos = at<int32_t>(ws, L.token_pos);
-  int32_t* info = at<int32_t>(ws, L.seq_info);
+  return routed_block_impl(batch, hidden_in, hidden_out, scorer, ffn, logits_out, kept_idx_out, kept_offsets_out,
+                           nullptr, ws, ws_bytes, stream);
+}
 
-  // 1. routing logits (Eq. 4); the same launch writes the per-sequence
-  //    summaries. bf16: rank-tiled partial logits when that moves fewer
-  //    bytes per workgroup; the TopK step adds them up.
-  ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
-  sa.info = info;
-  int tm = 0, tn = 0;
-  const bool tiled = bf16 && score_tiling(batch->B, batch->T, scorer->d, scorer->r_core, scorer->r_exp, elem,
-                                          &tm, &tn, &sa.n_ct, &sa.n_rt);
-  if (tiled) {
-    sa.part = at<float>(ws, L.score_part);
-    CE_TRY(launch_score_tiles(sa, tm, tn, s));
-  } else {
-    CE_TRY(launch_score(sa, bf16, s));
-  }
-  // FFN launch arguments (host-known; the row counts stay on the device)
-  const int32_t* kt = kept_off + batch->B;
-  int32_t* grp = ffn->n_sets == 2 ? at<int32_t>(ws, L.grp_rows) : nullptr;
-  int32_t* n0 = ffn->n_sets == 2 ? at<int32_t>(ws, L.grp_n0) : nullptr;
-  char* act = at<char>(ws, L.act);
-  FfnGemmArgs dn = down_args(ffn, batch, act, nullptr, static_cast<char*>(hidden_out), grp,
-                             kept_idx, static_cast<const char*>(hidden_in), kt, n0);
-  set_split(dn, ws, L, 1);
-  FfnGemmArgs g = gateup_args(ffn, batch, static_cast<const char*>(hidden_in), grp, kept_idx, act,
-                              nullptr, kt, n0);
-  set_split(g, ws, L, 0);
-  g.clear_n = ffn_split_counters(dn, 1, bf16);
-  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
-  const int gu_counters = ffn_split_counters(g, 0, bf16);
-
-  // 2-3. per-sequence TopK + packed index maps (Eq. 6); the select launch
-  //      also clears the gate/up launch's arrival counters
-  SelectArgs sel{};
-  sel.logits = logits;
-  if (tiled) {
-    sel.part = sa.part;
-    sel.logits_w = logits;
-    sel.n_ct = sa.n_ct;
-    sel.n_rt = sa.n_rt;
-    sel.T = batch->T;
-    sel.r_exp = scorer->r_exp;
-    sel.n_seg = scorer->n_seg;
-    sel.b2c = scorer->b2_core;
-    sel.b2e = scorer->b2_exp;
-    sel.t = batch->t;
-  }
-  sel.flags = batch->flags;
-  sel.info = info;
-  sel.B = batch->B;
-  sel.keep = batch->keep;
-  sel.cap = batch->kept_capacity;
-  sel.kept_idx = kept_idx;
-  sel.kept_offsets = kept_off;
-  sel.token_pos = token_pos;
-  sel.status = at<uint32_t>(ws, L.status);
-  sel.clear_cnt = gu_counters > 0 ? g.tile_cnt : nullptr;
-  sel.clear_n = gu_counters;
-  CE_TRY(launch_select(sel, s));
-  // bypass path for a separate output buffer: dropped rows copied unchanged
-  if (hidden_in != hidden_out)
-    CE_TRY(launch_copy_rows(static_cast<const char*>(hidden_in), static_cast<char*>(hidden_out),
-                            (int64_t)ffn->d * elem, batch->T, token_pos, s));
-  if (batch->kept_capacity == 0) return CE_OK;
-  // 4. SwiGLU FFN on the retained rows, gathered straight from hidden_in
-  if (ffn->n_sets == 2)
-    CE_TRY(launch_group(kept_idx, kept_off, batch->B, batch->kept_capacity, batch->T, batch->flags,
-                        grp, n0, s));
-  CE_TRY(launch_ffn_gateup(g, bf16, s, gu_counters > 0));
-  // 5. down projection + residual, scattered straight into the token rows
-  CE_TRY(launch_ffn_down(dn, bf16, s, g.clear_cnt != nullptr));
-  return CE_OK;
+int ce_routed_block_gap(const ce_batch* batch, const void* hidden_in, void* hidden_out,
+                        const ce_scorer_w* scorer, const ce_ffn_w* ffn, float* logits_out,
+                        int32_t* kept_idx_out, int32_t* kept_offsets_out, float delta, float* cos,
+                        float* rho_all, float* rho_ret, float* gap, uint8_t* skip, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (!rho_all || !rho_ret || !gap) return CE_ERR_INVALID_ARG;
+  if (!isfinite(delta)) return CE_ERR_INVALID_ARG;
+  if (batch && batch->T > 0 && !cos) return CE_ERR_INVALID_ARG;
+  const GapOut go{delta, cos, rho_all, rho_ret, gap, skip};
+  return routed_block_impl(batch, hidden_in, hidden_out, scorer, ffn, logits_out, kept_idx_out, kept_offsets_out,
+                           &go, ws, ws_bytes, stream);
 }
 
 int ce_score_tiling(const ce_batch* batch, const ce_scorer_w* scorer, int32_t* tile_out) {

@@ -266,6 +266,7 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
       }
     } else {
       const char* rrow = a.res ? a.res + (int64_t)orow_idx * a.res_ld : nullptr;
+      double gdot = 0.0, gin = 0.0, gout = 0.0;  // layer-gap sums over this lane's features
 #pragma unroll
       for (int i = 0; i < kMW; ++i) {
         const int fb = f0 + ww * kWRw + 32 * i + 4 * lhalf;
@@ -275,11 +276,37 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
           const int f = fb + 8 * g;
           float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
           float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+          f32x4_t r = {0.0f, 0.0f, 0.0f, 0.0f};
           if (rrow) {
-            f32x4_t r = load4<kBF16>(rrow + (int64_t)f * kElem);
+            r = load4<kBF16>(rrow + (int64_t)f * kElem);
             v0 += r.x; v1 += r.y; v2 += r.z; v3 += r.w;
           }
           store4<kBF16>(orow + (int64_t)f * kElem, v0, v1, v2, v3);
+          if (a.gap_part) {
+            // the values as stored (bf16: after the one rounding)
+            const f32x4_t y = load4<kBF16>(orow + (int64_t)f * kElem);
+            const float ri[4] = {r.x, r.y, r.z, r.w}, yo[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              gdot = fma((double)ri[e], (double)yo[e], gdot);
+              gin = fma((double)ri[e], (double)ri[e], gin);
+              gout = fma((double)yo[e], (double)yo[e], gout);
+            }
+          }
+        }
+      }
+      if (a.gap_part) {
+        // lanes l and l ^ 32 hold the same token's other features
+        gdot += __shfl_xor(gdot, 32);
+        gin += __shfl_xor(gin, 32);
+        gout += __shfl_xor(gout, 32);
+        // a wave whose features all lie past the last one has no slot
+        if (lhalf == 0 && f0 + ww * kWRw < n_feat) {
+          const int prow = a.omap1 ? a.omap1[jr] : jr;
+          double* gp = a.gap_part + ((int64_t)prow * a.gap_np + (f0 + ww * kWRw) / kWRw) * 4;
+          gp[0] = gdot;
+          gp[1] = gin;
+          gp[2] = gout;
         }
       }
     }
@@ -762,6 +789,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         }
       }
       merge_block(j);
+      double gdot = 0.0, gin = 0.0, gout = 0.0;  // layer-gap sums over this lane's features
 #pragma unroll
       for (int i = 0; i < kMW; ++i) {
         const int fb0_ = f0 + ww * 128 + 32 * i + 4 * lhalf;
@@ -770,13 +798,44 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         for (int g = 0; g < 4; ++g) {
           float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
           float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
+          float r[4] = {0.0f, 0.0f, 0.0f, 0.0f};
           if (rrow[j]) {
-            v0 += bf16_to_f32(rv[i][g].x & 0xffffu);
-            v1 += bf16_to_f32(rv[i][g].x >> 16);
-            v2 += bf16_to_f32(rv[i][g].y & 0xffffu);
-            v3 += bf16_to_f32(rv[i][g].y >> 16);
+            r[0] = bf16_to_f32(rv[i][g].x & 0xffffu);
+            r[1] = bf16_to_f32(rv[i][g].x >> 16);
+            r[2] = bf16_to_f32(rv[i][g].y & 0xffffu);
+            r[3] = bf16_to_f32(rv[i][g].y >> 16);
+            v0 += r[0]; v1 += r[1]; v2 += r[2]; v3 += r[3];
           }
-          store4<true>(orow[j] + (int64_t)(fb0_ + 8 * g) * 2, v0, v1, v2, v3);
+          u32x2_t pk;
+          pk.x = pack_bf16(v0, v1);
+          pk.y = pack_bf16(v2, v3);
+          *reinterpret_cast<u32x2_t*>(orow[j] + (int64_t)(fb0_ + 8 * g) * 2) = pk;
+          if (a.gap_part) {
+            // the values as stored, after the one rounding
+            const float y[4] = {bf16_to_f32(pk.x & 0xffffu), bf16_to_f32(pk.x >> 16), bf16_to_f32(pk.y & 0xffffu),
+                                bf16_to_f32(pk.y >> 16)};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              gdot = fma((double)r[e], (double)y[e], gdot);
+              gin = fma((double)r[e], (double)r[e], gin);
+              gout = fma((double)y[e], (double)y[e], gout);
+            }
+          }
+        }
+      }
+      if (a.gap_part) {
+        // lanes l and l ^ 32 hold the same token's other features
+        gdot += __shfl_xor(gdot, 32);
+        gin += __shfl_xor(gin, 32);
+        gout += __shfl_xor(gout, 32);
+        // a wave whose features all lie past the last one has no slot
+        if (lhalf == 0 && f0 + ww * 128 < n_feat) {
+          const int jr = row_lo + wt * 64 + 32 * j + lrow;
+          const int prow = a.omap1 ? a.omap1[jr] : jr;
+          double* gp = a.gap_part + ((int64_t)prow * a.gap_np + (f0 + ww * 128) / 128) * 4;
+          gp[0] = gdot;
+          gp[1] = gin;
+          gp[2] = gout;
         }
       }
     }
@@ -900,6 +959,19 @@ int ffn_split_counters(const FfnGemmArgs& a, int mode, bool bf16) {
   const GemmSplit sp = mode == 0 ? pp2_plan<0>(a, &n_tt, &n_ft) : pp2_plan<1>(a, &n_tt, &n_ft);
   if (mode == 1 && !down_on_pp2(a, sp, n_tt, n_ft)) return 0;
   return sp.pieces > 1 ? kXcds * sp.tail_x : 0;
+}
+
+int ffn_down_gap_slots(const FfnGemmArgs& a, bool bf16) {
+  int fpw;  // output features per wave of the kernel launch_ffn_down picks
+  if (bf16) {
+    int n_tt, n_ft;
+    const GemmSplit sp = pp2_plan<1>(a, &n_tt, &n_ft);
+    if (down_on_pp2(a, sp, n_tt, n_ft)) fpw = 128;
+    else fpw = 64;  // 256 x 128 tiles on 4 x 2 waves, 128 x 128 on 2 x 2
+  } else {
+    fpw = grid_tiles(a, 128, 128) < 128 ? 32 : 64;
+  }
+  return (a.n_feat + fpw - 1) / fpw;
 }
 
 hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, bool counters_clear) {

@@ -127,16 +127,17 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
   const size_t sT = (size_t)(T < 0 ? 0 : T);
   const size_t sC = (size_t)(cap < 0 ? 0 : cap);
   const size_t sF = (size_t)(d_ff < 0 ? 0 : d_ff);
+  const bool block = which == CE_WS_BLOCK || which == CE_WS_BLOCK_GAP;
   L.status = take(16);
-  if (which == CE_WS_TOPK || which == CE_WS_BLOCK) L.seq_info = take(3 * sB * 4);
-  if (which == CE_WS_BLOCK) {
+  if (which == CE_WS_TOPK || block) L.seq_info = take(3 * sB * 4);
+  if (block) {
     L.kept_off = take((sB + 1) * 4);
     L.kept_idx = take(sC * 4);
     L.token_pos = take(sT * 4);
     L.logits = take(sT * 4);
     L.score_part = take((size_t)kScoreMaxTiles * sT * 4);
   }
-  if (which == CE_WS_FFN || which == CE_WS_BLOCK) {
+  if (which == CE_WS_FFN || block) {
     L.grp_rows = take(sC * 4);
     L.grp_n0 = take(4);
     L.act = take(sC * sF * (size_t)elem);
@@ -158,6 +159,11 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
       L.dn_cnt = take((size_t)kSplitMaxSlots * 4);
     }
     L.sal_part = take(((size_t)kSalSplits * sB * sF + sB * ((sF + 255) / 256) * 2) * 4);
+  }
+  if (which == CE_WS_BLOCK_GAP) {
+    // one slot per wave of the down GEMM and row; waves cover >= 32 features
+    const size_t sD = (size_t)(d < 0 ? 0 : d);
+    L.gap_part = take(sC * ((sD + 31) / 32) * 4 * sizeof(double));
   }
   L.total = off;
   return L;
@@ -269,7 +275,8 @@ int64_t ce_kept_count_host(int32_t B, int32_t T, const int32_t* offs, const uint
 }
 
 size_t ce_workspace_size(int which, const ce_batch* batch, int32_t d, int32_t d_ff, int dtype) {
-  if (!batch || (which != CE_WS_TOPK && which != CE_WS_FFN && which != CE_WS_BLOCK)) return 0;
+  if (!batch || (which != CE_WS_TOPK && which != CE_WS_FFN && which != CE_WS_BLOCK && which != CE_WS_BLOCK_GAP))
+    return 0;
   const int elem = ce::elem_size(dtype);
   if (!elem) return 0;
   return ce::ws_layout(which, batch->B, batch->T, batch->kept_capacity, d, d_ff, elem).total;

@@ -29,6 +29,7 @@ struct WsLayout {
   size_t gemm_part;  // float [slots x 256 x 256] K-piece partial sums of the FFN GEMMs' tail tiles
   size_t gu_cnt;     // int32 [kSplitMaxSlots] arrival counters of the gate/up tail tiles
   size_t dn_cnt;     // int32 [kSplitMaxSlots] arrival counters of the down tail tiles
+  size_t gap_part;   // double [cap x ceil(d / 32) x 4] layer-gap partial sums (CE_WS_BLOCK_GAP)
   size_t sal_part;   // float [kSalSplits x B x d_ff] FFN-saliency partial sums, then
                      // float [B x ceil(d_ff / 256) x 2] per-chunk totals
   size_t total;

@@ -41,6 +41,13 @@ struct FfnGemmArgs {
   // workgroup (NULL: none), so that launch needs no fill kernel
   int32_t* clear_cnt;
   int clear_n;
+  // down only: per-row partial sums of the layer-skipping gap (NULL: none).
+  // For packed row p the epilogue of each wave writes, at slot q = (first
+  // feature of the wave) / (features per wave), the fp64 sums over its
+  // features of in*out, in*in and out*out (in = residual, out = the stored
+  // output): gap_part[(p * gap_np + q) * 4 + {0, 1, 2}]
+  double* gap_part;
+  int gap_np;
 };
 
 // counters_clear: this launch's arrival counters (tile_cnt) were already
@@ -51,6 +58,9 @@ hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, 
 // Number of arrival counters a GEMM launch with these arguments uses (0: no
 // split); mode 0 = gate/up, 1 = down.
 int ffn_split_counters(const FfnGemmArgs& a, int mode, bool bf16);
+// Gap partial-sum slots per row (gap_np) of the down kernel that
+// launch_ffn_down picks for these arguments: ceil(d / features per wave).
+int ffn_down_gap_slots(const FfnGemmArgs& a, bool bf16);
 
 struct ScoreArgs {
   const char* hidden;
@@ -147,6 +157,14 @@ hipError_t launch_saliency(const char* act, const int32_t* kept_idx, const int32
                            float* saliency, float* lambda, uint8_t* use_pruned, hipStream_t stream);
 hipError_t launch_mask_channels(char* act, const int32_t* kept_offsets, int B, int cap, int d_ff, bool bf16,
                                 const uint8_t* mask, const uint8_t* use_pruned, hipStream_t stream);
+
+// Layer gap of a routed block from the down GEMM's per-row partial sums:
+// cos = 1 for dropped tokens (they bypass the layer), else from the slots of
+// the token's packed row; then the per-sequence means, gap and skip.
+// Packed rows at or past cap (an overflowing batch) get cos = NaN.
+hipError_t launch_gap_from_parts(const double* gap_part, int gap_np, int cap, const int32_t* seq_offsets, int B,
+                                 int T, const int32_t* token_pos, float delta, float* cos_tok, float* rho_all,
+                                 float* rho_ret, float* gap, uint8_t* skip, hipStream_t stream);
 
 hipError_t launch_layer_gap(const char* x_in, const char* x_out, const int32_t* seq_offsets, int B, int T, int d,
                             bool bf16, const int32_t* token_pos, float delta, float* cos_tok, float* rho_all,

@@ -8,7 +8,10 @@
 //   gap[b]      = rho_all[b] - rho_ret[b]                               (Eq. 7)
 //   skip[b]     = gap[b] <= delta_LS
 //
-// Two launches, both bandwidth-bound on the two [T x d] reads: a wave per
+// The fused routed block (ce_routed_block_gap) gets the per-token sums from
+// its down GEMM's epilogue instead (token_cos_parts_kernel), so it reads
+// neither matrix again. The standalone entry point takes
+// two launches, both bandwidth-bound on the two [T x d] reads: a wave per
 // token accumulates the three sums in fp64 from 16-byte loads (bf16 and fp32
 // products are exact in fp64, so only the summation order rounds) and writes
 // the token's cosine; then a workgroup per sequence adds the cosines in fp64
@@ -69,6 +72,44 @@ __global__ __launch_bounds__(256) void token_cos_kernel(const char* __restrict__
   }
 }
 
+// Per-token cosine of a routed block from the down GEMM's per-row partial
+// sums (a wave per token): dropped tokens bypass the layer (output = input),
+// so their cosine is 1 (also for a zero row); for a retained token the lanes
+// load the gap_np slots of its packed row together (lane q, q + 64, ...) and
+// add them in fp64, then across the wave in a fixed tree order.
+__global__ __launch_bounds__(256) void token_cos_parts_kernel(const double* __restrict__ gap_part, int gap_np, int T,
+                                                              int cap, const int32_t* __restrict__ token_pos,
+                                                              float* __restrict__ cos_out) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= T) return;
+  const int p = token_pos[i];
+  if (p < 0) {
+    if (lane == 0) cos_out[i] = 1.0f;
+    return;
+  }
+  if (p >= cap) {  // more retained rows than the capacity (reported in the status word)
+    if (lane == 0) cos_out[i] = __builtin_nanf("");
+    return;
+  }
+  const double* g = gap_part + (int64_t)p * gap_np * 4;
+  double dot = 0.0, na = 0.0, nb = 0.0;
+  for (int q = lane; q < gap_np; q += 64) {
+    dot += g[4 * q + 0];
+    na += g[4 * q + 1];
+    nb += g[4 * q + 2];
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    dot += __shfl_xor(dot, o);
+    na += __shfl_xor(na, o);
+    nb += __shfl_xor(nb, o);
+  }
+  if (lane == 0) {
+    const double both = sqrt(na) * sqrt(nb);
+    cos_out[i] = (float)(both > 0.0 ? dot / both : (na == 0.0 && nb == 0.0 ? 1.0 : 0.0));
+  }
+}
+
 __global__ __launch_bounds__(256) void gap_kernel(const int32_t* __restrict__ offs, int T,
                                                   const int32_t* __restrict__ token_pos,
                                                   const float* __restrict__ cos_tok, float delta,
@@ -115,6 +156,20 @@ __global__ __launch_bounds__(256) void gap_kernel(const int32_t* __restrict__ of
 }
 
 }  // namespace
+
+hipError_t launch_gap_from_parts(const double* gap_part, int gap_np, int cap, const int32_t* seq_offsets, int B,
+                                 int T, const int32_t* token_pos, float delta, float* cos_tok, float* rho_all,
+                                 float* rho_ret, float* gap, uint8_t* skip, hipStream_t stream) {
+  if (T > 0) {
+    hipLaunchKernelGGL(token_cos_parts_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, gap_part, gap_np, T, cap,
+                       token_pos, cos_tok);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(gap_kernel, dim3(B), dim3(256), 0, stream, seq_offsets, T, token_pos,
+                     (const float*)cos_tok, delta, rho_all, rho_ret, gap, skip);
+  return hipGetLastError();
+}
 
 hipError_t launch_layer_gap(const char* x_in, const char* x_out, const int32_t* seq_offsets, int B, int T, int d,
                             bool bf16, const int32_t* token_pos, float delta, float* cos_tok, float* rho_all,

@@ -509,19 +509,25 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
 #pragma unroll
       for (int e = 0; e < NACC; ++e) acc[i][j][e] = f32x16_t{};
 
-  // Issue order: iteration k issues token slab k + kTokRing - 1, then rank
-  // slab k + kRankRing - 1; the prologue runs the same pattern for
+  // Issue order: iteration k issues rank slab k + kRankRing - 1, then token
+  // slab k + kTokRing - 1; the prologue runs the same pattern for
   // k = -(kTokRing - 1) .. -1 (negative slabs skipped). Operations complete
-  // in order and rank slab k is issued after token slab k, so "slab k has
-  // landed" is "at most (kRankRing - 2) iterations' operations are in flight".
+  // in order, and rank slab k is issued after token slab k (kTokRing >
+  // kRankRing), so "slab k has landed" is "rank slab k has landed": at most
+  // the token part of its own iteration and (kRankRing - 2) whole iterations
+  // are in flight. Token rows, which come from HBM, thus have kTokRing - 1
+  // iterations to land and rank rows, mostly L2 hits, kRankRing - 1 (issuing
+  // the tokens first would make each rank slab wait for the token slab issued
+  // just before it, leaving the tokens only kRankRing - 1 iterations).
+  static_assert(kTokRing > kRankRing, "token slabs run further ahead");
   for (int k = -(kTokRing - 1); k < 0; ++k) {
-    dma_t(k + kTokRing - 1, k + kTokRing - 1);
     if (k + kRankRing - 1 >= 0) dma_r(k + kRankRing - 1, k + kRankRing - 1);
+    dma_t(k + kTokRing - 1, k + kTokRing - 1);
   }
   const uint32_t rkey = (uint32_t)((lrow >> 1) & 7);
   int tst = 0, rst = 0;  // ring stages of slab k
   for (int k = 0; k < nk; ++k) {
-    wait_vmcnt<(kRankRing - 2) * (IT + IR)>();
+    wait_vmcnt<IT + (kRankRing - 2) * (IT + IR)>();
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
     const char* sa = smem + kTokRing * kTokB + rst * kRankB;
@@ -539,8 +545,8 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
     }
     // every wave is past slab k - 1 (the barrier above): its stages receive
     // token slab k + kTokRing - 1 and rank slab k + kRankRing - 1
-    dma_t(k + kTokRing - 1, tst == 0 ? kTokRing - 1 : tst - 1);
     dma_r(k + kRankRing - 1, rst == 0 ? kRankRing - 1 : rst - 1);
+    dma_t(k + kTokRing - 1, tst == 0 ? kTokRing - 1 : tst - 1);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int step = 0; step < 4; ++step)

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -414,3 +414,22 @@ def test_noalloc_topk_validation():
     assert f(ctypes.byref(b), FAKE, FAKE, ce.CE_BF16, 100, FAKE, FAKE, None, FAKE, None, None) == ce.CE_ERR_UNSUPPORTED
     big = _batch(B=65537, T=70000, cap=70000)
     assert f(ctypes.byref(big), FAKE, None, 0, 0, FAKE, FAKE, None, None, None, None) == ce.CE_ERR_UNSUPPORTED
+
+
+def test_block_gap_validation():
+    """ce_routed_block_gap rejects missing gap outputs, a non-finite delta and
+    a workspace sized for ce_routed_block (CE_WS_BLOCK) before any launch."""
+    f = ce.lib.ce_routed_block_gap
+    b = _batch(cap=60)
+    sw, fw = _scorer(), _ffn()
+    need = ce.lib.ce_workspace_size(ce.CE_WS_BLOCK_GAP, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    small = ce.lib.ce_workspace_size(ce.CE_WS_BLOCK, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    assert need > small
+    args = lambda **k: [ctypes.byref(b), FAKE, FAKE, ctypes.byref(sw), ctypes.byref(fw), None, None, None,
+                        k.get("delta", 0.004), k.get("cos", FAKE), k.get("ra", FAKE), k.get("rr", FAKE),
+                        k.get("g", FAKE), None, FAKE, k.get("ws", need), None]
+    assert f(*args(cos=None)) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(ra=None)) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(g=None)) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(delta=float("nan"))) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(ws=small)) == ce.CE_ERR_WORKSPACE

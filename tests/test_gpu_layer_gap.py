@@ -171,3 +171,47 @@ def test_gap_of_the_routed_block(G, kind):
     got, ref = run_gap(G, G.host(dw.hidden), G.host(out), wl.seq_offsets, tp, "bf16")
     dropped = tp < 0
     assert np.all(got[3][dropped] == 1.0)
+
+
+@pytest.mark.parametrize("inplace", [True, False])
+@pytest.mark.parametrize("kind,d,F", [("und", 128, 256), ("gen", 128, 256), ("mixed", 128, 256),
+                                      ("mot", 128, 256), ("mot", 512, 2048), ("und", 2048, 1024)])
+def test_fused_gap_of_the_routed_block(G, kind, d, F, inplace):
+    """ce_routed_block_gap: the same outputs as ce_routed_block bit for bit,
+    and the gap (Eq. 7) of its own input and output against the oracle, from
+    the down GEMM's epilogue sums (generic and ping-pong down kernels, split
+    tail tiles at 512 / 2048 and 2048 / 1024, MoT groups); dropped tokens have
+    cos = 1 exactly."""
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = small_workload(kind, seed=14, dtype="bf16", d=d, F=F)
+    dw = G.DevWorkload(wl)
+    ref_in = dw.hidden.clone()
+    ref_out = ref_in if inplace else torch.full_like(ref_in, 5.0)
+    ce.ce_routed_block(dw.batch, ref_in, ref_out, dw.scorer, dw.ffn, dw.ws(ce.CE_WS_BLOCK))
+    h_in = dw.hidden.clone()
+    out = h_in if inplace else torch.full_like(h_in, 5.0)
+    kidx, koff = dw.new_idx()
+    cos = torch.full((max(wl.T, 1),), float("nan"), device="cuda")
+    ra, rr, g = (torch.full((wl.B,), float("nan"), device="cuda") for _ in range(3))
+    skip = torch.full((wl.B,), 7, dtype=torch.uint8, device="cuda")
+    ws = dw.ws(ce.CE_WS_BLOCK_GAP)
+    ce.ce_routed_block_gap(dw.batch, h_in, out, dw.scorer, dw.ffn, ws, DELTA, cos, ra, rr, g, skip,
+                           kept_idx_out=kidx, kept_offsets_out=koff)
+    torch.cuda.synchronize()
+    assert ce.ce_workspace_status(ws) == 0
+    y = G.host(out)
+    np.testing.assert_array_equal(y, G.host(ref_out))
+    kept = G.host(kidx)[:int(G.host(koff)[-1])]
+    tp = np.full(wl.T, -1, np.int32)
+    tp[kept] = np.arange(len(kept))
+    r_all, r_ret, gp, c = lg.redundancy_gap(wl.hidden, y, wl.seq_offsets, tp)
+    got_c = G.host(cos)[:wl.T]
+    np.testing.assert_allclose(got_c, c, rtol=0, atol=COS_TOL)
+    assert np.all(got_c[tp < 0] == 1.0)
+    np.testing.assert_allclose(G.host(ra), r_all, rtol=0, atol=RHO_TOL)
+    np.testing.assert_allclose(G.host(rr), r_ret, rtol=0, atol=RHO_TOL)
+    np.testing.assert_allclose(G.host(g), gp, rtol=0, atol=GAP_TOL)
+    far = np.abs(gp - DELTA) > GAP_TOL
+    np.testing.assert_array_equal(G.host(skip)[far], (gp <= DELTA)[far].astype(np.uint8))
+    print(f"[fused gap {kind} d={d} F={F} inplace={inplace}] gap {gp[:3]}", flush=True)
