@@ -80,7 +80,7 @@ enum {
 };
 
 /* ---- workspace kinds ---------------------------------------------------- */
-enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2, CE_WS_BLOCK_GAP = 3 };
+enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2, CE_WS_BLOCK_GAP = 3, CE_WS_FFN_PRUNED = 4 };
 
 /*
  * A ragged batch of B sequences packed back to back: sequence b owns tokens
@@ -409,6 +409,38 @@ int ce_ffn_saliency(const ce_batch* batch, const void* act, const int32_t* kept_
 int ce_ffn_mask_channels(const ce_batch* batch, void* act, const int32_t* kept_offsets, int dtype,
                          int32_t d_ff, const uint8_t* prune_mask, const uint8_t* use_pruned,
                          void* stream);
+
+/*
+ * The FFN on the packed rows with the pruning decision taken on the fly and
+ * the pruned FFN doing less work (section 3.4, UCS operator (2); Eq. 8-9).
+ * P is the tail of the channels, [n_keep, d_ff): a layer whose static mask is
+ * another set permutes its FFN channels once (W_gate / W_up rows and W_down
+ * columns together, which leaves the FFN unchanged) so that P comes last.
+ *   1. gate/up + SwiGLU as ce_ffn_gateup; its epilogue also adds up |z| per
+ *      channel over each run of rows of one sequence (no second pass over the
+ *      [Kt x d_ff] activations);
+ *   2. saliency[b][c] = mean_j |z[j][c]| * norms[set(j)][c] over the packed rows of
+ *      sequence b (Eq. 8), leakage[b] = sum_{c >= n_keep} saliency[b][c] /
+ *      sum_c saliency[b][c] (Eq. 9; 0 when the sum is 0), use_pruned[b] =
+ *      leakage[b] <= delta;
+ *   3. down: rows of sequences with use_pruned skip the channels of P (they
+ *      read zeros there, and a 256-row tile whose rows all run pruned stops
+ *      its K loop at n_keep), so ffn_out is the pruned FFN for those sequences
+ *      and the full FFN for the others, as ce_ffn_mask_channels + ce_ffn_down.
+ * Arguments as ce_routed_ffn, plus
+ *   norms       device float32 [n_sets x d_ff]: ce_ffn_down_colnorms of w
+ *   n_keep      channels kept by the pruned FFN: 0 <= n_keep <= d_ff, n_keep % 64 == 0
+ *   delta       leakage threshold (the paper's delta_FFN is 0.150), finite
+ *   saliency    device float32 [B x d_ff] out; leakage device float32 [B] out
+ *   use_pruned  device uint8 [B] out (read back by step 3)
+ *   ws          device workspace of ce_workspace_size(CE_WS_FFN_PRUNED, ...) bytes
+ * bf16 only, with d and d_ff such that both GEMMs run on the ping-pong kernel
+ * (K at least 3 x 64 elements); else CE_ERR_UNSUPPORTED. Deterministic.
+ */
+int ce_routed_ffn_pruned(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
+                         const int32_t* kept_offsets, const ce_ffn_w* w, const float* norms,
+                         int32_t n_keep, float delta, void* ffn_out, float* saliency, float* leakage,
+                         uint8_t* use_pruned, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Layer-skipping redundancy gap (section 3.4, UCS operator (1); Eq. 7). For a

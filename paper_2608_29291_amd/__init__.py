@@ -31,7 +31,7 @@ CE_OK, CE_ERR_INVALID_ARG, CE_ERR_UNSUPPORTED, CE_ERR_WORKSPACE, CE_ERR_HIP = 0,
 CE_F32, CE_BF16 = 0, 1
 CE_TOK_GEN, CE_TOK_KEEP = 1, 2
 CE_DEV_BAD_OFFSETS, CE_DEV_OVERFLOW = 1, 2
-CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK, CE_WS_BLOCK_GAP = 0, 1, 2, 3
+CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK, CE_WS_BLOCK_GAP, CE_WS_FFN_PRUNED = 0, 1, 2, 3, 4
 
 EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
@@ -39,6 +39,7 @@ EXPORTED = [
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "ce_routed_attention", "ce_score_tiling", "ce_topk_compact_noalloc", "ce_routed_block_gap",
+    "ce_routed_ffn_pruned",
 ]
 
 
@@ -117,6 +118,8 @@ _sig("ce_routed_block", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.P
 _sig("ce_routed_block_gap", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.POINTER(CEScorerW),
                                            ctypes.POINTER(CEFFNW), _p, _p, _p, ctypes.c_float, _p, _p, _p, _p, _p,
                                            _p, ctypes.c_size_t, _p])
+_sig("ce_routed_ffn_pruned", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _i32,
+                                            ctypes.c_float, _p, _p, _p, _p, _p, ctypes.c_size_t, _p])
 _sig("ce_drop_stability", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, _p, _p, _p])
 _sig("ce_ffn_down_colnorms", ctypes.c_int, [ctypes.POINTER(CEFFNW), _p, _p])
 _sig("ce_ffn_saliency", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, _p, ctypes.POINTER(CEFFNW), _p, _p,
@@ -479,6 +482,29 @@ def ce_ffn_down(batch: Batch, act, kept_idx, kept_offsets, ffn: FFN, ffn_out, ws
                            wp, wn, _stream(stream)), "ce_ffn_down")
 
 
+def ce_routed_ffn_pruned(batch: Batch, compact, kept_idx, kept_offsets, ffn: FFN, norms, n_keep, delta, ffn_out,
+                         saliency, leakage, use_pruned, ws, stream=None):
+    """SwiGLU FFN on the packed rows with the FFN-pruning decision (Eq. 8-9)
+    taken from the gate/up epilogue's |z| sums; P = channels [n_keep, d_ff).
+    ws: ce_workspace_size(CE_WS_FFN_PRUNED, ...) bytes."""
+    import torch
+    cb = batch.c()
+    fw = ffn.c()
+    cap, B = int(batch.kept_capacity), batch.B
+    tdt = ffn.w_gate[0].dtype
+    f32 = torch.float32
+    wp, wn = _ws_ptr(ws, ce_workspace_size(CE_WS_FFN_PRUNED, batch, fw.d, fw.d_ff, fw.dtype))
+    _check(lib.ce_routed_ffn_pruned(ctypes.byref(cb), _chk(compact, "compact", tdt, shape=(None, fw.d), rows_min=cap),
+                                    _chk(kept_idx, "kept_idx", torch.int32, numel=cap),
+                                    _chk(kept_offsets, "kept_offsets", torch.int32, numel=B + 1), ctypes.byref(fw),
+                                    _chk(norms, "norms", f32, numel=fw.n_sets * fw.d_ff), int(n_keep), float(delta),
+                                    _chk(ffn_out, "ffn_out", tdt, shape=(None, fw.d), rows_min=cap),
+                                    _chk(saliency, "saliency", f32, numel=B * fw.d_ff),
+                                    _chk(leakage, "leakage", f32, numel=B),
+                                    _chk(use_pruned, "use_pruned", torch.uint8, numel=B), wp, wn, _stream(stream)),
+           "ce_routed_ffn_pruned")
+
+
 def ce_scatter_residual(batch: Batch, ffn_out, kept_idx, kept_offsets, hidden_in, hidden_out,
                         stream=None):
     import torch
@@ -643,10 +669,10 @@ def ce_routed_attention(q, k, v, o, q_offsets, kv_offsets, causal, scale, stream
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
-    "ce_score", "ce_topk_compact", "ce_topk_compact_noalloc", "ce_routed_ffn", "ce_ffn_gateup", "ce_ffn_down",
+    "ce_score", "ce_topk_compact", "ce_topk_compact_noalloc", "ce_routed_ffn", "ce_routed_ffn_pruned", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block", "ce_routed_block_gap", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "ce_routed_attention", "CEAttn",
-    "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK", "CE_WS_BLOCK_GAP",
+    "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK", "CE_WS_BLOCK_GAP", "CE_WS_FFN_PRUNED",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -403,6 +403,60 @@ int ce_routed_ffn(const ce_batch* batch, const void* compact, const int32_t* kep
   return CE_OK;
 }
 
+int ce_routed_ffn_pruned(const ce_batch* batch, const void* compact, const int32_t* kept_idx,
+                         const int32_t* kept_offsets, const ce_ffn_w* w, const float* norms, int32_t n_keep,
+                         float delta, void* ffn_out, float* saliency, float* leakage, uint8_t* use_pruned,
+                         void* ws, size_t ws_bytes, void* stream) {
+  CE_CHECK(check_batch(batch, false));
+  CE_CHECK(check_ffn(w));
+  if (!kept_offsets || !norms || !saliency || !leakage || !use_pruned) return CE_ERR_INVALID_ARG;
+  if (batch->kept_capacity > 0 && (!compact || !kept_idx || !ffn_out)) return CE_ERR_INVALID_ARG;
+  if (!isfinite(delta)) return CE_ERR_INVALID_ARG;
+  if (w->dtype != CE_BF16) return CE_ERR_UNSUPPORTED;
+  if (n_keep < 0 || n_keep > w->d_ff || (n_keep % 64) != 0) return CE_ERR_UNSUPPORTED;
+  const WsLayout L = ws_layout(CE_WS_FFN_PRUNED, batch->B, batch->T, batch->kept_capacity, w->d, w->d_ff, 2);
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int32_t* kt = kept_offsets + batch->B;
+  int32_t* grp = w->n_sets == 2 ? at<int32_t>(ws, L.grp_rows) : nullptr;
+  int32_t* n0 = w->n_sets == 2 ? at<int32_t>(ws, L.grp_n0) : nullptr;
+  char* act = at<char>(ws, L.act);
+  int32_t* row_seq = at<int32_t>(ws, L.row_seq);
+  FfnGemmArgs g = gateup_args(w, batch, static_cast<const char*>(compact), grp, nullptr, act, nullptr, kt, n0);
+  set_split(g, ws, L, 0);
+  g.row_seq = row_seq;
+  g.sal_part = at<float>(ws, L.sal_seg);
+  g.sal_meta = at<int32_t>(ws, L.sal_meta);
+  FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr, nullptr, kt, n0);
+  set_split(dn, ws, L, 1);
+  dn.row_seq = row_seq;
+  dn.use_pruned = use_pruned;
+  dn.ns_keep = n_keep * 2 / 128;
+  dn.n_seq = batch->B;
+  if (batch->kept_capacity > 0 && !ffn_pruned_ok(g, dn)) return CE_ERR_UNSUPPORTED;
+  float* chunk_tot = at<float>(ws, L.sal_part) + (size_t)kSalSplits * batch->B * w->d_ff;
+  if (batch->kept_capacity == 0) {
+    // no rows: zero saliency, leakage 0 (the pruned FFN runs, on nothing)
+    FfnGemmArgs none = g;
+    return hip_status(launch_saliency_segments(none, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot,
+                                               saliency, leakage, use_pruned, s));
+  }
+  if (w->n_sets == 2)
+    CE_TRY(launch_group(kept_idx, kept_offsets, batch->B, batch->kept_capacity, batch->T, batch->flags, grp, n0,
+                        s));
+  CE_TRY(launch_row_seq(kept_offsets, batch->B, batch->kept_capacity, row_seq, s));
+  g.clear_n = ffn_split_counters(dn, 1, true);
+  g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
+  // 1. gate/up + SwiGLU, with the per-segment |z| sums
+  CE_TRY(launch_ffn_gateup(g, true, s));
+  // 2. saliency (Eq. 8), leakage (Eq. 9) and the pruned/full choice per sequence
+  CE_TRY(launch_saliency_segments(g, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot, saliency, leakage,
+                                  use_pruned, s));
+  // 3. down, skipping the channels of P on the rows that run pruned
+  CE_TRY(launch_ffn_down_pruned(dn, s, g.clear_cnt != nullptr));
+  return CE_OK;
+}
+
 int ce_scatter_residual(const ce_batch* batch, const void* ffn_out, const int32_t* kept_idx,
                         const int32_t* kept_offsets, int dtype, int32_t d, const void* hidden_in,
                         void* hidden_out, void* stream) {

@@ -340,8 +340,11 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
 // kSplit: 1 = whole tiles only; 2 = tail tiles in two K pieces; 0 = tail
 // tiles in sp.pieces > 2 K pieces (separate instances keep the whole-tile and
 // two-piece code free of the general merge).
+// kPrune (down only): rows of sequences that run the pruned FFN read zeros
+// for the channels of P (the K tail from superslab a.ns_keep on), and a whole
+// tile of such rows stops its K loop there.
 template <int kMode, int kGroup, bool kPrio, int kSplit, int kWBufs = 2, bool kSpreadW = true,
-          bool kSpreadT = true>
+          bool kSpreadT = true, bool kPrune = false>
 __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) void ffn_gemm_pp2_kernel(
     FfnGemmArgs a, int n_tt, int n_ft, GemmSplit sp) {
   constexpr int kWR = 256, kTR = 256;
@@ -428,6 +431,8 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   // real data.
   const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, (uint32_t)(a.tok_rows * a.tok_ld));
   uint32_t voff[8];
+  uint32_t voff2[kPrune ? 8 : 1];
+  bool lane_pruned = true;
   if (is_w) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -468,6 +473,48 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       const int c = pch ^ ((r >> 1) & 7);
       voff[q] = src[q] < 0 ? 0x80000000u : (uint32_t)((int64_t)src[q] * a.tok_ld + c * 16);
     }
+    if constexpr (kPrune) {
+      // rows whose sequence runs pruned: a second set of offsets past the
+      // resource (zeros, no traffic) for the superslabs of P
+      int pk[8], sq[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int j = row_lo + 64 * (wave & 3) + 8 * q + r8;
+        pk[q] = j < row_hi ? j : -1;
+      }
+      if (a.omap1) {
+        int v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = a.omap1[pk[q] < 0 ? 0 : pk[q]];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) pk[q] = pk[q] < 0 ? -1 : v[q];
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        int b = a.row_seq[pk[q] < 0 ? 0 : pk[q]];
+        sq[q] = b < 0 ? 0 : (b >= a.n_seq ? a.n_seq - 1 : b);
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const bool pr = a.use_pruned[sq[q]] != 0;
+        voff2[q] = (pk[q] >= 0 && pr) ? 0x80000000u : voff[q];
+        lane_pruned = lane_pruned && (pk[q] < 0 || pr);
+      }
+    }
+  }
+  // every row of the tile runs pruned: a workgroup-wide and through the (not
+  // yet used) ring, one vote per wave; waves without pruning information vote yes
+  bool tile_pruned = false;
+  if constexpr (kPrune) {
+    int* const votes = reinterpret_cast<int*>(smem);
+    const bool wave_yes = __ballot(!lane_pruned) == 0ull;
+    if (lane == 0) votes[wave] = wave_yes ? 1 : 0;
+    __syncthreads();
+    int all = 1;
+#pragma unroll
+    for (int w2 = 0; w2 < 8; ++w2) all &= votes[w2];
+    tile_pruned = all != 0;
+    __syncthreads();  // every wave has read the votes before the DMA fills the ring
   }
   // weight row block (64 w + 8 q) / 32 has the parity of q / 4: the gate / up
   // choice is fixed per instruction at compile time. kPart 0 issues all 8
@@ -484,11 +531,13 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
               (kMode == 0 && ((q >> 2) & 1)) ? wr1 : wr0,
               (__attribute__((address_space(3))) void*)(region + 8 * q * kRow), 16, (int)voff[q], soff, 0, 0);
     } else {
+      const bool tail = kPrune && s >= a.ns_keep;  // a superslab of P
 #pragma unroll
       for (int q = 0; q < 8; ++q)
         if (kPart == 0 || (kPart == 1) == (q < 4))
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              trs, (__attribute__((address_space(3))) void*)(region + 8 * q * kRow), 16, (int)voff[q], soff, 0, 0);
+              trs, (__attribute__((address_space(3))) void*)(region + 8 * q * kRow), 16,
+              (int)(tail ? voff2[kPrune ? q : 0] : voff[q]), soff, 0, 0);
     }
   };
   using I0 = std::integral_constant<int, 0>;
@@ -519,7 +568,10 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   // tile is split (>= 3 per range, checked by the launcher)
   const int ns_all = a.k_bytes / kRow;
   const int s0 = ns_all * piece / pieces;
-  const int ns = ns_all * (piece + 1) / pieces;
+  int ns = ns_all * (piece + 1) / pieces;
+  // a whole tile of pruned rows skips the superslabs of P (they would only
+  // multiply zeros); K pieces keep their range and read zeros there
+  if (kPrune && pieces == 1 && tile_pruned && a.ns_keep >= 3 && a.ns_keep < ns) ns = a.ns_keep;
   // each ring starts with all but one of its slots in flight; the first
   // superslab must have landed
   constexpr int kBufs0 = kWBufs;  // waves 0-3 (weights)
@@ -758,6 +810,66 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         *reinterpret_cast<u32x4_t*>(a.out + (int64_t)map_row(jr, a.omap1, a.omap2) * a.out_ld +
                                     (int64_t)(f0 + 8 * cc) * 2) = v;
     }
+    if (a.sal_part) {
+      // ---- FFN-pruning signal (Eq. 8): per segment of the tile (a run of
+      //      rows of one sequence) and feature, the sum of |z| over its rows,
+      //      from the staged tile (the values just written, after rounding).
+      //      Scratch after the staged tile: row keys [256], segment starts
+      //      [kSalSegs + 2], per-wave start counts [4], sums [4][128] ----
+      int* const keys = reinterpret_cast<int*>(smem + 65536);
+      int* const seg = keys + 256;
+      int* const wcnt = seg + kSalSegs + 2;
+      float* const red = reinterpret_cast<float*>(smem + 65536 + 2048);
+      const int nvalid = min(256, row_hi - row_lo);
+      if (tid < 256) {
+        int key = -1;
+        if (tid < nvalid) {
+          const int jr = row_lo + tid;
+          key = a.row_seq[a.map1 ? a.map1[jr] : jr];
+        }
+        keys[tid] = key;
+      }
+      __syncthreads();
+      bool st = false;
+      uint64_t sm = 0;
+      if (tid < 256) {
+        const int key = keys[tid];
+        st = key >= 0 && (tid == 0 || keys[tid - 1] != key);
+        sm = __ballot(st);
+        if (lane == 0) wcnt[wave] = __popcll(sm);
+      }
+      __syncthreads();
+      if (tid < 256) {
+        int k = 0;
+        for (int w2 = 0; w2 < wave; ++w2) k += wcnt[w2];
+        k += __popcll(sm & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+        if (st && k < kSalSegs) seg[k] = tid;
+        if (tid == 0) seg[kSalSegs + 1] = (wcnt[0] + wcnt[1]) + (wcnt[2] + wcnt[3]);
+      }
+      __syncthreads();
+      const int nseg = seg[kSalSegs + 1];
+      if (nseg <= kSalSegs) {
+        const int f = tid & 127, q = tid >> 7;
+        const int cf = f >> 3, fe = (f & 7) * 2;
+        for (int k = 0; k < nseg; ++k) {
+          const int r0 = seg[k], r1 = k + 1 < nseg ? seg[k + 1] : nvalid;
+          float sum = 0.0f;
+          for (int r = r0 + q; r < r1; r += 4)
+            sum += fabsf(bf16_to_f32(*reinterpret_cast<const uint16_t*>(ost + r * 256 + ((cf ^ (r & 15)) << 4) + fe)));
+          red[q * 128 + f] = sum;
+          __syncthreads();
+          if (q == 0 && f0 + f < n_feat)
+            a.sal_part[((int64_t)tt * kSalSegs + k) * n_feat + f0 + f] =
+                ((red[f] + red[128 + f]) + red[256 + f]) + red[384 + f];
+          __syncthreads();
+        }
+      }
+      if (ft == 0 && tid <= kSalSegs) {
+        int32_t* meta = a.sal_meta + (int64_t)tt * (kSalSegs + 1);
+        if (tid == 0) meta[0] = nseg;
+        else if (tid - 1 < nseg) meta[tid] = keys[seg[tid - 1]];
+      }
+    }
   } else {
     __builtin_amdgcn_sched_barrier(0);  // keep the residual loads out of the split-K merge above
     char* orow[kMT];
@@ -867,7 +979,8 @@ GemmSplit pp2_plan(const FfnGemmArgs& a, int* n_tt, int* n_ft) {
   return sp;
 }
 
-template <int kMode, int kGroup, bool kPrio, int kWBufs = 2, bool kSpreadW = true, bool kSpreadT = true>
+template <int kMode, int kGroup, bool kPrio, int kWBufs = 2, bool kSpreadW = true, bool kSpreadT = true,
+          bool kPrune = false>
 hipError_t launch_pp2(const FfnGemmArgs& a, const GemmSplit& sp, int n_tt, int n_ft, hipStream_t stream,
                       bool counters_clear) {
   if (n_tt <= 0 || n_ft <= 0) return hipSuccess;
@@ -880,13 +993,13 @@ hipError_t launch_pp2(const FfnGemmArgs& a, const GemmSplit& sp, int n_tt, int n
   }
   const int grid = kXcds * (sp.whole_x + sp.tail_x * sp.pieces);
   if (sp.pieces == 1)
-    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 1, kWBufs, kSpreadW, kSpreadT>), dim3(grid),
+    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 1, kWBufs, kSpreadW, kSpreadT, kPrune>), dim3(grid),
                        dim3(512), 0, stream, a, n_tt, n_ft, sp);
   else if (sp.pieces == 2)
-    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 2, kWBufs, kSpreadW, kSpreadT>), dim3(grid),
+    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 2, kWBufs, kSpreadW, kSpreadT, kPrune>), dim3(grid),
                        dim3(512), 0, stream, a, n_tt, n_ft, sp);
   else
-    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 0, kWBufs, kSpreadW, kSpreadT>), dim3(grid),
+    hipLaunchKernelGGL((ffn_gemm_pp2_kernel<kMode, kGroup, kPrio, 0, kWBufs, kSpreadW, kSpreadT, kPrune>), dim3(grid),
                        dim3(512), 0, stream, a, n_tt, n_ft, sp);
   return hipGetLastError();
 }
@@ -959,6 +1072,14 @@ int ffn_split_counters(const FfnGemmArgs& a, int mode, bool bf16) {
   const GemmSplit sp = mode == 0 ? pp2_plan<0>(a, &n_tt, &n_ft) : pp2_plan<1>(a, &n_tt, &n_ft);
   if (mode == 1 && !down_on_pp2(a, sp, n_tt, n_ft)) return 0;
   return sp.pieces > 1 ? kXcds * sp.tail_x : 0;
+}
+
+bool ffn_pruned_ok(const FfnGemmArgs& g, const FfnGemmArgs& dn) { return pp2_ok(g) && pp2_ok(dn); }
+
+hipError_t launch_ffn_down_pruned(const FfnGemmArgs& a, hipStream_t stream, bool counters_clear) {
+  int n_tt, n_ft;
+  const GemmSplit sp = pp2_plan<1>(a, &n_tt, &n_ft);
+  return launch_pp2<1, 8, true, 2, true, true, true>(a, sp, n_tt, n_ft, stream, counters_clear);
 }
 
 int ffn_down_gap_slots(const FfnGemmArgs& a, bool bf16) {

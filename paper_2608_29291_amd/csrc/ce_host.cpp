@@ -137,7 +137,8 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
     L.logits = take(sT * 4);
     L.score_part = take((size_t)kScoreMaxTiles * sT * 4);
   }
-  if (which == CE_WS_FFN || block) {
+  const bool pruned = which == CE_WS_FFN_PRUNED;
+  if (which == CE_WS_FFN || block || pruned) {
     L.grp_rows = take(sC * 4);
     L.grp_n0 = take(4);
     L.act = take(sC * sF * (size_t)elem);
@@ -159,6 +160,12 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
       L.dn_cnt = take((size_t)kSplitMaxSlots * 4);
     }
     L.sal_part = take(((size_t)kSalSplits * sB * sF + sB * ((sF + 255) / 256) * 2) * 4);
+  }
+  if (pruned) {
+    const size_t tiles = (sC + 255) / 256 + 1;  // token tiles of either number of weight sets
+    L.row_seq = take(sC * 4);
+    L.sal_seg = take(tiles * kSalSegs * sF * 4);
+    L.sal_meta = take(tiles * (kSalSegs + 1) * 4);
   }
   if (which == CE_WS_BLOCK_GAP) {
     // one slot per wave of the down GEMM and row; waves cover >= 32 features
@@ -275,8 +282,7 @@ int64_t ce_kept_count_host(int32_t B, int32_t T, const int32_t* offs, const uint
 }
 
 size_t ce_workspace_size(int which, const ce_batch* batch, int32_t d, int32_t d_ff, int dtype) {
-  if (!batch || (which != CE_WS_TOPK && which != CE_WS_FFN && which != CE_WS_BLOCK && which != CE_WS_BLOCK_GAP))
-    return 0;
+  if (!batch || which < CE_WS_TOPK || which > CE_WS_FFN_PRUNED) return 0;
   const int elem = ce::elem_size(dtype);
   if (!elem) return 0;
   return ce::ws_layout(which, batch->B, batch->T, batch->kept_capacity, d, d_ff, elem).total;

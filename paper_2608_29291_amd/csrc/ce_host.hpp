@@ -30,6 +30,9 @@ struct WsLayout {
   size_t gu_cnt;     // int32 [kSplitMaxSlots] arrival counters of the gate/up tail tiles
   size_t dn_cnt;     // int32 [kSplitMaxSlots] arrival counters of the down tail tiles
   size_t gap_part;   // double [cap x ceil(d / 32) x 4] layer-gap partial sums (CE_WS_BLOCK_GAP)
+  size_t row_seq;    // int32 [cap] sequence of each packed row (CE_WS_FFN_PRUNED)
+  size_t sal_seg;    // float [tiles x kSalSegs x d_ff] per-segment |z| sums (CE_WS_FFN_PRUNED)
+  size_t sal_meta;   // int32 [tiles x (kSalSegs + 1)] segment counts and sequences (CE_WS_FFN_PRUNED)
   size_t sal_part;   // float [kSalSplits x B x d_ff] FFN-saliency partial sums, then
                      // float [B x ceil(d_ff / 256) x 2] per-chunk totals
   size_t total;
@@ -70,6 +73,9 @@ void gemm_items(int mode, int cap, int d, int d_ff, int n_sets, int elem, int64_
 // The FFN-saliency reduction splits each sequence's rows over at most this
 // many workgroups (partial sums in the workspace, summed in a fixed order).
 constexpr int kSalSplits = 16;
+// The pruned FFN's gate/up epilogue keeps |z| sums for at most this many
+// segments (runs of rows of one sequence) per 256-row token tile.
+constexpr int kSalSegs = 8;
 
 // Token tile of the single-launch scorer: 32, or (bf16, r_core + r_exp <=
 // 384) 128 when that takes fewer rounds of 256 workgroups x rows of K each

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ce_host.hpp"
+
 namespace ce {
 
 // One "weights x tokens" FFN GEMM (see ce_ffn.hip).
@@ -48,6 +50,21 @@ struct FfnGemmArgs {
   // output): gap_part[(p * gap_np + q) * 4 + {0, 1, 2}]
   double* gap_part;
   int gap_np;
+  // FFN pruning (ce_routed_ffn_pruned). row_seq[p]: sequence of packed row p.
+  // gate/up: per token tile tt, the epilogue sums |z| over each run of rows of
+  // one sequence (a segment, at most kSalSegs per tile) into
+  // sal_part[(tt * kSalSegs + k) * d_ff + c]; sal_meta[tt * (kSalSegs + 1)] =
+  // the tile's segment count (more than kSalSegs: no partials), then each
+  // segment's sequence (NULL: none).
+  // down: rows whose sequence has use_pruned set read zeros from K superslab
+  // ns_keep on (the channels of P, the tail); a whole tile whose rows all run
+  // pruned stops its K loop there (NULL: no pruning).
+  const int32_t* row_seq;
+  float* sal_part;
+  int32_t* sal_meta;
+  const uint8_t* use_pruned;
+  int ns_keep;
+  int n_seq;  // B (clamps the sequence indices read from row_seq)
 };
 
 // counters_clear: this launch's arrival counters (tile_cnt) were already
@@ -58,6 +75,20 @@ hipError_t launch_ffn_down(const FfnGemmArgs& a, bool bf16, hipStream_t stream, 
 // Number of arrival counters a GEMM launch with these arguments uses (0: no
 // split); mode 0 = gate/up, 1 = down.
 int ffn_split_counters(const FfnGemmArgs& a, int mode, bool bf16);
+// Down GEMM of the pruned FFN: always the ping-pong kernel (the pruning
+// logic lives there); the caller checks ffn_pruned_ok first.
+hipError_t launch_ffn_down_pruned(const FfnGemmArgs& a, hipStream_t stream, bool counters_clear);
+bool ffn_pruned_ok(const FfnGemmArgs& gateup, const FfnGemmArgs& down);
+
+// Pruned FFN: row_seq[p] = b for the packed rows p of each sequence b.
+hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, hipStream_t stream);
+// Saliency (Eq. 8) of each sequence from the gate/up epilogue's segment sums
+// (falling back to act for tiles with more than kSalSegs segments) and the
+// leakage (Eq. 9) of the tail channels [n_keep, d_ff); use_pruned = leakage <= delta.
+hipError_t launch_saliency_segments(const FfnGemmArgs& gateup, const int32_t* kept_offsets, const float* norms,
+                                    int B, int n_keep, float delta, float* chunk_tot, float* saliency, float* lambda,
+                                    uint8_t* use_pruned, hipStream_t stream);
+
 // Gap partial-sum slots per row (gap_np) of the down kernel that
 // launch_ffn_down picks for these arguments: ceil(d / features per wave).
 int ffn_down_gap_slots(const FfnGemmArgs& a, bool bf16);

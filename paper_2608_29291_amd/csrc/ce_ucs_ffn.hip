@@ -211,7 +211,118 @@ __global__ __launch_bounds__(256) void mask_kernel(char* __restrict__ act, const
   }
 }
 
+// row_seq[p] = b for the packed rows p of sequence b (workgroup per sequence)
+__global__ __launch_bounds__(256) void row_seq_kernel(const int32_t* __restrict__ kept_offsets, int cap,
+                                                      int32_t* __restrict__ row_seq) {
+  const int b = blockIdx.x;
+  int j0 = kept_offsets[b], j1 = kept_offsets[b + 1];
+  j0 = j0 < 0 ? 0 : (j0 > cap ? cap : j0);
+  j1 = j1 < j0 ? j0 : (j1 > cap ? cap : j1);
+  for (int j = j0 + threadIdx.x; j < j1; j += 256) row_seq[j] = b;
+}
+
+// Saliency from the gate/up epilogue's segment sums (workgroup: channel chunk
+// x, sequence y; thread per channel). The token tiles are enumerated as the
+// GEMM does (set 0 rows, then set 1 rows, 256 per tile); each tile's segments
+// of sequence b add their |z| sums in tile order, per weight set; a tile with
+// more segments than the epilogue kept adds the rows of b from act instead.
+// saliency = (sum_set0 * norm0 + sum_set1 * norm1) / rows of b; the chunk's
+// totals over all channels and over the tail [n_keep, d_ff) go to chunk_tot
+// (the layout leakage_kernel reads).
+struct SegSalArgs {
+  const float* sal_part;
+  const int32_t* sal_meta;
+  const char* act;  // bf16 [cap x d_ff], GEMM row order
+  const int32_t* grp;  // GEMM row -> packed row (two weight sets) or NULL
+  const int32_t* row_seq;
+  const int32_t* kept_offsets;
+  const int32_t* kt_ptr;
+  const int32_t* n0_ptr;
+  const float* norms;
+  int B, cap, d_ff, n_sets, n_keep;
+  float* saliency;
+  float* chunk_tot;
+};
+
+__global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
+  __shared__ float red[2][4];
+  const int b = blockIdx.y;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  int kt = *a.kt_ptr;
+  kt = kt < 0 ? 0 : (kt > a.cap ? a.cap : kt);
+  int n0 = kt;
+  if (a.n_sets == 2 && a.n0_ptr) {
+    n0 = *a.n0_ptr;
+    n0 = n0 < 0 ? 0 : (n0 > kt ? kt : n0);
+  }
+  const int tiles0 = (n0 + 255) / 256;
+  const int tiles = tiles0 + (kt - n0 + 255) / 256;
+  float tot = 0.0f, pm = 0.0f;
+  if (c < a.d_ff) {
+    float acc[2] = {0.0f, 0.0f};
+    for (int tt = 0; tt < tiles; ++tt) {
+      const int set = tt < tiles0 ? 0 : 1;
+      const int32_t* meta = a.sal_meta + (int64_t)tt * (kSalSegs + 1);
+      const int cnt = meta[0];
+      if (cnt <= kSalSegs) {
+        for (int k = 0; k < cnt; ++k)
+          if (meta[1 + k] == b) acc[set] += a.sal_part[((int64_t)tt * kSalSegs + k) * a.d_ff + c];
+      } else {
+        const int lo = set == 0 ? tt * 256 : n0 + (tt - tiles0) * 256;
+        const int hi = min(lo + 256, set == 0 ? n0 : kt);
+        for (int j = lo; j < hi; ++j) {
+          const int p = a.grp ? a.grp[j] : j;
+          if (p >= 0 && p < a.cap && a.row_seq[p] == b)
+            acc[set] += fabsf(bf16_to_f32(reinterpret_cast<const uint16_t*>(a.act)[(int64_t)j * a.d_ff + c]));
+        }
+      }
+    }
+    int j0 = a.kept_offsets[b], j1 = a.kept_offsets[b + 1];
+    j0 = j0 < 0 ? 0 : (j0 > a.cap ? a.cap : j0);
+    j1 = j1 < j0 ? j0 : (j1 > a.cap ? a.cap : j1);
+    const float n1c = a.n_sets == 2 ? a.norms[(int64_t)a.d_ff + c] : 0.0f;
+    const float v = j1 > j0 ? (acc[0] * a.norms[c] + acc[1] * n1c) / (float)(j1 - j0) : 0.0f;
+    a.saliency[(int64_t)b * a.d_ff + c] = v;
+    tot = v;
+    pm = c >= a.n_keep ? v : 0.0f;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    tot += __shfl_xor(tot, o);
+    pm += __shfl_xor(pm, o);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = tot;
+    red[1][threadIdx.x >> 6] = pm;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float* o = a.chunk_tot + ((int64_t)b * gridDim.x + blockIdx.x) * 2;
+    o[0] = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    o[1] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, hipStream_t stream) {
+  hipLaunchKernelGGL(row_seq_kernel, dim3(B), dim3(256), 0, stream, kept_offsets, cap, row_seq);
+  return hipGetLastError();
+}
+
+hipError_t launch_saliency_segments(const FfnGemmArgs& g, const int32_t* kept_offsets, const float* norms, int B,
+                                    int n_keep, float delta, float* chunk_tot, float* saliency, float* lambda,
+                                    uint8_t* use_pruned, hipStream_t stream) {
+  // gate/up: GEMM row j is packed row map1[j] (the MoT grouping) or j; act is in GEMM row order
+  SegSalArgs s{g.sal_part, g.sal_meta, g.out, g.map1, g.row_seq, kept_offsets, g.kt_ptr, g.n0_ptr, norms,
+               B, g.cap, g.n_feat, g.n_sets, n_keep, saliency, chunk_tot};
+  const int chunks = (g.n_feat + 255) / 256;
+  hipLaunchKernelGGL(saliency_seg_kernel, dim3(chunks, B), dim3(256), 0, stream, s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(leakage_kernel, dim3((B + 255) / 256), dim3(256), 0, stream, (const float*)chunk_tot, chunks,
+                     B, delta, lambda, use_pruned);
+  return hipGetLastError();
+}
 
 hipError_t launch_colnorms(const char* w0, const char* w1, int n_sets, int d, int d_ff, bool bf16,
                            float* norms, hipStream_t stream) {

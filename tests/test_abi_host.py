@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 22
+    assert len(names) == 23
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -433,3 +433,26 @@ def test_block_gap_validation():
     assert f(*args(g=None)) == ce.CE_ERR_INVALID_ARG
     assert f(*args(delta=float("nan"))) == ce.CE_ERR_INVALID_ARG
     assert f(*args(ws=small)) == ce.CE_ERR_WORKSPACE
+
+
+def test_pruned_ffn_validation():
+    """ce_routed_ffn_pruned rejects missing outputs, a non-finite delta, a
+    channel split that is not whole 64-channel groups, fp32 and a workspace of
+    the plain FFN kind before any launch."""
+    f = ce.lib.ce_routed_ffn_pruned
+    b = _batch(cap=60)
+    fw = _ffn(d=256, F=512)
+    need = ce.lib.ce_workspace_size(ce.CE_WS_FFN_PRUNED, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    plain = ce.lib.ce_workspace_size(ce.CE_WS_FFN, ctypes.byref(b), 256, 512, ce.CE_BF16)
+    assert need > plain
+    args = lambda **k: [ctypes.byref(b), FAKE, FAKE, FAKE, ctypes.byref(k.get("w", fw)), k.get("norms", FAKE),
+                        k.get("n_keep", 384), k.get("delta", 0.15), FAKE, k.get("sal", FAKE), FAKE,
+                        k.get("use", FAKE), FAKE, k.get("ws", need), None]
+    assert f(*args(norms=None)) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(sal=None)) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(use=None)) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(delta=float("inf"))) == ce.CE_ERR_INVALID_ARG
+    assert f(*args(n_keep=100)) == ce.CE_ERR_UNSUPPORTED
+    assert f(*args(n_keep=576)) == ce.CE_ERR_UNSUPPORTED
+    assert f(*args(w=_ffn(d=256, F=512, dtype=ce.CE_F32))) == ce.CE_ERR_UNSUPPORTED
+    assert f(*args(ws=plain)) == ce.CE_ERR_WORKSPACE

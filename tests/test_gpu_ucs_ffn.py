@@ -14,7 +14,7 @@ import pytest
 
 import oracle
 from oracle import ucs_ffn as uf
-from ce_workloads import bf16_round, small_workload
+from ce_workloads import bf16_round, small_workload, make_workload, U, G as GEN, KEEP
 
 pytestmark = pytest.mark.gpu
 
@@ -178,3 +178,81 @@ def test_pruned_ffn_end_to_end(G, kind):
     err = G.rel_err(G.host(out)[:len(kept_idx)], ref_out)
     print(f"[pruned ffn {kind}] output rel err {err:.3e}")
     assert err <= G.OUT_TOL["bf16"]
+
+
+
+@pytest.mark.parametrize("kind,d,F", [("und", 256, 512), ("mot", 256, 512), ("mixed", 512, 2048),
+                                      ("mot", 512, 2048), ("und", 2048, 1024), ("short", 256, 512)])
+@pytest.mark.parametrize("mode", ["mixed", "all", "none"])
+def test_routed_ffn_pruned(G, kind, d, F, mode):
+    """ce_routed_ffn_pruned (P = the channel tail [n_keep, d_ff), about 30%):
+    saliency and leakage from the gate/up epilogue's segment sums against the
+    oracle on the same activations, the decisions where the leakage is clear
+    of delta, and ffn_out bit for bit equal to ce_ffn_mask_channels +
+    ce_ffn_down on those decisions (zeros read instead of P, and whole pruned
+    tiles stopping at n_keep, change no sum) and within the FFN bar of the
+    oracle's pruned / full FFN. Shapes with split tail tiles in both GEMMs
+    (512 / 2048, 2048 / 1024), MoT groups, and delta so that some, all or no
+    sequences run pruned; 41 short sequences for the segment-slot fallback."""
+    import torch
+    import paper_2608_29291_amd as ce
+    if kind == "short":
+        # 41 sequences of 2..40 tokens (two FFN sets): far more than the
+        # epilogue's per-tile segment slots, so most sequences take the fallback
+        rng = np.random.default_rng(31)
+        layout = [[(int(n), int(rng.choice([U, GEN, KEEP])))] for n in rng.integers(2, 41, size=41)]
+        wl = make_workload("short-seqs", layout, d=d, F=F, r_c=64, r_e=32, keep=0.5, dtype="bf16", seed=15,
+                           n_sets=2, biases=True)
+    else:
+        wl = small_workload(kind, seed=15, dtype="bf16", d=d, F=F)
+    n_keep = F - 64 * max(1, int(round(0.3 * F / 64)))
+    mask = np.arange(F) >= n_keep
+    _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    ref_sel = oracle.select(l32, wl.flags, wl.seq_offsets, wl.keep)
+    kept_idx, kept_off = ref_sel["kept_idx"], ref_sel["kept_offsets"]
+    kt = len(kept_idx)
+    dw = G.DevWorkload(wl)
+    kidx, koff = dw.new_idx()
+    comp = torch.zeros((max(dw.cap, 1), wl.d), dtype=torch.bfloat16, device="cuda")
+    ce.ce_topk_compact(dw.batch, G.to_dev(l32.astype(np.float32)), kidx, koff, dw.ws(ce.CE_WS_TOPK),
+                       hidden=dw.hidden, compact=comp)
+    n_sets = len(wl.ffn)
+    norms = torch.empty(n_sets * F, device="cuda")
+    ce.ce_ffn_down_colnorms(dw.ffn, norms)
+    # the activations the FFN computes (ce_ffn_gateup: the same kernel, packed order)
+    ws_f = dw.ws(ce.CE_WS_FFN)
+    act = torch.zeros((max(dw.cap, 1), F), dtype=torch.bfloat16, device="cuda")
+    ce.ce_ffn_gateup(dw.batch, comp, kidx, koff, dw.ffn, act, ws_f)
+    torch.cuda.synchronize()
+    z = G.host(act)[:kt]
+    s_ref, lam_ref, row_seq = oracle_signal(wl, z, kept_idx, kept_off, mask)
+    delta = {"mixed": float(np.median(lam_ref)), "all": 1.0, "none": -1.0}[mode]
+    ws = dw.ws(ce.CE_WS_FFN_PRUNED)
+    out = torch.full((max(dw.cap, 1), wl.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    sal = torch.full((wl.B * F,), float("nan"), device="cuda")
+    lam = torch.full((wl.B,), float("nan"), device="cuda")
+    use = torch.full((wl.B,), 7, dtype=torch.uint8, device="cuda")
+    ce.ce_routed_ffn_pruned(dw.batch, comp, kidx, koff, dw.ffn, norms, n_keep, delta, out, sal, lam, use, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(G.host(sal).reshape(wl.B, F), s_ref, rtol=S_RTOL, atol=1e-30)
+    lam_g = G.host(lam)
+    assert np.max(np.abs(lam_g - lam_ref)) <= LAM_ATOL
+    use_g = G.host(use).astype(bool)
+    clear = np.abs(lam_ref - delta) > LAM_ATOL
+    np.testing.assert_array_equal(use_g[clear], uf.use_pruned(lam_ref, delta)[clear])
+    # the same FFN through the staged masking path, on the GPU's own decisions
+    m = G.to_dev(mask.astype(np.uint8))
+    ce.ce_ffn_mask_channels(dw.batch, act, koff, m, G.to_dev(use_g.astype(np.uint8)))
+    out2 = torch.full_like(out, float("nan"))
+    ce.ce_ffn_down(dw.batch, act, kidx, koff, dw.ffn, out2, ws_f)
+    torch.cuda.synchronize()
+    f = G.host(out)[:kt]
+    np.testing.assert_array_equal(f, G.host(out2)[:kt])
+    zm = uf.masked_activations(z, row_seq, mask, use_g)
+    ref_out = np.zeros((kt, wl.d))
+    for j, tok in enumerate(kept_idx):
+        fset = wl.ffn[1] if (n_sets == 2 and wl.flags[tok] & 1) else wl.ffn[0]
+        ref_out[j] = zm[j] @ np.asarray(fset.w_down, np.float64).T
+    err = G.rel_err(f, ref_out)
+    print(f"[ffn pruned {kind} d={d} F={F} {mode}] pruned {use_g.sum()}/{wl.B}, out rel err {err:.2e}", flush=True)
+    assert err <= G.FFN_TOL["bf16"]
