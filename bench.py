@@ -474,6 +474,29 @@ def main():
                "frac": round(sal_bytes / (sal_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     log(f"ffn saliency + leakage: {sal_us:.1f} us")
 
+    # the pruned FFN in one call (bf16): P = the channel tail, about 30% of
+    # d_ff in whole 64-channel groups; every sequence pruned (delta = 1), none
+    # (delta = -1), beside the full FFN, in turn under the same load
+    if bf16:
+        n_keep = F - 64 * max(1, int(round(0.3 * F / 64)))
+        ws_pr = ce.alloc_workspace(ce.CE_WS_FFN_PRUNED, batch, d, F, dtc, device=dev)
+        out_pr = torch.empty_like(ffn_out)
+        pr = lambda delta: (lambda i: ce.ce_routed_ffn_pruned(
+            batch, compact, kept_idx, kept_off, ffn0, norms, n_keep, delta, out_pr, sal, lam, use, ws_pr,
+            stream=stream))
+        full_us, all_us, none_us = timed_pipeline(
+            (lambda i: ce.ce_routed_ffn(batch, compact, kept_idx, kept_off, ffn0, ffn_out, ws_ffn, stream=stream),
+             pr(1.0), pr(-1.0)), reps, gemm_warm)
+        ucs_ffn["pruned_ffn"] = {
+            "n_keep": n_keep, "pruned_channels": F - n_keep, "full_ffn_us": round(full_us, 2),
+            "pruned_ffn_all_sequences_us": round(all_us, 2), "pruned_ffn_no_sequence_us": round(none_us, 2),
+            "staged_signal_path_us": round(full_us + sal_us, 2),
+            "note": "ce_routed_ffn_pruned: saliency sums in the gate/up epilogue, P's channels skipped in the "
+                    "down GEMM; staged = ce_routed_ffn + ce_ffn_saliency (mask launch not counted)"}
+        log(f"pruned ffn: full {full_us:.1f} us, all pruned {all_us:.1f} us, none pruned {none_us:.1f} us "
+            f"(P = {F - n_keep} of {F})")
+        del ws_pr, out_pr
+
     # layer-skipping gap (section 3.4, Eq. 7) over this workload's hidden
     # states: two [T x d] reads, the per-token cosines written and re-read
     kt = int(kept_off[-1].item())

@@ -429,17 +429,16 @@ int ce_routed_ffn_pruned(const ce_batch* batch, const void* compact, const int32
   g.sal_meta = at<int32_t>(ws, L.sal_meta);
   FfnGemmArgs dn = down_args(w, batch, act, nullptr, static_cast<char*>(ffn_out), grp, nullptr, nullptr, kt, n0);
   set_split(dn, ws, L, 1);
-  dn.row_seq = row_seq;
-  dn.use_pruned = use_pruned;
+  uint8_t* row_flag = at<uint8_t>(ws, L.row_flag);
+  dn.row_flag = row_flag;
   dn.ns_keep = n_keep * 2 / 128;
-  dn.n_seq = batch->B;
   if (batch->kept_capacity > 0 && !ffn_pruned_ok(g, dn)) return CE_ERR_UNSUPPORTED;
   float* chunk_tot = at<float>(ws, L.sal_part) + (size_t)kSalSplits * batch->B * w->d_ff;
   if (batch->kept_capacity == 0) {
     // no rows: zero saliency, leakage 0 (the pruned FFN runs, on nothing)
     FfnGemmArgs none = g;
     return hip_status(launch_saliency_segments(none, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot,
-                                               saliency, leakage, use_pruned, s));
+                                               saliency, leakage, use_pruned, nullptr, s));
   }
   if (w->n_sets == 2)
     CE_TRY(launch_group(kept_idx, kept_offsets, batch->B, batch->kept_capacity, batch->T, batch->flags, grp, n0,
@@ -451,7 +450,7 @@ int ce_routed_ffn_pruned(const ce_batch* batch, const void* compact, const int32
   CE_TRY(launch_ffn_gateup(g, true, s));
   // 2. saliency (Eq. 8), leakage (Eq. 9) and the pruned/full choice per sequence
   CE_TRY(launch_saliency_segments(g, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot, saliency, leakage,
-                                  use_pruned, s));
+                                  use_pruned, row_flag, s));
   // 3. down, skipping the channels of P on the rows that run pruned
   CE_TRY(launch_ffn_down_pruned(dn, s, g.clear_cnt != nullptr));
   return CE_OK;

@@ -416,6 +416,17 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int n_feat = a.n_feat;
   constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
   const int f0 = ft * kFTile;
+  // gate/up with the FFN-pruning sums: the sequence of tile row tid - 256
+  // (token waves), loaded here so that its latency hides behind the K loop
+  // (in the epilogue instead where the two-piece merge leaves no register)
+  int sal_key = -1;
+  auto load_sal_key = [&]() __attribute__((always_inline)) {
+    if (a.sal_part && tid >= 256) {
+      const int jr = row_lo + tid - 256;
+      if (jr < row_hi) sal_key = a.row_seq[a.map1 ? a.map1[jr] : jr];
+    }
+  };
+  if constexpr (kMode == 0 && kSplit != 2) load_sal_key();
 
   // ---- DMA plan: waves 0-3 fetch weight rows 64 (w & 3) .. +63, waves 4-7
   //      the same token rows; instruction q covers 8 rows x 128 B ----
@@ -432,7 +443,6 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const __amdgpu_buffer_rsrc_t trs = make_rsrc(a.tok, (uint32_t)(a.tok_rows * a.tok_ld));
   uint32_t voff[8];
   uint32_t voff2[kPrune ? 8 : 1];
-  bool lane_pruned = true;
   if (is_w) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -473,54 +483,55 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       const int c = pch ^ ((r >> 1) & 7);
       voff[q] = src[q] < 0 ? 0x80000000u : (uint32_t)((int64_t)src[q] * a.tok_ld + c * 16);
     }
+  }
+  // Pruned FFN: lane l reads the flags of rows l, l + 64, l + 128, l + 192 of
+  // the tile (through the packed-row map with two weight sets). Every wave
+  // does, so each knows whether all rows of the tile run pruned without an
+  // exchange; the token waves move the flags of their DMA rows over with
+  // shuffles. The loads go out before the first DMAs and are used after them.
+  [[maybe_unused]] int fl4[kPrune ? 4 : 1];
+  [[maybe_unused]] bool ok4[kPrune ? 4 : 1];
+  if constexpr (kPrune) {
+    int jc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = row_lo + lane + 64 * i;
+      ok4[i] = j < row_hi;
+      jc[i] = ok4[i] ? j : row_lo;  // a valid row either way: branch-free loads
+    }
+    if (a.omap1) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) jc[i] = a.omap1[jc[i]];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fl4[i] = a.row_flag[jc[i]];
+  }
+  bool tile_pruned = false;
+  auto resolve_pruned = [&]() __attribute__((always_inline)) {
     if constexpr (kPrune) {
-      // rows whose sequence runs pruned: a second set of offsets past the
-      // resource (zeros, no traffic) for the superslabs of P
-      int pk[8], sq[8];
+      bool pr[4];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int j = row_lo + 64 * (wave & 3) + 8 * q + r8;
-        pk[q] = j < row_hi ? j : -1;
-      }
-      if (a.omap1) {
-        int v[8];
+      for (int i = 0; i < 4; ++i) pr[i] = ok4[i] && fl4[i] != 0;
+      const bool lane_all = (!ok4[0] || pr[0]) && (!ok4[1] || pr[1]) && (!ok4[2] || pr[2]) && (!ok4[3] || pr[3]);
+      tile_pruned = __ballot(!lane_all) == 0ull;
+      if (!is_w) {
+        // DMA row 64 (wave & 3) + 8 q + r8 is row lane 8 q + r8, slot wave & 3
+        const int slot = wave & 3;
+        const int mine = (int)(slot == 0 ? pr[0] : slot == 1 ? pr[1] : slot == 2 ? pr[2] : pr[3]);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] = a.omap1[pk[q] < 0 ? 0 : pk[q]];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) pk[q] = pk[q] < 0 ? -1 : v[q];
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        int b = a.row_seq[pk[q] < 0 ? 0 : pk[q]];
-        sq[q] = b < 0 ? 0 : (b >= a.n_seq ? a.n_seq - 1 : b);
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const bool pr = a.use_pruned[sq[q]] != 0;
-        voff2[q] = (pk[q] >= 0 && pr) ? 0x80000000u : voff[q];
-        lane_pruned = lane_pruned && (pk[q] < 0 || pr);
+        for (int q = 0; q < 8; ++q) voff2[q] = __shfl(mine, 8 * q + r8) ? 0x80000000u : voff[q];
       }
     }
-  }
-  // every row of the tile runs pruned: a workgroup-wide and through the (not
-  // yet used) ring, one vote per wave; waves without pruning information vote yes
-  bool tile_pruned = false;
-  if constexpr (kPrune) {
-    int* const votes = reinterpret_cast<int*>(smem);
-    const bool wave_yes = __ballot(!lane_pruned) == 0ull;
-    if (lane == 0) votes[wave] = wave_yes ? 1 : 0;
-    __syncthreads();
-    int all = 1;
-#pragma unroll
-    for (int w2 = 0; w2 < 8; ++w2) all &= votes[w2];
-    tile_pruned = all != 0;
-    __syncthreads();  // every wave has read the votes before the DMA fills the ring
-  }
+  };
   // weight row block (64 w + 8 q) / 32 has the parity of q / 4: the gate / up
   // choice is fixed per instruction at compile time. kPart 0 issues all 8
   // instructions, 1 the first four (rows 0-31 of the wave's 64), 2 the rest.
-  auto dma = [&](int s, int buf, auto part) __attribute__((always_inline)) {
+  // tmode (pruned FFN, token rows): 0 = not a superslab of P, 1 = one, 2 =
+  // decided here from s (the K loop runs as two loops, so only the prologue
+  // selects per instruction)
+  auto dma = [&](int s, int buf, auto part, auto tmode) __attribute__((always_inline)) {
     constexpr int kPart = decltype(part)::value;
+    constexpr int kTail = decltype(tmode)::value;
     const int soff = s * kRow;
     char* region = (is_w ? wsm : tsm) + buf * kSlab + 64 * (wave & 3) * kRow;
     if (is_w) {
@@ -531,7 +542,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
               (kMode == 0 && ((q >> 2) & 1)) ? wr1 : wr0,
               (__attribute__((address_space(3))) void*)(region + 8 * q * kRow), 16, (int)voff[q], soff, 0, 0);
     } else {
-      const bool tail = kPrune && s >= a.ns_keep;  // a superslab of P
+      const bool tail = kPrune && (kTail == 1 || (kTail == 2 && s >= a.ns_keep));  // a superslab of P
 #pragma unroll
       for (int q = 0; q < 8; ++q)
         if (kPart == 0 || (kPart == 1) == (q < 4))
@@ -569,27 +580,33 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const int ns_all = a.k_bytes / kRow;
   const int s0 = ns_all * piece / pieces;
   int ns = ns_all * (piece + 1) / pieces;
-  // a whole tile of pruned rows skips the superslabs of P (they would only
-  // multiply zeros); K pieces keep their range and read zeros there
-  if (kPrune && pieces == 1 && tile_pruned && a.ns_keep >= 3 && a.ns_keep < ns) ns = a.ns_keep;
   // each ring starts with all but one of its slots in flight; the first
   // superslab must have landed
   constexpr int kBufs0 = kWBufs;  // waves 0-3 (weights)
   constexpr int kBufs1 = kTBufs;  // waves 4-7 (tokens)
+  // the pruning choice is needed before the first DMAs only when they reach
+  // the superslabs of P; otherwise its loads overlap theirs
+  const bool resolve_first = kPrune && s0 + kBufs1 - 1 > a.ns_keep;
+  if (resolve_first) resolve_pruned();
+  using T2 = std::integral_constant<int, kPrune ? 2 : 0>;
   if (is_w) {
 #pragma unroll
-    for (int q = 0; q < kBufs0 - 1; ++q) dma(s0 + q, q, I0{});
-    wait_vmcnt<8 * (kBufs0 - 2)>();
+    for (int q = 0; q < kBufs0 - 1; ++q) dma(s0 + q, q, I0{}, I0{});
   } else {
 #pragma unroll
-    for (int q = 0; q < kBufs1 - 1; ++q) dma(s0 + q, q, I0{});
-    wait_vmcnt<8 * (kBufs1 - 2)>();
+    for (int q = 0; q < kBufs1 - 1; ++q) dma(s0 + q, q, I0{}, T2{});
   }
+  if (kPrune && !resolve_first) resolve_pruned();
+  // a whole tile of pruned rows skips the superslabs of P (they would only
+  // multiply zeros); K pieces keep their range and read zeros there
+  if (kPrune && pieces == 1 && tile_pruned && a.ns_keep >= 3 && a.ns_keep < ns) ns = a.ns_keep;
+  if (is_w) wait_vmcnt<8 * (kBufs0 - 2)>();
+  else wait_vmcnt<8 * (kBufs1 - 2)>();
   lds_barrier();  // superslab 0 is in LDS
   if (late) lds_barrier();
   int wb = 0, tb = 0;  // ring slots of superslab s
   // one memory phase and one compute phase over K half H of superslab s
-  auto half = [&](int s, auto hc, auto on) __attribute__((always_inline)) {
+  auto half = [&](int s, auto hc, auto on, auto tmode) __attribute__((always_inline)) {
     constexpr int H = decltype(hc)::value;
     constexpr bool kOn = decltype(on)::value;
     // ---- memory phase: fragments of K half H of superslab s ----
@@ -614,11 +631,11 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     const int fslot = slot == 0 ? nb - 1 : slot - 1;
     if (fill < ns) {
       if (is_w) {
-        if constexpr (kSpreadW) dma(fill, fslot, std::integral_constant<int, H + 1>{});
-        else if constexpr (H == 0) dma(fill, fslot, I0{});
+        if constexpr (kSpreadW) dma(fill, fslot, std::integral_constant<int, H + 1>{}, I0{});
+        else if constexpr (H == 0) dma(fill, fslot, I0{}, I0{});
       } else {
-        if constexpr (kSpreadT) dma(fill, fslot, std::integral_constant<int, H + 1>{});
-        else if constexpr (H == 0) dma(fill, fslot, I0{});
+        if constexpr (kSpreadT) dma(fill, fslot, std::integral_constant<int, H + 1>{}, tmode);
+        else if constexpr (H == 0) dma(fill, fslot, I0{}, tmode);
       }
     }
     // superslab s + 1 is read right after the barrier that ends group A's
@@ -654,12 +671,24 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   // two instances of the K loop, picked once per tile: with MFMAs, and
   // without them for a wave whose rows are all past the tile's end (same DMA
   // and barriers); a branch inside the loop cost 1-1.5% on full tiles
+  // The pruned FFN's K loop runs in two parts: the token DMAs of the first
+  // fill superslabs before P, those of the second superslabs of P (token
+  // waves fill superslab s + kBufs1 - 1 in iteration s).
   auto kloop = [&](auto on) __attribute__((always_inline)) {
-    for (int s = s0; s < ns; ++s) {
-      half(s, I0{}, on);
-      half(s, I1{}, on);
-      wb = wb + 1 == kBufs0 ? 0 : wb + 1;
-      tb = tb + 1 == kBufs1 ? 0 : tb + 1;
+    auto run = [&](int lo, int hi, auto tmode) __attribute__((always_inline)) {
+      for (int s = lo; s < hi; ++s) {
+        half(s, I0{}, on, tmode);
+        half(s, I1{}, on, tmode);
+        wb = wb + 1 == kBufs0 ? 0 : wb + 1;
+        tb = tb + 1 == kBufs1 ? 0 : tb + 1;
+      }
+    };
+    if constexpr (kPrune) {
+      const int s_sw = min(max(a.ns_keep - (kBufs1 - 1), s0), ns);
+      run(s0, s_sw, I0{});
+      run(s_sw, ns, I1{});
+    } else {
+      run(s0, ns, I0{});
     }
   };
   if (mfma_on) kloop(std::true_type{});
@@ -815,21 +844,16 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       //      rows of one sequence) and feature, the sum of |z| over its rows,
       //      from the staged tile (the values just written, after rounding).
       //      Scratch after the staged tile: row keys [256], segment starts
-      //      [kSalSegs + 2], per-wave start counts [4], sums [4][128] ----
+      //      [kSalSegs + 2], per-wave start counts [4], sums [8][128] ----
       int* const keys = reinterpret_cast<int*>(smem + 65536);
       int* const seg = keys + 256;
       int* const wcnt = seg + kSalSegs + 2;
+      static_assert(kMode != 0 || (kWBufs + kTBufs) * kSlab >= 131072, "saliency reads past the staged tile");
       float* const red = reinterpret_cast<float*>(smem + 65536 + 2048);
       const int nvalid = min(256, row_hi - row_lo);
-      if (tid < 256) {
-        int key = -1;
-        if (tid < nvalid) {
-          const int jr = row_lo + tid;
-          key = a.row_seq[a.map1 ? a.map1[jr] : jr];
-        }
-        keys[tid] = key;
-      }
-      __syncthreads();
+      if constexpr (kSplit == 2) load_sal_key();
+      if (tid >= 256) keys[tid - 256] = sal_key;
+      lds_barrier();
       bool st = false;
       uint64_t sm = 0;
       if (tid < 256) {
@@ -838,7 +862,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         sm = __ballot(st);
         if (lane == 0) wcnt[wave] = __popcll(sm);
       }
-      __syncthreads();
+      lds_barrier();
       if (tid < 256) {
         int k = 0;
         for (int w2 = 0; w2 < wave; ++w2) k += wcnt[w2];
@@ -846,22 +870,56 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         if (st && k < kSalSegs) seg[k] = tid;
         if (tid == 0) seg[kSalSegs + 1] = (wcnt[0] + wcnt[1]) + (wcnt[2] + wcnt[3]);
       }
-      __syncthreads();
+      lds_barrier();
       const int nseg = seg[kSalSegs + 1];
       if (nseg <= kSalSegs) {
-        const int f = tid & 127, q = tid >> 7;
-        const int cf = f >> 3, fe = (f & 7) * 2;
+        // thread: features 8 cf .. 8 cf + 7 (one 16-byte chunk) of the rows
+        // rg, rg + 32, ...; the 32 row classes are added in a fixed order
+        // (lanes xor 16 and 32 in the wave, then the 8 waves in turn)
+        const int cf = lane & 15;
+        const int rg = 4 * wave + (lane >> 4);
         for (int k = 0; k < nseg; ++k) {
           const int r0 = seg[k], r1 = k + 1 < nseg ? seg[k + 1] : nvalid;
-          float sum = 0.0f;
-          for (int r = r0 + q; r < r1; r += 4)
-            sum += fabsf(bf16_to_f32(*reinterpret_cast<const uint16_t*>(ost + r * 256 + ((cf ^ (r & 15)) << 4) + fe)));
-          red[q * 128 + f] = sum;
-          __syncthreads();
-          if (q == 0 && f0 + f < n_feat)
-            a.sal_part[((int64_t)tt * kSalSegs + k) * n_feat + f0 + f] =
-                ((red[f] + red[128 + f]) + red[256 + f]) + red[384 + f];
-          __syncthreads();
+          float sum[8] = {};
+          // rows rs, rs + 32, ... below r1 (rs: the first row >= r0 of this
+          // class); all share the swizzle rs & 15, so they lie 8 KB apart
+          const int rs = r0 + ((rg - r0) & 31);
+          const int nr = rs < r1 ? (r1 - rs + 31) >> 5 : 0;
+          // All eight reads are issued, then the ones past r1 are masked:
+          // they stay inside the LDS block (rows < 255 + 32 + 7 * 32 of 256
+          // bytes = 128 KB), and reading them costs less than waiting for
+          // each read in turn.
+          const char* const src = ost + rs * 256 + ((cf ^ (rs & 15)) << 4);
+          u32x4_t v[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) v[i] = *reinterpret_cast<const u32x4_t*>(src + i * 8192);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t keep = i < nr ? 0xffffffffu : 0u;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const uint32_t w = v[i][e] & keep;
+              sum[2 * e] += fabsf(__uint_as_float(w << 16));
+              sum[2 * e + 1] += fabsf(__uint_as_float(w & 0xffff0000u));
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            sum[e] += __shfl_xor(sum[e], 16);
+            sum[e] += __shfl_xor(sum[e], 32);
+          }
+          float* const rk = red + (k & 1) * 1024;  // two buffers: one barrier per segment
+          if (lane < 16) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) rk[wave * 128 + 8 * cf + e] = sum[e];
+          }
+          lds_barrier();
+          if (tid < 128 && f0 + tid < n_feat) {
+            float t = 0.0f;
+#pragma unroll
+            for (int w2 = 0; w2 < 8; ++w2) t += rk[w2 * 128 + tid];
+            a.sal_part[((int64_t)tt * kSalSegs + k) * n_feat + f0 + tid] = t;
+          }
         }
       }
       if (ft == 0 && tid <= kSalSegs) {

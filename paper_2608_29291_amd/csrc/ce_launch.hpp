@@ -56,15 +56,15 @@ struct FfnGemmArgs {
   // sal_part[(tt * kSalSegs + k) * d_ff + c]; sal_meta[tt * (kSalSegs + 1)] =
   // the tile's segment count (more than kSalSegs: no partials), then each
   // segment's sequence (NULL: none).
-  // down: rows whose sequence has use_pruned set read zeros from K superslab
-  // ns_keep on (the channels of P, the tail); a whole tile whose rows all run
-  // pruned stops its K loop there (NULL: no pruning).
+  // down: packed rows p with row_flag[p] != 0 (their sequence runs pruned)
+  // read zeros from K superslab ns_keep on (the channels of P, the tail); a
+  // whole tile whose rows all run pruned stops its K loop there (NULL: no
+  // pruning).
   const int32_t* row_seq;
   float* sal_part;
   int32_t* sal_meta;
-  const uint8_t* use_pruned;
+  const uint8_t* row_flag;
   int ns_keep;
-  int n_seq;  // B (clamps the sequence indices read from row_seq)
 };
 
 // counters_clear: this launch's arrival counters (tile_cnt) were already
@@ -84,10 +84,11 @@ bool ffn_pruned_ok(const FfnGemmArgs& gateup, const FfnGemmArgs& down);
 hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, hipStream_t stream);
 // Saliency (Eq. 8) of each sequence from the gate/up epilogue's segment sums
 // (falling back to act for tiles with more than kSalSegs segments) and the
-// leakage (Eq. 9) of the tail channels [n_keep, d_ff); use_pruned = leakage <= delta.
+// leakage (Eq. 9) of the tail channels [n_keep, d_ff); use_pruned = leakage <= delta,
+// also written to row_flag for every packed row of the sequence.
 hipError_t launch_saliency_segments(const FfnGemmArgs& gateup, const int32_t* kept_offsets, const float* norms,
                                     int B, int n_keep, float delta, float* chunk_tot, float* saliency, float* lambda,
-                                    uint8_t* use_pruned, hipStream_t stream);
+                                    uint8_t* use_pruned, uint8_t* row_flag, hipStream_t stream);
 
 // Gap partial-sum slots per row (gap_np) of the down kernel that
 // launch_ffn_down picks for these arguments: ceil(d / features per wave).

@@ -175,17 +175,40 @@ __global__ __launch_bounds__(256) void saliency_combine_kernel(const float* __re
 // thread per sequence: leakage = masked total / total over the channel chunks, in chunk order
 __global__ __launch_bounds__(256) void leakage_kernel(const float* __restrict__ chunk_tot, int chunks, int B,
                                                       float delta, float* __restrict__ lambda,
-                                                      uint8_t* __restrict__ use_pruned) {
-  const int b = blockIdx.x * 256 + threadIdx.x;
+                                                      uint8_t* __restrict__ use_pruned,
+                                                      const int32_t* __restrict__ kept_offsets, int cap,
+                                                      uint8_t* __restrict__ row_flag) {
+  // one wave per sequence: lane l adds chunks l, l + 64, ..., then the lanes
+  // are added in a fixed tree
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (b >= B) return;
   float t = 0.0f, p = 0.0f;
-  for (int k = 0; k < chunks; ++k) {
+  for (int k = lane; k < chunks; k += 64) {
     t += chunk_tot[((int64_t)b * chunks + k) * 2];
     p += chunk_tot[((int64_t)b * chunks + k) * 2 + 1];
   }
+  for (int o = 32; o > 0; o >>= 1) {
+    t += __shfl_xor(t, o);
+    p += __shfl_xor(p, o);
+  }
+  // lane 0's totals (a butterfly may round differently in other lanes)
+  t = __shfl(t, 0);
+  p = __shfl(p, 0);
   const float lam = t > 0.0f ? p / t : 0.0f;
-  lambda[b] = lam;
-  if (use_pruned) use_pruned[b] = lam <= delta ? 1 : 0;
+  const uint8_t use = lam <= delta ? 1 : 0;
+  if (lane == 0) {
+    lambda[b] = lam;
+    if (use_pruned) use_pruned[b] = use;
+  }
+  if (row_flag) {
+    // the choice for each packed row of the sequence (the pruned down GEMM
+    // reads one byte per row instead of row -> sequence -> choice)
+    int j0 = kept_offsets[b], j1 = kept_offsets[b + 1];
+    j0 = j0 < 0 ? 0 : (j0 > cap ? cap : j0);
+    j1 = j1 < j0 ? j0 : (j1 > cap ? cap : j1);
+    for (int j = j0 + lane; j < j1; j += 64) row_flag[j] = use;
+  }
 }
 
 // one workgroup per packed row: zero the masked channels of rows whose sequence runs pruned
@@ -257,10 +280,17 @@ __global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
   }
   const int tiles0 = (n0 + 255) / 256;
   const int tiles = tiles0 + (kt - n0 + 255) / 256;
+  int j0 = a.kept_offsets[b], j1 = a.kept_offsets[b + 1];
+  j0 = j0 < 0 ? 0 : (j0 > kt ? kt : j0);
+  j1 = j1 < j0 ? j0 : (j1 > kt ? kt : j1);
+  // one FFN set: GEMM rows are packed rows, so only the tiles over [j0, j1)
+  // hold rows of sequence b; two sets: its rows may sit in any tile
+  const int t_lo = a.n_sets == 2 ? 0 : j0 / 256;
+  const int t_hi = a.n_sets == 2 ? tiles : (j1 > j0 ? (j1 - 1) / 256 + 1 : t_lo);
   float tot = 0.0f, pm = 0.0f;
   if (c < a.d_ff) {
     float acc[2] = {0.0f, 0.0f};
-    for (int tt = 0; tt < tiles; ++tt) {
+    for (int tt = t_lo; tt < t_hi; ++tt) {
       const int set = tt < tiles0 ? 0 : 1;
       const int32_t* meta = a.sal_meta + (int64_t)tt * (kSalSegs + 1);
       const int cnt = meta[0];
@@ -277,9 +307,6 @@ __global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
         }
       }
     }
-    int j0 = a.kept_offsets[b], j1 = a.kept_offsets[b + 1];
-    j0 = j0 < 0 ? 0 : (j0 > a.cap ? a.cap : j0);
-    j1 = j1 < j0 ? j0 : (j1 > a.cap ? a.cap : j1);
     const float n1c = a.n_sets == 2 ? a.norms[(int64_t)a.d_ff + c] : 0.0f;
     const float v = j1 > j0 ? (acc[0] * a.norms[c] + acc[1] * n1c) / (float)(j1 - j0) : 0.0f;
     a.saliency[(int64_t)b * a.d_ff + c] = v;
@@ -311,7 +338,7 @@ hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* 
 
 hipError_t launch_saliency_segments(const FfnGemmArgs& g, const int32_t* kept_offsets, const float* norms, int B,
                                     int n_keep, float delta, float* chunk_tot, float* saliency, float* lambda,
-                                    uint8_t* use_pruned, hipStream_t stream) {
+                                    uint8_t* use_pruned, uint8_t* row_flag, hipStream_t stream) {
   // gate/up: GEMM row j is packed row map1[j] (the MoT grouping) or j; act is in GEMM row order
   SegSalArgs s{g.sal_part, g.sal_meta, g.out, g.map1, g.row_seq, kept_offsets, g.kt_ptr, g.n0_ptr, norms,
                B, g.cap, g.n_feat, g.n_sets, n_keep, saliency, chunk_tot};
@@ -319,8 +346,8 @@ hipError_t launch_saliency_segments(const FfnGemmArgs& g, const int32_t* kept_of
   hipLaunchKernelGGL(saliency_seg_kernel, dim3(chunks, B), dim3(256), 0, stream, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(leakage_kernel, dim3((B + 255) / 256), dim3(256), 0, stream, (const float*)chunk_tot, chunks,
-                     B, delta, lambda, use_pruned);
+  hipLaunchKernelGGL(leakage_kernel, dim3((B + 3) / 4), dim3(256), 0, stream, (const float*)chunk_tot, chunks,
+                     B, delta, lambda, use_pruned, kept_offsets, g.cap, row_flag);
   return hipGetLastError();
 }
 
@@ -353,8 +380,8 @@ hipError_t launch_saliency(const char* act, const int32_t* kept_idx, const int32
                      B, kept_offsets, cap, mask, d_ff, saliency, chunk_tot);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(leakage_kernel, dim3((B + 255) / 256), dim3(256), 0, stream, (const float*)chunk_tot, cchunks,
-                     B, delta, lambda, use_pruned);
+  hipLaunchKernelGGL(leakage_kernel, dim3((B + 3) / 4), dim3(256), 0, stream, (const float*)chunk_tot, cchunks,
+                     B, delta, lambda, use_pruned, kept_offsets, cap, (uint8_t*)nullptr);
   return hipGetLastError();
 }
 

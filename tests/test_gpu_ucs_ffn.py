@@ -205,7 +205,7 @@ def test_routed_ffn_pruned(G, kind, d, F, mode):
                            n_sets=2, biases=True)
     else:
         wl = small_workload(kind, seed=15, dtype="bf16", d=d, F=F)
-    n_keep = F - 64 * max(1, int(round(0.3 * F / 64)))
+    n_keep = {"keep0": 0, "keepall": F}.get(mode, F - 64 * max(1, int(round(0.3 * F / 64))))
     mask = np.arange(F) >= n_keep
     _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
     ref_sel = oracle.select(l32, wl.flags, wl.seq_offsets, wl.keep)
@@ -226,7 +226,7 @@ def test_routed_ffn_pruned(G, kind, d, F, mode):
     torch.cuda.synchronize()
     z = G.host(act)[:kt]
     s_ref, lam_ref, row_seq = oracle_signal(wl, z, kept_idx, kept_off, mask)
-    delta = {"mixed": float(np.median(lam_ref)), "all": 1.0, "none": -1.0}[mode]
+    delta = {"mixed": float(np.median(lam_ref)), "all": 1.0, "none": -1.0, "keep0": 1.0, "keepall": 0.5}[mode]
     ws = dw.ws(ce.CE_WS_FFN_PRUNED)
     out = torch.full((max(dw.cap, 1), wl.d), float("nan"), dtype=torch.bfloat16, device="cuda")
     sal = torch.full((wl.B * F,), float("nan"), device="cuda")
@@ -256,3 +256,17 @@ def test_routed_ffn_pruned(G, kind, d, F, mode):
     err = G.rel_err(f, ref_out)
     print(f"[ffn pruned {kind} d={d} F={F} {mode}] pruned {use_g.sum()}/{wl.B}, out rel err {err:.2e}", flush=True)
     assert err <= G.FFN_TOL["bf16"]
+    if mode == "keep0":
+        # every channel in P and every sequence pruned: the down GEMM reads only zeros
+        assert use_g.all() and not np.any(f)
+    if mode == "keepall":
+        # P empty: leakage 0, every sequence "pruned", nothing skipped
+        assert use_g.all() and not np.any(lam_g)
+
+
+@pytest.mark.parametrize("kind,d,F", [("mixed", 512, 2048), ("mot", 256, 512)])
+@pytest.mark.parametrize("mode", ["keep0", "keepall"])
+def test_routed_ffn_pruned_edges(G, kind, d, F, mode):
+    """ce_routed_ffn_pruned with P = every channel (n_keep = 0) and P empty
+    (n_keep = d_ff)."""
+    test_routed_ffn_pruned(G, kind, d, F, mode)
