@@ -396,10 +396,11 @@ def main():
     act = torch.empty((cap, F), dtype=dt, device=dev)
     ffn_out = torch.empty((cap, d), dtype=dt, device=dev)
     ws_topk = ce.alloc_workspace(ce.CE_WS_TOPK, batch, d, F, dtc, device=dev)
+    ws_score = ce.alloc_workspace(ce.CE_WS_SCORE, batch, d, F, dtc, device=dev)
     ws_ffn = ce.alloc_workspace(ce.CE_WS_FFN, batch, d, F, dtc, device=dev)
     h0 = base_h
     sc0, ff0 = wsets[0]
-    ce.ce_score(batch, h0, sc0, logits, stream=stream)
+    ce.ce_score_ws(batch, h0, sc0, logits, ws_score, stream=stream)
     ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk, hidden=h0, compact=compact,
                        stream=stream)
     torch.cuda.synchronize()
@@ -447,7 +448,7 @@ def main():
 
     stage_names = ("score", "topk_compact", "ffn_gateup", "ffn_down")
     stage_fns = (
-        lambda i: ce.ce_score(batch, h0, wsets[i % n_sets][0], logits, stream=stream),
+        lambda i: ce.ce_score_ws(batch, h0, wsets[i % n_sets][0], logits, ws_score, stream=stream),
         lambda i: ce.ce_topk_compact(batch, logits, kept_idx, kept_off, ws_topk, stream=stream),
         lambda i: ce.ce_ffn_gateup(batch, compact, kept_idx, kept_off, wsets[i % n_sets][1], act, ws_ffn,
                                    stream=stream),
@@ -455,6 +456,9 @@ def main():
                                  stream=stream))
     stages = dict(zip(stage_names, timed_pipeline(stage_fns, reps, gemm_warm)))
     log("stages (us): " + ", ".join(f"{k}={v:.1f}" for k, v in stages.items()))
+    # the workspace-free ce_score (single-launch scorer) on the same data
+    score_single_us = timed(lambda i: ce.ce_score(batch, h0, wsets[i % n_sets][0], logits, stream=stream), reps)
+    log(f"ce_score without a workspace: {score_single_us:.1f} us")
 
     # FFN-pruning signal (section 3.4, Eq. 8-9) on this step's activations: one
     # read of act plus the per-sequence saliency rows; a 30% static mask
@@ -550,6 +554,7 @@ def main():
         "block_tflops": round(block_flops / (ms * 1e-3) / 1e12, 2),
         "step_us": step_stats,
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
+        "score_single_launch_us": round(score_single_us, 2),
         "roofline": roofline,
     }
     result["ucs_signals"] = time_drop_stability(ce, stream, max(args.steps, 10))

@@ -80,7 +80,7 @@ enum {
 };
 
 /* ---- workspace kinds ---------------------------------------------------- */
-enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2, CE_WS_BLOCK_GAP = 3, CE_WS_FFN_PRUNED = 4 };
+enum { CE_WS_TOPK = 0, CE_WS_FFN = 1, CE_WS_BLOCK = 2, CE_WS_BLOCK_GAP = 3, CE_WS_FFN_PRUNED = 4, CE_WS_SCORE = 5 };
 
 /*
  * A ragged batch of B sequences packed back to back: sequence b owns tokens
@@ -196,6 +196,20 @@ int ce_workspace_status(const void* ws, uint32_t* status_out, void* stream);
  */
 int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w,
              float* logits, float* probs, void* stream);
+
+/*
+ * Step 1 with a workspace (section 3.2, Eq. 4 and Eq. 6): the scorer
+ * ce_routed_block uses. Where ce_score_tiling returns 1 (large bf16 batches
+ * with many ranks) the rank-tiled kernel writes per-token partial sums into
+ * the workspace and a second launch adds them in the fused block's TopK
+ * order, so the logits equal that block's bit for bit; otherwise this is
+ * ce_score. Arguments as ce_score;
+ *   ws  device workspace of ce_workspace_size(CE_WS_SCORE, ...) bytes
+ *       (d = the scorer's hidden size; d_ff is not read)
+ * Errors as ce_score; CE_ERR_WORKSPACE for a missing or short workspace.
+ */
+int ce_score_ws(const ce_batch* batch, const void* hidden, const ce_scorer_w* w,
+                float* logits, float* probs, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Steps 2-3 -- per-sequence TopK and packing (section 3.4, Eq. 6).

@@ -31,7 +31,7 @@ CE_OK, CE_ERR_INVALID_ARG, CE_ERR_UNSUPPORTED, CE_ERR_WORKSPACE, CE_ERR_HIP = 0,
 CE_F32, CE_BF16 = 0, 1
 CE_TOK_GEN, CE_TOK_KEEP = 1, 2
 CE_DEV_BAD_OFFSETS, CE_DEV_OVERFLOW = 1, 2
-CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK, CE_WS_BLOCK_GAP, CE_WS_FFN_PRUNED = 0, 1, 2, 3, 4
+CE_WS_TOPK, CE_WS_FFN, CE_WS_BLOCK, CE_WS_BLOCK_GAP, CE_WS_FFN_PRUNED, CE_WS_SCORE = 0, 1, 2, 3, 4, 5
 
 EXPORTED = [
     "ce_status_string", "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size",
@@ -39,7 +39,7 @@ EXPORTED = [
     "ce_ffn_down", "ce_scatter_residual", "ce_routed_block", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "ce_routed_attention", "ce_score_tiling", "ce_topk_compact_noalloc", "ce_routed_block_gap",
-    "ce_routed_ffn_pruned",
+    "ce_routed_ffn_pruned", "ce_score_ws",
 ]
 
 
@@ -101,6 +101,8 @@ _sig("ce_kept_count_host", ctypes.c_int64, [_i32, _i32, _p, _p, ctypes.c_float])
 _sig("ce_workspace_size", ctypes.c_size_t, [ctypes.c_int, ctypes.POINTER(CEBatch), _i32, _i32, ctypes.c_int])
 _sig("ce_workspace_status", ctypes.c_int, [_p, ctypes.POINTER(ctypes.c_uint32), _p])
 _sig("ce_score", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, ctypes.POINTER(CEScorerW), _p, _p, _p])
+_sig("ce_score_ws", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, ctypes.POINTER(CEScorerW), _p, _p, _p,
+                                   ctypes.c_size_t, _p])
 _sig("ce_topk_compact", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p, _p,
                                        _p, _p, ctypes.c_size_t, _p])
 _sig("ce_topk_compact_noalloc", ctypes.c_int, [ctypes.POINTER(CEBatch), _p, _p, ctypes.c_int, _i32, _p, _p,
@@ -393,6 +395,20 @@ def ce_score(batch: Batch, hidden, scorer: Scorer, logits, probs=None, stream=No
            "ce_score")
 
 
+def ce_score_ws(batch: Batch, hidden, scorer: Scorer, logits, ws, probs=None, stream=None):
+    """ce_score with a workspace (CE_WS_SCORE): the fused block's scorer,
+    rank-tiled where ce_score_tiling picks it."""
+    import torch
+    cb, sw = batch.c(), scorer.c()
+    T = batch.T
+    h = _hidden(hidden, "hidden", T, sw.d, _torch_dtype(sw.dtype) if sw.dtype in (0, 1) else None)
+    wp, wn = _ws_ptr(ws, ce_workspace_size(CE_WS_SCORE, batch, sw.d, 0, sw.dtype))
+    _check(lib.ce_score_ws(ctypes.byref(cb), h, ctypes.byref(sw),
+                           _chk(logits, "logits", torch.float32, numel=T),
+                           _chk(probs, "probs", torch.float32, numel=T, optional=True), wp, wn, _stream(stream)),
+           "ce_score_ws")
+
+
 def ce_topk_compact(batch: Batch, logits, kept_idx, kept_offsets, ws, token_pos=None,
                     hidden=None, compact=None, stream=None):
     import torch
@@ -669,10 +685,12 @@ def ce_routed_attention(q, k, v, o, q_offsets, kv_offsets, causal, scale, stream
 __all__ = [
     "Batch", "Scorer", "FFN", "CERouterError", "lib", "alloc_workspace",
     "ce_version", "ce_num_keep", "ce_kept_count_host", "ce_workspace_size", "ce_workspace_status",
-    "ce_score", "ce_topk_compact", "ce_topk_compact_noalloc", "ce_routed_ffn", "ce_routed_ffn_pruned", "ce_ffn_gateup", "ce_ffn_down",
+    "ce_score", "ce_score_ws", "ce_topk_compact", "ce_topk_compact_noalloc", "ce_routed_ffn",
+    "ce_routed_ffn_pruned", "ce_ffn_gateup", "ce_ffn_down",
     "ce_scatter_residual", "ce_routed_block", "ce_routed_block_gap", "ce_drop_stability",
     "ce_ffn_down_colnorms", "ce_ffn_saliency", "ce_ffn_mask_channels", "ce_layer_gap",
     "ce_routed_attention", "CEAttn",
-    "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK", "CE_WS_BLOCK_GAP", "CE_WS_FFN_PRUNED",
+    "CE_F32", "CE_BF16", "CE_TOK_GEN", "CE_TOK_KEEP", "CE_WS_TOPK", "CE_WS_FFN", "CE_WS_BLOCK", "CE_WS_BLOCK_GAP",
+    "CE_WS_FFN_PRUNED", "CE_WS_SCORE",
     "CE_DEV_BAD_OFFSETS", "CE_DEV_OVERFLOW",
 ]

@@ -332,6 +332,27 @@ int ce_score(const ce_batch* batch, const void* hidden, const ce_scorer_w* w, fl
   return hip_status(launch_score(a, w->dtype == CE_BF16, static_cast<hipStream_t>(stream)));
 }
 
+int ce_score_ws(const ce_batch* batch, const void* hidden, const ce_scorer_w* w, float* logits, float* probs,
+                void* ws, size_t ws_bytes, void* stream) {
+  CE_CHECK(check_batch(batch, w != nullptr && w->r_exp > 0));
+  CE_CHECK(check_scorer(w));
+  if (batch->T > 0 && (!hidden || !logits)) return CE_ERR_INVALID_ARG;
+  const int elem = elem_size(w->dtype);
+  const WsLayout L = ws_layout(CE_WS_SCORE, batch->B, batch->T, batch->kept_capacity, w->d, 0, elem);
+  CE_CHECK(check_ws(ws, ws_bytes, L.total));
+  if (batch->T == 0) return CE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ScoreArgs a = make_score_args(batch, hidden, w, logits, probs);
+  const bool bf16 = w->dtype == CE_BF16;
+  int tm = 0, tn = 0;
+  if (!(bf16 && score_tiling(batch->B, batch->T, w->d, w->r_core, w->r_exp, elem, &tm, &tn, &a.n_ct, &a.n_rt)))
+    return hip_status(launch_score(a, bf16, s));
+  a.part = at<float>(ws, L.score_part);
+  CE_TRY(launch_score_tiles(a, tm, tn, s));
+  CE_TRY(launch_score_assemble(a, s));
+  return CE_OK;
+}
+
 int ce_topk_compact(const ce_batch* batch, const float* logits, const void* hidden, int dtype,
                     int32_t d, int32_t* kept_idx, int32_t* kept_offsets, int32_t* token_pos,
                     void* compact, void* ws, size_t ws_bytes, void* stream) {

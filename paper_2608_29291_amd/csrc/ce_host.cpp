@@ -130,6 +130,7 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
   const bool block = which == CE_WS_BLOCK || which == CE_WS_BLOCK_GAP;
   L.status = take(16);
   if (which == CE_WS_TOPK || block) L.seq_info = take(3 * sB * 4);
+  if (which == CE_WS_SCORE) L.score_part = take((size_t)kScoreMaxTiles * sT * 4);
   if (block) {
     L.kept_off = take((sB + 1) * 4);
     L.kept_idx = take(sC * 4);
@@ -283,7 +284,7 @@ int64_t ce_kept_count_host(int32_t B, int32_t T, const int32_t* offs, const uint
 }
 
 size_t ce_workspace_size(int which, const ce_batch* batch, int32_t d, int32_t d_ff, int dtype) {
-  if (!batch || which < CE_WS_TOPK || which > CE_WS_FFN_PRUNED) return 0;
+  if (!batch || which < CE_WS_TOPK || which > CE_WS_SCORE) return 0;
   const int elem = ce::elem_size(dtype);
   if (!elem) return 0;
   return ce::ws_layout(which, batch->B, batch->T, batch->kept_capacity, d, d_ff, elem).total;

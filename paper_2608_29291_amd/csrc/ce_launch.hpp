@@ -123,6 +123,9 @@ hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream);
 // Rank-tiled scorer (bf16): tiles of tm tokens x tn ranks (tm, tn in {64, 128})
 // write per-token partial logits to a.part; the TopK step adds them up.
 hipError_t launch_score_tiles(const ScoreArgs& a, int tm, int tn, hipStream_t stream);
+// Logits (and probs) from a.part in the TopK step's order (the staged
+// rank-tiled path).
+hipError_t launch_score_assemble(const ScoreArgs& a, hipStream_t stream);
 
 // Per-sequence summary written by the count kernel: {lo, len, keep_count | bad<<31}.
 hipError_t launch_seq_info(const int32_t* seq_offsets, const uint8_t* flags, int B, int T,

@@ -192,9 +192,11 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   asm volatile("" : "+s"(ring));
   // Each tile walks K starting from its own slab, so the workgroups running
   // at the same time fetch different weight lines instead of all hitting the
-  // same L2 lines (the sum order is fixed per tile).
+  // same L2 lines. The start follows the tile's index, not the workgroup's,
+  // so the sum order is fixed per tile whether or not the launch has the
+  // summary workgroups in front.
   const int nk_all = a.k_bytes / kSlabRow;
-  const int rot = (int)(blockIdx.x % (unsigned)nk_all);
+  const int rot = (int)((unsigned)tile % (unsigned)nk_all);
   auto dma = [&](int kb, int buf) __attribute__((always_inline)) {
     lds_char* st = ring + buf * stage;
     int ks = kb + rot;
@@ -475,10 +477,11 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
   lds_char* ring = (lds_char*)smem;
   asm volatile("" : "+s"(ring));
   const int nk = a.k_bytes / kSlabRow;
-  // each workgroup walks K from its own slab, so the workgroups running at
+  // each work item walks K from its own slab, so the workgroups running at
   // the same time read different lines instead of the same slab column of
-  // every row (the sum order is fixed per workgroup)
-  const int rot = (int)(blockIdx.x % (unsigned)nk);
+  // every row (the sum order is fixed per item, with or without the summary
+  // workgroups in front of the launch)
+  const int rot = (int)((unsigned)item % (unsigned)nk);
   auto slab_off = [&](int k) __attribute__((always_inline)) {
     int ks = k + rot;
     ks = ks >= nk ? ks - nk : ks;
@@ -594,6 +597,53 @@ hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream) {
     hipLaunchKernelGGL((score_kernel<true, 32>), dim3(tiles), dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL((score_kernel<false, 32>), dim3(tiles), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+// Logits (Eq. 4) and scores (Eq. 6) from the rank-tiled scorer's partial
+// sums, added in the order the TopK step of the fused block adds them (core
+// tiles, b2_core, then for generation tokens the expansion tiles plus
+// b2_exp[m]), so both paths give the same logits bit for bit. Workgroup
+// (x, b): the tokens of sequence b, strided over gridDim.x workgroups.
+__global__ __launch_bounds__(256) void score_assemble_kernel(ScoreArgs a) {
+  const int b = blockIdx.y;
+  int lo = a.seq_offsets[b], hi = a.seq_offsets[b + 1];
+  lo = lo < 0 ? 0 : (lo > a.T ? a.T : lo);
+  hi = hi < lo ? lo : (hi > a.T ? a.T : hi);
+  float b2e_m = 0.0f;
+  if (a.r_exp > 0 && a.b2e) {
+    const double mf = floor((double)a.n_seg * (double)a.t[b]);
+    const int m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
+    b2e_m = a.b2e[m];
+  }
+  const bool has_exp = a.r_exp > 0 && a.n_rt > a.n_ct;
+  for (int i = lo + blockIdx.x * 256 + (int)threadIdx.x; i < hi; i += gridDim.x * 256) {
+    const uint8_t f = a.flags[i];
+    float l;
+    if (f & CE_TOK_KEEP) {
+      l = __builtin_inff();
+    } else {
+      const float* pp = a.part + i;
+      l = pp[0];
+      for (int q = 1; q < a.n_ct; ++q) l += pp[(int64_t)q * a.T];
+      l += a.b2c;
+      if ((f & CE_TOK_GEN) && has_exp) {
+        float e = pp[(int64_t)a.n_ct * a.T];
+        for (int q = a.n_ct + 1; q < a.n_rt; ++q) e += pp[(int64_t)q * a.T];
+        l += e + b2e_m;
+      }
+    }
+    a.logits[i] = l;
+    if (a.probs) a.probs[i] = (f & CE_TOK_KEEP) ? 1.0f : 1.0f / (1.0f + expf(-l));
+  }
+}
+
+hipError_t launch_score_assemble(const ScoreArgs& a, hipStream_t stream) {
+  if (!a.part || a.n_rt <= 0 || a.B <= 0) return hipErrorInvalidValue;
+  // about one workgroup per 256 tokens of an average sequence, at most 64
+  int gx = (int)(((int64_t)a.T + (int64_t)a.B * 256 - 1) / ((int64_t)a.B * 256));
+  gx = gx < 1 ? 1 : (gx > 64 ? 64 : gx);
+  hipLaunchKernelGGL(score_assemble_kernel, dim3(gx, a.B), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 23
+    assert len(names) == 24
     for n in names:
         assert hasattr(ce.lib, n), n
     assert set(names) == set(ce.EXPORTED)
@@ -112,6 +112,28 @@ def score(b, w, hidden=FAKE, logits=FAKE):
 def test_score_validation(mut, code):
     b, w = mut(_batch(), _scorer())
     assert score(b, w) == code
+
+
+def score_ws(b, w, hidden=FAKE, logits=FAKE, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = ce.lib.ce_workspace_size(ce.CE_WS_SCORE, ctypes.byref(b), 256, 0, ce.CE_BF16) if b else 0
+    return ce.lib.ce_score_ws(ctypes.byref(b) if b is not None else None, hidden,
+                              ctypes.byref(w) if w is not None else None, logits, None, ws, ws_bytes, None)
+
+
+def test_score_ws_validation():
+    """ce_score_ws: the scorer checks of ce_score, then the workspace (10
+    fp32 partial logits per token, whatever the scorer picks)."""
+    b, w = _batch(T=1000), _scorer()
+    need = ce.lib.ce_workspace_size(ce.CE_WS_SCORE, ctypes.byref(b), 256, 0, ce.CE_BF16)
+    assert need >= 10 * 1000 * 4
+    assert score_ws(None, w) == ce.CE_ERR_INVALID_ARG
+    assert score_ws(b, None) == ce.CE_ERR_INVALID_ARG
+    assert score_ws(b, _scorer(d=100)) == ce.CE_ERR_UNSUPPORTED
+    assert score_ws(b, w, logits=None) == ce.CE_ERR_INVALID_ARG
+    assert score_ws(b, w, hidden=None) == ce.CE_ERR_INVALID_ARG
+    assert score_ws(b, w, ws=None) == ce.CE_ERR_WORKSPACE
+    assert score_ws(b, w, ws_bytes=need - 1) == ce.CE_ERR_WORKSPACE
 
 
 def test_score_null_buffers():

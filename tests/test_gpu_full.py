@@ -3,7 +3,8 @@ the benchmark times (ce_routed_block, in place, capacity = exact Kt).
 
 Nothing is sampled. For every workload (workload 3: each of its 50 denoising
 steps) the test checks
-  * every logit against the oracle's (Eq. 4), float64 on the same inputs;
+  * every logit against the oracle's (Eq. 4), float64 on the same inputs,
+    and ce_score_ws's logits bit for bit equal to the block's;
   * the whole selection (Eq. 6): the oracle's TopK run on the GPU's own
     logits gives the GPU's kept_idx / kept_offsets bit for bit, and against
     the oracle's own logits only tokens within 4 eps of their sequence's
@@ -51,6 +52,13 @@ def run_full(G, wl, check_outputs=True, dw=None):
     kidx, koff = G.host(kept_idx), G.host(kept_off)
     y = G.host(h)
     del h
+
+    # the staged scorer with a workspace gives the block's logits bit for bit
+    lw = torch.full((wl.T,), float("nan"), device="cuda")
+    ce.ce_score_ws(dw.batch, dw.hidden, dw.scorer, lw, dw.ws(ce.CE_WS_SCORE))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(G.host(lw), lg)
+    del lw
 
     # every logit (Eq. 4)
     l64, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)

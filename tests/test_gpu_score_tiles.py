@@ -119,3 +119,56 @@ def test_tiled_scorer_register_limit(GU):
     for k in ("y", "logits", "kidx", "koff"):
         np.testing.assert_array_equal(r[k], r2[k])
     print(f"[tiles 16k] out err {err:.2e} swaps {swaps}", flush=True)
+
+
+@pytest.mark.parametrize("case", [*CASES, "long", "tok128", "b4"])
+def test_score_ws(GU, case):
+    """ce_score_ws, the staged form of the block's scorer: rank-tiled where
+    ce_score_tiling picks it, its logits bit for bit those of the fused block
+    (same partial sums, added in the TopK step's order), within the logit bar
+    of the oracle, scores within 1e-4 of the oracle's sigmoid, +inf / 1 for
+    always-kept tokens; where the single-launch scorer is picked, bit for bit
+    ce_score and the block."""
+    import torch
+    import oracle
+    import paper_2608_29291_amd as ce
+    from oracle.score import sigmoid
+    if case == "long":
+        wl = make_workload("ws-long", [[(9000, G), (300, K), (7700, U)]], d=64, F=64, r_c=384, r_e=96,
+                           keep=0.3, dtype="bf16", seed=5, biases=True)
+    elif case == "b4":
+        # 4 sequences and 6 K slabs: the block's launch puts 4 summary
+        # workgroups in front, which must not change any tile's sum order
+        wl = make_workload("ws-b4", mixed_layout(4224, 4, 9), d=384, F=64, r_c=384, r_e=96, keep=0.4,
+                           dtype="bf16", seed=9, biases=True)
+    elif case == "tok128":
+        wl = make_workload("ws-tok128", mixed_layout(8320, 4, 77), d=128, F=64, r_c=32, r_e=64, keep=0.4,
+                           dtype="bf16", seed=77, biases=True)
+    else:
+        tile, T, r_c, r_e = case
+        wl = make_workload(f"ws-{tile[0]}x{tile[1]}", mixed_layout(T, 3, sum(tile)), d=192, F=128,
+                           r_c=r_c, r_e=r_e, keep=0.45, dtype="bf16", seed=tile[0] + tile[1], biases=True)
+    dw = GU.DevWorkload(wl)
+    tiling = ce.ce_score_tiling(dw.batch, dw.scorer)
+    ws = dw.ws(ce.CE_WS_SCORE)
+    logits = torch.full((wl.T,), float("nan"), device="cuda")
+    probs = torch.full((wl.T,), float("nan"), device="cuda")
+    ce.ce_score_ws(dw.batch, dw.hidden, dw.scorer, logits, ws, probs=probs)
+    torch.cuda.synchronize()
+    lg, pg = GU.host(logits), GU.host(probs)
+    l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    keep = (wl.flags & K) != 0
+    assert np.all(np.isposinf(lg[keep])) and np.all(pg[keep] == 1.0)
+    eps = GU.logit_err(lg, l64)
+    assert eps <= GU.LOGIT_TOL["bf16"], eps
+    assert np.max(np.abs(pg[~keep] - sigmoid(l64[~keep]))) <= 1e-4
+    if tiling[1] > 0:
+        r = GU.run_block(wl)
+        np.testing.assert_array_equal(lg, r["logits"])
+    else:
+        ref = torch.full((wl.T,), float("nan"), device="cuda")
+        ce.ce_score(dw.batch, dw.hidden, dw.scorer, ref)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(lg, GU.host(ref))
+        np.testing.assert_array_equal(lg, GU.run_block(wl)["logits"])
+    print(f"[score_ws {tiling}] T={wl.T} logit err {eps:.2e}", flush=True)
