@@ -145,41 +145,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int r = 16 * wave + 4 * i + kr_sub;
     kvo[i] = (uint32_t)((int64_t)klo * kv_row + (int64_t)kvh * kKRow + (int64_t)r * kv_row + ((kpc ^ (r & 15)) << 4));
   }
+  // Keys of a ragged last tile past the sequence's end are fetched as they
+  // are (the next sequence's rows, or zeros past the buffer): every score of
+  // a key at or past n_kv is replaced by -inf before the softmax reads it.
   auto dma_k = [&](int tile, int buf) __attribute__((always_inline)) {
     char* region = kbuf + buf * kKBytes + 16 * wave * kKRow;
-    const bool full = (tile + 1) * kKT <= nk;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      uint32_t voff = kvo[i];
-      int soff = (int)(tile * tile_bytes);
-      if (!full) {  // ragged last tile: clamp the key to the last one
-        const int r = 16 * wave + 4 * i + kr_sub;
-        const int key = min(tile * kKT + r, nk - 1);
-        voff = (uint32_t)((int64_t)(klo + key) * kv_row + (int64_t)kvh * kKRow + ((kpc ^ (r & 15)) << 4));
-        soff = 0;
-      }
+    for (int i = 0; i < 4; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (__attribute__((address_space(3))) void*)(region + 4 * i * kKRow),
-                                               16, (int)voff, soff, 0, 0);
-    }
+                                               16, (int)kvo[i], (int)(tile * tile_bytes), 0, 0);
   };
   // ---- V tile: thread (kg = tid % 16, dg = tid / 16) loads keys 4 kg .. +3 of
   //      dims 8 dg .. +7 and writes them transposed (one byte permute per
   //      output dword) ----
   const int vkg = tid & 15;
   const int vdg = tid >> 4;
-  const char* vsrc = a.v + (int64_t)(klo + 4 * vkg) * kv_row + (int64_t)kvh * kKRow + vdg * 16;
+  // keys of a ragged last tile past the sequence's end read its last key
+  // instead (finite values: their probabilities are 0, and 0 * NaN is not)
+  const char* vsrc = a.v + (int64_t)klo * kv_row + (int64_t)kvh * kKRow + vdg * 16;
   u32x4_t vreg[4];
   auto load_v = [&](int tile) __attribute__((always_inline)) {
-    const bool full = (tile + 1) * kKT <= nk;
+    const int k0 = tile * kKT + 4 * vkg;
+    const int kmax = nk - 1;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const char* p = vsrc + tile * tile_bytes + i * kv_row;
-      if (!full) {
-        const int key = min(tile * kKT + 4 * vkg + i, nk - 1);
-        p = a.v + (int64_t)(klo + key) * kv_row + (int64_t)kvh * kKRow + vdg * 16;
-      }
-      vreg[i] = *reinterpret_cast<const u32x4_t*>(p);
-    }
+    for (int i = 0; i < 4; ++i)
+      vreg[i] = *reinterpret_cast<const u32x4_t*>(vsrc + (int64_t)min(k0 + i, kmax) * kv_row);
   };
   // odd dim groups take the dims of each pair in the other order, so one
   // instruction writes rows of both parities
