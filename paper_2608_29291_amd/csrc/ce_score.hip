@@ -92,6 +92,155 @@ __device__ __forceinline__ void find_tile(const ScoreArgs& a, int tile, int* sh,
   }
 }
 
+// Exclusive prefix sum over the 256 threads of a workgroup (4 waves), plus
+// the total; scr: 4 ints of LDS. Every thread must call it.
+__device__ __forceinline__ int block_excl_scan(int v, int* scr, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) scr[wave] = x;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += scr[w];
+  total = (scr[0] + scr[1]) + (scr[2] + scr[3]);
+  __syncthreads();  // scr is free again
+  return before + x - v;
+}
+
+// The rank-tiled scorer's live work items. A token tile (kTile tokens of one
+// sequence, sequences tiled in order) holds n_ct core items if any of its
+// tokens is scored (not always-kept) and n_rt - n_ct expansion items if any
+// scored token is a generation token; the other items have nothing to do.
+// Live items are numbered tile by tile, core before expansion; the grid slot
+// `slot` takes live item w = (slot % 8) * ceil(n_live / 8) + slot / 8, so each
+// XCD (workgroup L runs on XCD L % 8) gets a contiguous range. Returns w and
+// the item (sequence b, tokens [lo, hi), rank tile q), or b = -1.
+// Every thread walks the same tiles: sequences 256 at a time (tile counts and
+// their prefix sums in LDS), their tiles 256 at a time (thread per tile: its
+// sequence by binary search, its flags by 16-byte loads all issued at once),
+// live counts by a prefix sum. When the tiles fit one such round (the usual
+// case) the item is found from the registers of that round; otherwise a
+// second walk finds it. scr: LDS of at least 3 * 257 + 8 ints.
+template <int kTile>
+__device__ void live_item(const ScoreArgs& a, int slot, int* scr, int& w, int& b, int& lo, int& hi, int& q) {
+  const int tid = threadIdx.x;
+  int* const t0s = scr;          // [257] first tile of each sequence of the chunk (chunk-relative)
+  int* const los = scr + 257;    // [257] clamped start of each sequence
+  int* const his = scr + 514;    // [257] clamped end
+  int* const res = scr + 771;    // [4] the wanted item
+  int* const sc4 = scr + 775;    // [4] scan scratch
+  const __amdgpu_buffer_rsrc_t frs = make_rsrc(a.flags, (uint32_t)a.T);
+  const int n_exp = a.n_rt - a.n_ct;
+  constexpr int kChunks = kTile / 16 + 1;  // 16-byte flag chunks a tile can touch
+  int live = 0, lex = 0, tlo = 0, thi = 0, jg = 0, rounds = 0;
+  // one round of a walk: tiles tb .. tb + 255 of sequence chunk s0
+  auto tile_round = [&](int s0, int cnt, int ctiles, int tb) __attribute__((always_inline)) {
+    const int t = tb + tid;
+    live = 0;
+    tlo = thi = 0;
+    jg = 0;
+    if (t < ctiles) {
+      // sequence of tile t: the last j with t0s[j] <= t
+      int l = 0, h = cnt;  // answer in [l, h)
+      while (h - l > 1) {
+        const int mid = (l + h) >> 1;
+        if (t0s[mid] <= t) l = mid;
+        else h = mid;
+      }
+      jg = s0 + l;
+      tlo = los[l] + (t - t0s[l]) * kTile;
+      thi = min(tlo + kTile, his[l]);
+    }
+    const int c0 = tlo & ~15;
+    u32x4_t v[kChunks];
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) v[i] = bload16(frs, (uint32_t)(c0 + 16 * i), 0);  // past T: zeros
+    // KEEP is bit 1, GEN bit 0 of each flag byte
+    uint32_t scored = 0, gscored = 0;
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint32_t valid = 0;
+#pragma unroll
+        for (int y = 0; y < 4; ++y) {
+          const int idx = c0 + 16 * i + 4 * e + y;
+          valid |= (idx >= tlo && idx < thi) ? (0xffu << (8 * y)) : 0u;
+        }
+        const uint32_t nk = ~v[i][e] & valid;  // bit 1 of a byte: not always-kept
+        scored |= nk & 0x02020202u;
+        gscored |= v[i][e] & (nk >> 1) & 0x01010101u;
+      }
+    live = scored ? a.n_ct + (gscored ? n_exp : 0) : 0;
+  };
+  // want < 0: count only; else also record live item `want`
+  auto walk = [&](int want) __attribute__((always_inline)) {
+    int total = 0;
+    rounds = 0;
+    for (int s0 = 0; s0 < a.B; s0 += 256) {
+      const int cnt = min(256, a.B - s0);
+      int nt = 0;
+      if (tid < cnt) {
+        int l0 = a.seq_offsets[s0 + tid], l1 = a.seq_offsets[s0 + tid + 1];
+        l0 = l0 < 0 ? 0 : (l0 > a.T ? a.T : l0);
+        l1 = l1 < l0 ? l0 : (l1 > a.T ? a.T : l1);
+        los[tid] = l0;
+        his[tid] = l1;
+        nt = (l1 - l0 + kTile - 1) / kTile;
+      }
+      int ctiles;
+      const int ex = block_excl_scan(nt, sc4, ctiles);
+      if (tid < cnt) t0s[tid] = ex;
+      if (tid == 0) t0s[cnt] = ctiles;
+      __syncthreads();
+      for (int tb = 0; tb < ctiles; tb += 256) {
+        tile_round(s0, cnt, ctiles, tb);
+        int ltotal;
+        lex = total + block_excl_scan(live, sc4, ltotal);
+        if (want >= 0 && live > 0 && want >= lex && want < lex + live) {
+          res[0] = jg;
+          res[1] = tlo;
+          res[2] = thi;
+          res[3] = want - lex;  // core items first, then the expansion items
+        }
+        total += ltotal;
+        ++rounds;
+      }
+      __syncthreads();  // the chunk's arrays are refilled by the next chunk
+    }
+    return total;
+  };
+  if (tid == 0) res[0] = -1;
+  const int n_live = walk(-1);
+  const int per = (n_live + 7) / 8;
+  w = (slot & 7) * per + (slot >> 3);
+  if ((slot >> 3) >= per || w >= n_live) {  // the grid is sized for every item: the rest exit
+    b = -1;
+    return;
+  }
+  if (rounds == 1) {
+    // the registers of the only round still describe every tile
+    if (live > 0 && w >= lex && w < lex + live) {
+      res[0] = jg;
+      res[1] = tlo;
+      res[2] = thi;
+      res[3] = w - lex;
+    }
+  } else {
+    walk(w);
+  }
+  __syncthreads();
+  b = res[0];
+  lo = res[1];
+  hi = res[2];
+  q = res[3];
+  __syncthreads();
+}
+
 template <bool kBF16, int kTM>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   static_assert(kTM == 32 || kTM == 128, "token tiles of 32 or 128");
@@ -402,20 +551,22 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
     }
     item -= a.B;
   }
-  // XCD-aware order: the rank tiles of a token tile run next to each other
-  // on one XCD (workgroup L runs on XCD L % 8), so the token rows are read
-  // from HBM once and from that XCD's L2 after
-  const int total = (a.T / TM + a.B) * a.n_rt;  // >= the number of (token tile, rank tile) items
-  const int per = (total + 7) / 8;
-  const int w = (item & 7) * per + (item >> 3);
-  if (w >= total) return;
-  const int tile = w / a.n_rt;
-  const int q = w - tile * a.n_rt;
-  int b, lo, hi;
-  find_tile<TM>(a, tile, sh, b, lo, hi);
+  // Only live items get a workgroup (expansion items of tiles without a
+  // generation token, and tiles of always-kept tokens only, have nothing to
+  // do), so the grid's first round of 256 is not spent on them while live
+  // items wait for a second. XCD-aware order: live items are numbered tile by
+  // tile and each XCD (workgroup L runs on XCD L % 8) takes a contiguous
+  // range, so the rank tiles of a token tile run next to each other on one
+  // XCD and its token rows are read from HBM once and from that XCD's L2
+  // after. The ring's LDS is the scratch of the walk.
+  int* const scr = reinterpret_cast<int*>(smem);
+  int w, b, lo, hi, q;
+  live_item<TM>(a, item, scr, w, b, lo, hi, q);
+  if (b < 0) return;  // the whole workgroup: b is the same in every thread
   b = __builtin_amdgcn_readfirstlane(b);
   lo = __builtin_amdgcn_readfirstlane(lo);
   hi = __builtin_amdgcn_readfirstlane(hi);
+  q = __builtin_amdgcn_readfirstlane(q);
   if (b < 0) return;
   const int n = hi - lo;
 
@@ -481,7 +632,7 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
   // the same time read different lines instead of the same slab column of
   // every row (the sum order is fixed per item, with or without the summary
   // workgroups in front of the launch)
-  const int rot = (int)((unsigned)item % (unsigned)nk);
+  const int rot = (int)((unsigned)w % (unsigned)nk);
   auto slab_off = [&](int k) __attribute__((always_inline)) {
     int ks = k + rot;
     ks = ks >= nk ? ks - nk : ks;
