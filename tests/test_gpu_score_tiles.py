@@ -172,3 +172,32 @@ def test_score_ws(GU, case):
         np.testing.assert_array_equal(lg, GU.host(ref))
         np.testing.assert_array_equal(lg, GU.run_block(wl)["logits"])
     print(f"[score_ws {tiling}] T={wl.T} logit err {eps:.2e}", flush=True)
+
+
+@pytest.mark.parametrize("case", ["300seq", "313tiles"])
+def test_tiled_scorer_many_tiles(GU, case):
+    """The live-item walk over more than one round: 300 ragged sequences (two
+    chunks of 256 sequences) and 40000 tokens in two sequences (more than 256
+    token tiles). Block against the oracle, ce_score_ws equal to the block's
+    logits bit for bit, run to run bitwise."""
+    import torch
+    import paper_2608_29291_amd as ce
+    if case == "300seq":
+        layout = mixed_layout(36000, 300, 3)
+    else:
+        layout = [[(9000, G), (3000, K), (8000, U)], [(20000, G)]]
+    wl = make_workload(f"walk-{case}", layout, d=64, F=64, r_c=384, r_e=96, keep=0.4, dtype="bf16", seed=31,
+                       biases=True)
+    dw = GU.DevWorkload(wl)
+    assert ce.ce_score_tiling(dw.batch, dw.scorer) == (128, 128)
+    print(f"[walk {case}] B={wl.B} T={wl.T}", flush=True)
+    r = GU.run_block(wl)
+    err, swaps = GU.check_block(wl, r)
+    r2 = GU.run_block(wl)
+    for k in ("y", "logits", "kidx", "koff"):
+        np.testing.assert_array_equal(r[k], r2[k])
+    lw = torch.full((wl.T,), float("nan"), device="cuda")
+    ce.ce_score_ws(dw.batch, dw.hidden, dw.scorer, lw, dw.ws(ce.CE_WS_SCORE))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(GU.host(lw), r["logits"])
+    print(f"[walk {case}] out err {err:.2e} swaps {swaps}", flush=True)
