@@ -698,16 +698,32 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
         fb[step][j] = *reinterpret_cast<const u32x4_t*>(sb + (32 * (wk * MBW + j) + lrow) * kSlabRow + off);
     }
     // every wave is past slab k - 1 (the barrier above): its stages receive
-    // token slab k + kTokRing - 1 and rank slab k + kRankRing - 1
-    dma_r(k + kRankRing - 1, rst == 0 ? kRankRing - 1 : rst - 1);
-    dma_t(k + kTokRing - 1, tst == 0 ? kTokRing - 1 : tst - 1);
+    // rank slab k + kRankRing - 1 and token slab k + kTokRing - 1, in that
+    // order. The wave issues in order, and a DMA instruction waits while the
+    // memory pipe's queue is full: issued all at once they held back the
+    // MFMAs behind them (each slab cost its DMA issue plus its MFMAs), so
+    // they go out one at a time between the MFMAs.
+    const int rso = slab_off(k + kRankRing - 1), tso = slab_off(k + kTokRing - 1);
+    const int rnext = rst == 0 ? kRankRing - 1 : rst - 1, tnext = tst == 0 ? kTokRing - 1 : tst - 1;
     __builtin_amdgcn_sched_barrier(0);
+    constexpr int kM = 4 * NBW * MBW;  // MFMAs of the slab
 #pragma unroll
-    for (int step = 0; step < 4; ++step)
+    for (int mi = 0; mi < kM; ++mi) {
+      const int step = mi / (NBW * MBW), i = (mi / MBW) % NBW, j = mi % MBW;
+      mfma_step<true>(acc[i][j][kTwoAcc ? (step & 1) : 0], fa[step][i], fb[step][j]);
+      // DMA instructions (IR + IT) * mi / kM .. (IR + IT) * (mi + 1) / kM: rank first
 #pragma unroll
-      for (int i = 0; i < NBW; ++i)
-#pragma unroll
-        for (int j = 0; j < MBW; ++j) mfma_step<true>(acc[i][j][kTwoAcc ? (step & 1) : 0], fa[step][i], fb[step][j]);
+      for (int x = (IR + IT) * mi / kM; x < (IR + IT) * (mi + 1) / kM; ++x) {
+        if (x < IR) {
+          lds_char* dst = ring + kTokRing * kTokB + rnext * kRankB + (32 * x + 8 * wave) * kSlabRow;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, dst, 16, (int)rvo[x], rso, 0, 0);
+        } else {
+          lds_char* dst = ring + tnext * kTokB + (32 * (x - IR) + 8 * wave) * kSlabRow;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(trs, dst, 16, (int)tvo[x - IR], tso, 0, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     tst = tst + 1 == kTokRing ? 0 : tst + 1;
     rst = rst + 1 == kRankRing ? 0 : rst + 1;
   }
