@@ -1,21 +1,26 @@
 """CE-Router routed block on MI355X (gfx950): thin Python binding of libce_router.so.
 
-The five calls below have the names and arguments of the C ABI in
-include/ce_router.h; this module only marshals torch tensors (device memory)
-and the current HIP stream into pointers. Every step of the routed block runs
-in the library's HIP kernels; there is no Python or CPU fallback. Importing
-this package fails loudly when the library has not been built.
+The calls below have the names and arguments of the C ABI in
+include/ce_router.h; this module only checks and marshals torch tensors
+(device memory) and the current HIP stream into pointers. Every step of the
+routed block runs in the library's HIP kernels; there is no Python or CPU
+fallback. Importing this package fails loudly when the library has not been
+built.
 
-    ce_score             routing logits (Eq. 4) [+ sigmoid scores, Eq. 6]
-    ce_topk_compact      per-sequence TopK (Eq. 6) + packed index maps [+ gather]
-    ce_routed_ffn        SwiGLU FFN on the packed rows
-    ce_scatter_residual  residual merge; dropped rows bypass
-    ce_routed_block      all of the above, fused
-    ce_drop_stability    drop-set Jaccard / RDA between two timesteps (Eq. 10-11)
+    ce_score, ce_score_ws  routing logits (Eq. 4) [+ sigmoid scores, Eq. 6];
+                           ce_score_ws with a workspace runs the fused block's scorer
+    ce_topk_compact        per-sequence TopK (Eq. 6) + packed index maps [+ gather]
+    ce_topk_compact_noalloc  the same without a workspace (a fixed device array)
+    ce_routed_ffn          SwiGLU FFN on the packed rows (ce_ffn_gateup + ce_ffn_down)
+    ce_routed_ffn_pruned   the FFN with the pruning choice (Eq. 8-9) fused in
+    ce_scatter_residual    residual merge; dropped rows bypass
+    ce_routed_block        all of the above, fused; ce_routed_block_gap adds the
+                           layer-skipping gap (Eq. 7) from the down GEMM's epilogue
+    ce_drop_stability      drop-set Jaccard / RDA between two timesteps (Eq. 10-11)
     ce_ffn_down_colnorms, ce_ffn_saliency, ce_ffn_mask_channels
-                         FFN-pruning saliency / leakage on the retained rows (Eq. 8-9)
-    ce_layer_gap         layer-skipping redundancy gap of input/output cosines (Eq. 7)
-    ce_routed_attention  attention over the packed retained tokens (compressed KV cache)
+                           FFN-pruning saliency / leakage on the retained rows (Eq. 8-9)
+    ce_layer_gap           layer-skipping redundancy gap of input/output cosines (Eq. 7)
+    ce_routed_attention    attention over the packed retained tokens (compressed KV cache)
 """
 from __future__ import annotations
 
