@@ -578,16 +578,23 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   // superslabs [s0, ns) of K: all of them, or this piece's range when the
   // tile is split (>= 3 per range, checked by the launcher)
   const int ns_all = a.k_bytes / kRow;
-  const int s0 = ns_all * piece / pieces;
+  int s0 = ns_all * piece / pieces;
   int ns = ns_all * (piece + 1) / pieces;
   // each ring starts with all but one of its slots in flight; the first
   // superslab must have landed
   constexpr int kBufs0 = kWBufs;  // waves 0-3 (weights)
   constexpr int kBufs1 = kTBufs;  // waves 4-7 (tokens)
-  // the pruning choice is needed before the first DMAs only when they reach
-  // the superslabs of P; otherwise its loads overlap theirs
-  const bool resolve_first = kPrune && s0 + kBufs1 - 1 > a.ns_keep;
+  // the pruning choice is needed before the first DMAs when they reach the
+  // superslabs of P, or when the tile is split (its K pieces may move);
+  // otherwise its loads overlap theirs
+  const bool resolve_first = kPrune && (pieces > 1 || s0 + kBufs1 - 1 > a.ns_keep);
   if (resolve_first) resolve_pruned();
+  // a split tile of pruned rows: its K pieces share the superslabs before P
+  // (at least 3 each), so every piece does less work, not only the last
+  if (kPrune && pieces > 1 && tile_pruned && a.ns_keep < ns_all && a.ns_keep >= 3 * pieces) {
+    s0 = a.ns_keep * piece / pieces;
+    ns = a.ns_keep * (piece + 1) / pieces;
+  }
   using T2 = std::integral_constant<int, kPrune ? 2 : 0>;
   if (is_w) {
 #pragma unroll
@@ -597,9 +604,14 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     for (int q = 0; q < kBufs1 - 1; ++q) dma(s0 + q, q, I0{}, T2{});
   }
   if (kPrune && !resolve_first) resolve_pruned();
-  // a whole tile of pruned rows skips the superslabs of P (they would only
-  // multiply zeros); K pieces keep their range and read zeros there
-  if (kPrune && pieces == 1 && tile_pruned && a.ns_keep >= 3 && a.ns_keep < ns) ns = a.ns_keep;
+  // a tile of pruned rows skips the superslabs of P (they would only
+  // multiply zeros): a whole tile or a K piece stops at ns_keep (keeping at
+  // least 3 superslabs, else it reads zeros there), and a K piece wholly in P
+  // runs no superslab and hands in zero partial sums
+  if (kPrune && tile_pruned && a.ns_keep < ns) {
+    if (pieces > 1 && a.ns_keep <= s0) ns = s0;
+    else if (a.ns_keep - s0 >= 3) ns = a.ns_keep;
+  }
   if (is_w) wait_vmcnt<8 * (kBufs0 - 2)>();
   else wait_vmcnt<8 * (kBufs1 - 2)>();
   lds_barrier();  // superslab 0 is in LDS

@@ -188,9 +188,10 @@ def test_routed_ffn_pruned(G, kind, d, F, mode):
     """ce_routed_ffn_pruned (P = the channel tail [n_keep, d_ff), about 30%):
     saliency and leakage from the gate/up epilogue's segment sums against the
     oracle on the same activations, the decisions where the leakage is clear
-    of delta, and ffn_out bit for bit equal to ce_ffn_mask_channels +
-    ce_ffn_down on those decisions (zeros read instead of P, and whole pruned
-    tiles stopping at n_keep, change no sum) and within the FFN bar of the
+    of delta, and ffn_out equal to ce_ffn_mask_channels + ce_ffn_down on
+    those decisions (zeros read instead of P, and whole pruned tiles stopping
+    at n_keep, change no sum; split tiles of pruned rows, whose K pieces share
+    the superslabs before P, may differ in the last bit) and within the FFN bar of the
     oracle's pruned / full FFN. Shapes with split tail tiles in both GEMMs
     (512 / 2048, 2048 / 1024), MoT groups, and delta so that some, all or no
     sequences run pruned; 41 short sequences for the segment-slot fallback."""
@@ -247,7 +248,15 @@ def test_routed_ffn_pruned(G, kind, d, F, mode):
     ce.ce_ffn_down(dw.batch, act, kidx, koff, dw.ffn, out2, ws_f)
     torch.cuda.synchronize()
     f = G.host(out)[:kt]
-    np.testing.assert_array_equal(f, G.host(out2)[:kt])
+    f2 = G.host(out2)[:kt]
+    # bit for bit, except where a split tile whose rows all run pruned shares
+    # the superslabs before P among its K pieces (another order of the same
+    # fp32 sums): there a bf16 output may round the other way, by at most a
+    # unit in the last place of the largest outputs (cancellation makes small
+    # outputs differ more relative to themselves)
+    assert np.max(np.abs(f - f2)) <= 2.0 ** -7 * np.max(np.abs(f2)), np.max(np.abs(f - f2))
+    if mode == "none":
+        np.testing.assert_array_equal(f, f2)
     zm = uf.masked_activations(z, row_seq, mask, use_g)
     ref_out = np.zeros((kt, wl.d))
     for j, tok in enumerate(kept_idx):
