@@ -455,23 +455,23 @@ int ce_routed_ffn_pruned(const ce_batch* batch, const void* compact, const int32
   dn.ns_keep = n_keep * 2 / 128;
   if (batch->kept_capacity > 0 && !ffn_pruned_ok(g, dn)) return CE_ERR_UNSUPPORTED;
   float* chunk_tot = at<float>(ws, L.sal_part) + (size_t)kSalSplits * batch->B * w->d_ff;
+  int32_t* seq_cnt = at<int32_t>(ws, L.seq_cnt);
+  CE_TRY(launch_row_seq(kept_offsets, batch->B, batch->kept_capacity, row_seq, seq_cnt, s));
   if (batch->kept_capacity == 0) {
     // no rows: zero saliency, leakage 0 (the pruned FFN runs, on nothing)
-    FfnGemmArgs none = g;
-    return hip_status(launch_saliency_segments(none, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot,
-                                               saliency, leakage, use_pruned, nullptr, s));
+    return hip_status(launch_saliency_segments(g, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot,
+                                               saliency, leakage, use_pruned, row_flag, seq_cnt, s));
   }
   if (w->n_sets == 2)
     CE_TRY(launch_group(kept_idx, kept_offsets, batch->B, batch->kept_capacity, batch->T, batch->flags, grp, n0,
                         s));
-  CE_TRY(launch_row_seq(kept_offsets, batch->B, batch->kept_capacity, row_seq, s));
   g.clear_n = ffn_split_counters(dn, 1, true);
   g.clear_cnt = g.clear_n > 0 ? dn.tile_cnt : nullptr;
   // 1. gate/up + SwiGLU, with the per-segment |z| sums
   CE_TRY(launch_ffn_gateup(g, true, s));
   // 2. saliency (Eq. 8), leakage (Eq. 9) and the pruned/full choice per sequence
   CE_TRY(launch_saliency_segments(g, kept_offsets, norms, batch->B, n_keep, delta, chunk_tot, saliency, leakage,
-                                  use_pruned, row_flag, s));
+                                  use_pruned, row_flag, seq_cnt, s));
   // 3. down, skipping the channels of P on the rows that run pruned
   CE_TRY(launch_ffn_down_pruned(dn, s, g.clear_cnt != nullptr));
   return CE_OK;

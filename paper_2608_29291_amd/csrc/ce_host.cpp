@@ -168,6 +168,7 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
     L.sal_seg = take(tiles * kSalSegs * sF * 4);
     L.sal_meta = take(tiles * (kSalSegs + 1) * 4);
     L.row_flag = take(sC);
+    L.seq_cnt = take(sB * 4);
   }
   if (which == CE_WS_BLOCK_GAP) {
     // one slot per wave of the down GEMM and row; waves cover >= 32 features

@@ -34,6 +34,7 @@ struct WsLayout {
   size_t sal_seg;    // float [tiles x kSalSegs x d_ff] per-segment |z| sums (CE_WS_FFN_PRUNED)
   size_t sal_meta;   // int32 [tiles x (kSalSegs + 1)] segment counts and sequences (CE_WS_FFN_PRUNED)
   size_t row_flag;   // uint8 [cap] 1 where the packed row's sequence runs pruned (CE_WS_FFN_PRUNED)
+  size_t seq_cnt;    // int32 [B] arrival counters of the saliency kernel (CE_WS_FFN_PRUNED)
   size_t sal_part;   // float [kSalSplits x B x d_ff] FFN-saliency partial sums, then
                      // float [B x ceil(d_ff / 256) x 2] per-chunk totals
   size_t total;

@@ -81,14 +81,18 @@ hipError_t launch_ffn_down_pruned(const FfnGemmArgs& a, hipStream_t stream, bool
 bool ffn_pruned_ok(const FfnGemmArgs& gateup, const FfnGemmArgs& down);
 
 // Pruned FFN: row_seq[p] = b for the packed rows p of each sequence b.
-hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, hipStream_t stream);
+// Also zeroes seq_cnt [B] (the saliency kernel's arrival counters).
+hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, int32_t* seq_cnt,
+                          hipStream_t stream);
 // Saliency (Eq. 8) of each sequence from the gate/up epilogue's segment sums
 // (falling back to act for tiles with more than kSalSegs segments) and the
 // leakage (Eq. 9) of the tail channels [n_keep, d_ff); use_pruned = leakage <= delta,
-// also written to row_flag for every packed row of the sequence.
+// also written to row_flag for every packed row of the sequence. One launch:
+// the last workgroup of each sequence (seq_cnt, zeroed by launch_row_seq)
+// forms its leakage.
 hipError_t launch_saliency_segments(const FfnGemmArgs& gateup, const int32_t* kept_offsets, const float* norms,
                                     int B, int n_keep, float delta, float* chunk_tot, float* saliency, float* lambda,
-                                    uint8_t* use_pruned, uint8_t* row_flag, hipStream_t stream);
+                                    uint8_t* use_pruned, uint8_t* row_flag, int32_t* seq_cnt, hipStream_t stream);
 
 // Gap partial-sum slots per row (gap_np) of the down kernel that
 // launch_ffn_down picks for these arguments: ceil(d / features per wave).

@@ -236,8 +236,9 @@ __global__ __launch_bounds__(256) void mask_kernel(char* __restrict__ act, const
 
 // row_seq[p] = b for the packed rows p of sequence b (workgroup per sequence)
 __global__ __launch_bounds__(256) void row_seq_kernel(const int32_t* __restrict__ kept_offsets, int cap,
-                                                      int32_t* __restrict__ row_seq) {
+                                                      int32_t* __restrict__ row_seq, int32_t* __restrict__ seq_cnt) {
   const int b = blockIdx.x;
+  if (threadIdx.x == 0) seq_cnt[b] = 0;  // the saliency kernel's arrival counter of sequence b
   int j0 = kept_offsets[b], j1 = kept_offsets[b + 1];
   j0 = j0 < 0 ? 0 : (j0 > cap ? cap : j0);
   j1 = j1 < j0 ? j0 : (j1 > cap ? cap : j1);
@@ -250,8 +251,8 @@ __global__ __launch_bounds__(256) void row_seq_kernel(const int32_t* __restrict_
 // of sequence b add their |z| sums in tile order, per weight set; a tile with
 // more segments than the epilogue kept adds the rows of b from act instead.
 // saliency = (sum_set0 * norm0 + sum_set1 * norm1) / rows of b; the chunk's
-// totals over all channels and over the tail [n_keep, d_ff) go to chunk_tot
-// (the layout leakage_kernel reads).
+// totals over all channels and over the tail [n_keep, d_ff) go to chunk_tot,
+// and the sequence's last workgroup turns them into its leakage.
 struct SegSalArgs {
   const float* sal_part;
   const int32_t* sal_meta;
@@ -265,10 +266,18 @@ struct SegSalArgs {
   int B, cap, d_ff, n_sets, n_keep;
   float* saliency;
   float* chunk_tot;
+  // leakage (Eq. 9) and the choice, by the last workgroup of each sequence
+  int32_t* seq_cnt;  // [B] arrival counters, zero on entry
+  float delta;
+  float* lambda;
+  uint8_t* use_pruned;
+  uint8_t* row_flag;
 };
 
 __global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
   __shared__ float red[2][4];
+  __shared__ int last_s;
+  __shared__ float lam_s;
   const int b = blockIdx.y;
   const int c = blockIdx.x * 256 + threadIdx.x;
   int kt = *a.kt_ptr;
@@ -326,28 +335,59 @@ __global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
     float* o = a.chunk_tot + ((int64_t)b * gridDim.x + blockIdx.x) * 2;
     o[0] = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
     o[1] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    // the totals are visible device-wide before the arrival is counted
+    __threadfence();
+    last_s = atomicAdd(a.seq_cnt + b, 1) == (int)gridDim.x - 1;
   }
+  __syncthreads();
+  if (!last_s) return;
+  // the last of sequence b's workgroups: its leakage from the per-chunk
+  // totals (wave 0: lane l adds chunks l, l + 64, ..., then the lanes in a
+  // fixed tree; coherent loads, the other workgroups wrote them), the choice,
+  // and a flag byte for each of its packed rows
+  __threadfence();
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const float* tp = a.chunk_tot + (int64_t)b * gridDim.x * 2;
+    float t = 0.0f, p = 0.0f;
+    for (int k = lane; k < (int)gridDim.x; k += 64) {
+      t += __hip_atomic_load(tp + 2 * k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      p += __hip_atomic_load(tp + 2 * k + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      t += __shfl_xor(t, o);
+      p += __shfl_xor(p, o);
+    }
+    if (lane == 0) {
+      const float lam = t > 0.0f ? p / t : 0.0f;
+      lam_s = lam;
+      a.lambda[b] = lam;
+      a.use_pruned[b] = lam <= a.delta ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  const uint8_t use = lam_s <= a.delta ? 1 : 0;
+  for (int j = j0 + (int)threadIdx.x; j < j1; j += 256) a.row_flag[j] = use;
 }
 
 }  // namespace
 
-hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, hipStream_t stream) {
-  hipLaunchKernelGGL(row_seq_kernel, dim3(B), dim3(256), 0, stream, kept_offsets, cap, row_seq);
+hipError_t launch_row_seq(const int32_t* kept_offsets, int B, int cap, int32_t* row_seq, int32_t* seq_cnt,
+                          hipStream_t stream) {
+  hipLaunchKernelGGL(row_seq_kernel, dim3(B), dim3(256), 0, stream, kept_offsets, cap, row_seq, seq_cnt);
   return hipGetLastError();
 }
 
 hipError_t launch_saliency_segments(const FfnGemmArgs& g, const int32_t* kept_offsets, const float* norms, int B,
                                     int n_keep, float delta, float* chunk_tot, float* saliency, float* lambda,
-                                    uint8_t* use_pruned, uint8_t* row_flag, hipStream_t stream) {
+                                    uint8_t* use_pruned, uint8_t* row_flag, int32_t* seq_cnt,
+                                    hipStream_t stream) {
   // gate/up: GEMM row j is packed row map1[j] (the MoT grouping) or j; act is in GEMM row order
   SegSalArgs s{g.sal_part, g.sal_meta, g.out, g.map1, g.row_seq, kept_offsets, g.kt_ptr, g.n0_ptr, norms,
-               B, g.cap, g.n_feat, g.n_sets, n_keep, saliency, chunk_tot};
+               B, g.cap, g.n_feat, g.n_sets, n_keep, saliency, chunk_tot, seq_cnt, delta, lambda, use_pruned,
+               row_flag};
   const int chunks = (g.n_feat + 255) / 256;
   hipLaunchKernelGGL(saliency_seg_kernel, dim3(chunks, B), dim3(256), 0, stream, s);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(leakage_kernel, dim3((B + 3) / 4), dim3(256), 0, stream, (const float*)chunk_tot, chunks,
-                     B, delta, lambda, use_pruned, kept_offsets, g.cap, row_flag);
   return hipGetLastError();
 }
 
