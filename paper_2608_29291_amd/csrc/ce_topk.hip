@@ -2,19 +2,20 @@
 // packed index maps that drive compaction.
 //
 // Selection is exact and deterministic: each float32 logit becomes an
-// order-preserving uint32 key (-0 == +0, NaN lowest); a 4-pass 8-bit radix
-// select finds the key theta of the k-th retained routable token; then one
-// sweep in token order retains every always-kept token, every key > theta and
-// the first (k - #{key > theta}) tokens with key == theta (lower index wins).
-// The same sweep assigns packed positions with wavefront ballot / popcount
-// prefix sums, so kept_idx comes out ascending within each sequence.
+// order-preserving uint32 key (-0 == +0, NaN lowest); a radix select finds the
+// key theta of the k-th retained routable token; then one sweep in token order
+// retains every always-kept token, every key > theta and the first
+// (k - #{key > theta}) tokens with key == theta (lower index wins). The same
+// sweep assigns packed positions with wavefront ballot / popcount prefix sums,
+// so kept_idx comes out ascending within each sequence.
 //
 // One 1024-thread workgroup per sequence. Sequences of up to 16384 tokens keep
-// their keys and KEEP bits in LDS: the loads of four 1024-token chunks are in
-// flight together, one wave sums the packed offset meanwhile, each radix pass
-// takes two barriers (alternating histograms) and the sweep ranks all chunks
-// with one scan. Longer sequences re-read logits and flags from global memory
-// on every pass.
+// their keys in LDS: the loads of eight 1024-token chunks (four when the
+// scorer left partial sums over more than four tiles) are in flight together,
+// one wave sums the packed offset meanwhile, three radix passes of 12, 10 and
+// 10 bits take two barriers each, and the sweep ranks all chunks with one
+// scan. Longer sequences re-read logits and flags from global memory on each
+// of four 8-bit passes.
 #include "ce_device.hpp"
 #include "ce_launch.hpp"
 
@@ -33,11 +34,15 @@ __global__ __launch_bounds__(256) void seq_info_kernel(const int32_t* __restrict
   seq_summary(offs, flags, B, T, blockIdx.x, info, scratch);
 }
 
+constexpr uint32_t kKeptKey = 0xffffffffu;  // LDS path: an always-kept token's key (logit keys stop at +inf's)
+constexpr int kBins0 = 4096;  // LDS path, pass 0: key bits 31..20
+constexpr int kBins1 = 1024;  // LDS path, passes 1 and 2: bits 19..10, then 9..0
+
 struct SelShared {
   uint32_t keys[kMaxChunks * kSelThreads];
-  uint64_t keepmask[kMaxChunks * kSelWaves];
   uint32_t hist[256];         // global-memory path
-  uint32_t hist2[2][256];     // LDS path: one histogram per pass parity
+  alignas(16) uint32_t hA[kBins0];  // LDS path: passes 0 and 2
+  alignas(16) uint32_t hB[kBins1];  // LDS path: pass 1
   uint32_t slot_cnt[kMaxChunks * kSelWaves];  // LDS path sweep: per (chunk, wave) counts
   int32_t wsum_s[kSelWaves];
   int32_t wsum_e[kSelWaves];
@@ -108,10 +113,110 @@ __device__ __forceinline__ void find_digit(const uint32_t* h, int krem, int lane
   }
 }
 
-// Sequences of at most kMaxChunks * kSelThreads tokens: keys and KEEP bits
-// in LDS. The loops stay loops: each workgroup runs this code once on a cold
-// instruction cache, and fully unrolled versions spent more time fetching
-// instructions than they saved.
+// Inclusive prefix sum over the 64 lanes of a wave (lane i: lanes 0..i), with
+// DPP row shifts inside each row of 16 lanes, then the row-15 and row-31
+// broadcasts.
+__device__ __forceinline__ int wave_prefix_incl(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+  return v;
+}
+
+// Wave 0: the bin of the krem-th largest key in histogram h of 64 * kPer
+// bins, and the number of keys in higher bins. Lane l first sums bins
+// [kPer * l, kPer * (l + 1)); the range that holds the krem-th key is then
+// searched one bin per lane. Needs 1 <= krem <= the histogram's total.
+template <int kPer>
+__device__ __forceinline__ void find_bin(const uint32_t* h, int krem, int lane, SelShared& sh) {
+  constexpr int kQ = kPer / 4;  // 16-byte reads per lane
+  static_assert(kQ == 4 || kQ % 16 == 0, "bin range of 16 or a multiple of 64");
+  // each lane starts its reads at a different 16-byte column, so that a
+  // wave's reads spread over all banks
+  const int rot = kQ >= 16 ? lane : lane / (16 / kQ);
+  const uint4* h4 = reinterpret_cast<const uint4*>(h + kPer * lane);
+  uint32_t s = 0;
+#pragma unroll
+  for (int j = 0; j < kQ; ++j) {
+    const uint4 v = h4[(j + rot) & (kQ - 1)];
+    s += (v.x + v.y) + (v.z + v.w);
+  }
+  const int pre = wave_prefix_incl((int)s);
+  const int above = __builtin_amdgcn_readlane(pre, 63) - pre;  // keys in higher lanes' ranges
+  const uint64_t hit = __ballot(above < krem && above + (int)s >= krem);
+  const int L = hit ? __builtin_ctzll(hit) : 0;
+  const int above_l = __builtin_amdgcn_readlane(above, L);
+  const int v = lane < kPer ? (int)h[kPer * L + lane] : 0;
+  const int pre2 = wave_prefix_incl(v);
+  const int above2 = above_l + (__builtin_amdgcn_readlane(pre2, 63) - pre2);
+  const uint64_t hit2 = __ballot(lane < kPer && above2 < krem && above2 + v >= krem);
+  const int j = hit2 ? __builtin_ctzll(hit2) : 0;
+  if (lane == j) {
+    sh.sel_digit = (uint32_t)(kPer * L + j);
+    sh.sel_above = above2;
+  }
+}
+
+// Keys of the 1024-token chunks [c0, c0 + kC) from the rank-tiled scorer's
+// partial sums (n_tiles <= kQ tiles): the loads of every tile for the kC
+// chunks are in flight together, then each logit is summed in a fixed order:
+// core tiles, b2c, then (generation tokens) the expansion tiles and b2e[m].
+template <int kC, int kQ>
+__device__ __forceinline__ void assemble_keys(const SelectArgs& a, SelShared& sh, int c0, int lo, int len,
+                                              int n_tiles, bool has_exp, float b2e_m) {
+  const int tid = threadIdx.x;
+  const int64_t T = a.T;
+  const float* pp = a.part + lo;
+  int ic[kC];
+  uint32_t fc[kC];
+  float pc[kQ][kC];
+#pragma unroll
+  for (int j = 0; j < kC; ++j) {
+    ic[j] = min((c0 + j) * kSelThreads + tid, len - 1);
+    fc[j] = a.flags[lo + ic[j]];
+  }
+#pragma unroll
+  for (int q = 0; q < kQ; ++q)
+    if (q < n_tiles) {
+#pragma unroll
+      for (int j = 0; j < kC; ++j) pc[q][j] = pp[q * T + ic[j]];
+    }
+#pragma unroll
+  for (int j = 0; j < kC; ++j) {
+    float l = pc[0][j];
+#pragma unroll
+    for (int q = 1; q < kQ; ++q)
+      if (q < a.n_ct) l += pc[q][j];
+    l += a.b2c;
+    if (has_exp) {
+      float e = 0.0f;
+#pragma unroll
+      for (int q = 1; q < kQ; ++q) {
+        if (q == a.n_ct) e = pc[q][j];
+        else if (q > a.n_ct && q < a.n_rt) e += pc[q][j];
+      }
+      if (fc[j] & 1u) l += e + b2e_m;
+    }
+    const int i = (c0 + j) * kSelThreads + tid;
+    const bool kp = (fc[j] & 2u) != 0;
+    if (i < len) {
+      sh.keys[i] = kp ? kKeptKey : logit_key(l);
+      a.logits_w[lo + i] = kp ? __builtin_inff() : l;
+    }
+  }
+}
+
+// Sequences of at most kMaxChunks * kSelThreads tokens: keys in LDS, an
+// always-kept token's key above every logit's (kKeptKey), so one histogram
+// counts both and krem starts at k + (always-kept count). Three passes on key
+// bits 31..20 (sign, exponent, three mantissa bits: routing logits spread
+// over many of these bins, where an 8-bit top digit puts most keys in one or
+// two bins and the LDS atomics serialize), 19..10 and 9..0. The loops stay
+// loops, each handling four tokens per thread at a time: each workgroup runs
+// this code once on a cold instruction cache.
 __device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& sh, int b, int lo, int len,
                                                 int nkeep) {
   const int tid = threadIdx.x;
@@ -130,89 +235,43 @@ __device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& 
     w0 = a.info[3 * lane + 2];
   }
 
-  // ---- keys: token c * 1024 + tid of chunk c; four chunks per round with
+  // ---- keys: token c * 1024 + tid of chunk c; eight chunks per round with
   //      their loads in flight together (clamped into the sequence) ----
   if (!a.part) {
 #pragma unroll 1
-    for (int c0 = 0; c0 < nc; c0 += 4) {
-      uint32_t f4[4];
-      float l4[4];
+    for (int c0 = 0; c0 < nc; c0 += 8) {
+      uint32_t f8[8];
+      float l8[8];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 8; ++j) {
         const int i = min((c0 + j) * kSelThreads + tid, len - 1);
-        f4[j] = a.flags[lo + i];
-        l4[j] = a.logits[lo + i];
+        f8[j] = a.flags[lo + i];
+        l8[j] = a.logits[lo + i];
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 8; ++j) {
         const int i = (c0 + j) * kSelThreads + tid;
-        const bool kp = (f4[j] & 2u) != 0 && i < len;
-        if (i < len) sh.keys[i] = logit_key(kp ? __builtin_inff() : l4[j]);
-        const uint64_t bal = __ballot(kp);
-        if (lane == 0 && c0 + j < nc) sh.keepmask[(c0 + j) * kSelWaves + wave] = bal;
+        if (i < len) sh.keys[i] = (f8[j] & 2u) ? kKeptKey : logit_key(l8[j]);
       }
     }
   } else {
-    // logits from the rank-tiled scorer's partial sums, tile by tile so that
-    // a tile's loads for the round's chunks are in flight together; fixed
-    // order: core tiles, b2c, then (generation tokens) the expansion tiles and
-    // b2e[m]
+    // logits from the rank-tiled scorer's partial sums: eight chunks per
+    // round with up to four tiles, else four
     float b2e_m = 0.0f;
     if (a.r_exp > 0 && a.b2e) {
       const double mf = floor((double)a.n_seg * (double)a.t[b]);
       const int m = (mf >= 0.0) ? (int)fmin(mf, (double)(a.n_seg - 1)) : 0;  // NaN -> 0
       b2e_m = a.b2e[m];
     }
-    const int64_t T = a.T;
-    const float* pp = a.part + lo;
     const bool has_exp = a.r_exp > 0 && a.n_rt > a.n_ct;
+    const int n_tiles = has_exp ? a.n_rt : a.n_ct;
+    if (n_tiles <= 4) {
 #pragma unroll 1
-    for (int c0 = 0; c0 < nc; c0 += 4) {
-      int i4[4];
-      uint32_t f4[4];
-      float l4[4], v4[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        i4[j] = min((c0 + j) * kSelThreads + tid, len - 1);
-        f4[j] = a.flags[lo + i4[j]];
-        l4[j] = pp[i4[j]];
-      }
+      for (int c0 = 0; c0 < nc; c0 += 8) assemble_keys<8, 4>(a, sh, c0, lo, len, n_tiles, has_exp, b2e_m);
+    } else {
 #pragma unroll 1
-      for (int q = 1; q < a.n_ct; ++q) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v4[j] = pp[q * T + i4[j]];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) l4[j] += v4[j];
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) l4[j] += a.b2c;
-      if (has_exp) {
-        float e4[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) e4[j] = pp[a.n_ct * T + i4[j]];
-#pragma unroll 1
-        for (int q = a.n_ct + 1; q < a.n_rt; ++q) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v4[j] = pp[q * T + i4[j]];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) e4[j] += v4[j];
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (f4[j] & 1u) l4[j] += e4[j] + b2e_m;
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = (c0 + j) * kSelThreads + tid;
-        const bool kp = (f4[j] & 2u) != 0 && i < len;
-        const float l = kp ? __builtin_inff() : l4[j];
-        if (i < len) {
-          sh.keys[i] = logit_key(l);
-          a.logits_w[lo + i] = l;
-        }
-        const uint64_t bal = __ballot(kp);
-        if (lane == 0 && c0 + j < nc) sh.keepmask[(c0 + j) * kSelWaves + wave] = bal;
-      }
+      for (int c0 = 0; c0 < nc; c0 += 4)
+        assemble_keys<4, kScoreMaxTiles>(a, sh, c0, lo, len, n_tiles, has_exp, b2e_m);
     }
   }
 
@@ -222,69 +281,86 @@ __device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& 
   } else if (st_wave) {
     batch_status_wave(a, lane, len0, w0);
   }
-  if (tid < 512) (&sh.hist2[0][0])[tid] = 0u;
+  // pass 0 counts into hA, pass 1 into hB, pass 2 into hA's first kBins1
+  // bins (cleared by wave 1 while wave 0 scans hB)
+#pragma unroll
+  for (int j = 0; j < kBins0 / kSelThreads; ++j) sh.hA[j * kSelThreads + tid] = 0u;
+  sh.hB[tid] = 0u;
   __syncthreads();
 
-  auto keep_of = [&](int i) -> bool { return (sh.keepmask[i >> 6] >> (i & 63)) & 1ull; };
   const int n_r = len - nkeep;
   const int k = num_keep_dev(a.keep, n_r);
   // mode: 0 = none of the routable tokens, 1 = all of them, 2 = threshold
   const int mode = (k <= 0) ? 0 : (k >= n_r ? 1 : 2);
 
-  uint32_t theta = 0;
-  int krem = k;
-  if (mode == 2) {
-    uint32_t prefix = 0, pmask = 0;
-    // two histograms alternate: wave 1 clears the next pass's while wave 0
-    // scans this one, so a pass takes two barriers
+  // Adds the keys of the sequence whose bits above `shift_m` equal `match` to
+  // h[(key >> shift) & mask], four tokens per thread at a time.
+  auto count_pass = [&](uint32_t* h, int shift_m, uint32_t match, int shift, uint32_t mask) {
 #pragma unroll 1
-    for (int p = 0; p < 4; ++p) {
-      const int shift = 24 - 8 * p;
-      uint32_t* h = sh.hist2[p & 1];
-#pragma unroll 1
-      for (int i = tid; i < len; i += kSelThreads) {
-        const uint32_t key = sh.keys[i];
-        if (!keep_of(i) && (key & pmask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
-      }
-      lds_barrier();
-      if (wave == 0) {
-        find_digit(h, krem, lane, sh);
-      } else if (wave == 1 && p < 3) {
-        uint32_t* hn = sh.hist2[(p + 1) & 1];  // scanned in the previous pass
+    for (int c0 = 0; c0 < nc; c0 += 4) {
+      uint32_t k4[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) hn[4 * lane + j] = 0u;
-      }
-      lds_barrier();
-      prefix |= sh.sel_digit << shift;
-      pmask |= 255u << shift;
-      krem -= sh.sel_above;
-    }
-    theta = prefix;
-  }
-  // krem = number of theta-equal routable tokens to retain (lowest indices first)
-
-  // ---- sweep: strong (always kept) and tie tokens counted per (chunk, wave)
-  //      in token order, one scan over those counts, then packed positions ----
-  auto classify = [&](int i, bool& st, bool& eq) {
-    st = false;
-    eq = false;
-    if (i < len) {
-      if (keep_of(i) || mode == 1) {
-        st = true;
-      } else if (mode == 2) {
-        const uint32_t key = sh.keys[i];
-        st = key > theta;
-        eq = key == theta;
+      for (int j = 0; j < 4; ++j) k4[j] = sh.keys[min((c0 + j) * kSelThreads + tid, len - 1)];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool in = (c0 + j) * kSelThreads + tid < len;
+        const bool sel = shift_m >= 32 || (k4[j] >> shift_m) == match;
+        if (in && sel) atomicAdd(&h[(k4[j] >> shift) & mask], 1u);
       }
     }
   };
+
+  uint32_t theta = 0;
+  int krem = k + nkeep;  // the always-kept keys are the nkeep largest
+  if (mode == 2) {
+    count_pass(sh.hA, 32, 0u, 20, kBins0 - 1);
+    lds_barrier();
+    if (wave == 0) find_bin<kBins0 / 64>(sh.hA, krem, lane, sh);
+    lds_barrier();
+    uint32_t prefix = sh.sel_digit << 20;
+    krem -= sh.sel_above;
+    count_pass(sh.hB, 20, prefix >> 20, 10, kBins1 - 1);
+    lds_barrier();
+    if (wave == 0) {
+      find_bin<kBins1 / 64>(sh.hB, krem, lane, sh);
+    } else if (wave == 1) {
+      uint4* z = reinterpret_cast<uint4*>(sh.hA) + lane * (kBins1 / 256);
+#pragma unroll
+      for (int j = 0; j < kBins1 / 256; ++j) z[j] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    lds_barrier();
+    prefix |= sh.sel_digit << 10;
+    krem -= sh.sel_above;
+    count_pass(sh.hA, 10, prefix >> 10, 0, kBins1 - 1);
+    lds_barrier();
+    if (wave == 0) find_bin<kBins1 / 64>(sh.hA, krem, lane, sh);
+    lds_barrier();
+    theta = prefix | sh.sel_digit;
+    krem -= sh.sel_above;
+  }
+  // krem = number of theta-equal routable tokens to retain (lowest indices
+  // first); theta < kKeptKey, so the always-kept tokens count as strong
+
+  // ---- sweep: strong (always kept) and tie tokens counted per (chunk, wave)
+  //      in token order, one scan over those counts, then packed positions ----
+  auto classify = [&](uint32_t key, bool in, bool& st, bool& eq) {
+    st = in && (mode == 1 || (mode == 0 ? key == kKeptKey : key > theta));
+    eq = in && mode == 2 && key == theta;
+  };
 #pragma unroll 1
-  for (int c = 0; c < nc; ++c) {
-    bool st, eq;
-    classify(c * kSelThreads + tid, st, eq);
-    const uint64_t bs = __ballot(st), be = __ballot(eq);
-    // strong count in the low 16 bits, ties in the high 16 (each at most 16384)
-    if (lane == 0) sh.slot_cnt[c * kSelWaves + wave] = (uint32_t)__popcll(bs) | ((uint32_t)__popcll(be) << 16);
+  for (int c0 = 0; c0 < nc; c0 += 4) {
+    uint32_t k4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) k4[j] = sh.keys[min((c0 + j) * kSelThreads + tid, len - 1)];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      bool st, eq;
+      classify(k4[j], (c0 + j) * kSelThreads + tid < len, st, eq);
+      const uint64_t bs = __ballot(st), be = __ballot(eq);
+      // strong count in the low 16 bits, ties in the high 16 (each at most 16384)
+      if (lane == 0 && c0 + j < nc)
+        sh.slot_cnt[(c0 + j) * kSelWaves + wave] = (uint32_t)__popcll(bs) | ((uint32_t)__popcll(be) << 16);
+    }
   }
   __syncthreads();
   if (wave == 0) {
@@ -295,12 +371,8 @@ __device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& 
 #pragma unroll
     for (int j = 0; j < 4; ++j) v4[j] = (4 * lane + j < n_ent) ? sh.slot_cnt[4 * lane + j] : 0u;
     const uint32_t tot = v4[0] + v4[1] + v4[2] + v4[3];
-    uint32_t incl = tot;
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t y = __shfl_up(incl, o);
-      if (lane >= o) incl += y;
-    }
-    uint32_t run = incl - tot;
+    // both 16-bit halves stay below 2^15, so the packed sums fit an int
+    uint32_t run = (uint32_t)wave_prefix_incl((int)tot) - tot;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if (4 * lane + j < n_ent) sh.slot_cnt[4 * lane + j] = run;
@@ -310,19 +382,27 @@ __device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& 
   __syncthreads();
   const int64_t off_b = sh.off_b;
 #pragma unroll 1
-  for (int c = 0; c < nc; ++c) {
-    const int i = c * kSelThreads + tid;
-    bool st, eq;
-    classify(i, st, eq);
-    const uint64_t bs = __ballot(st), be = __ballot(eq);
-    const uint32_t pre = sh.slot_cnt[c * kSelWaves + wave];
-    const int s_before = (int)(pre & 0xffffu) + __popcll(bs & lt_mask);
-    const int e_before = (int)(pre >> 16) + __popcll(be & lt_mask);
-    const bool kept = st || (eq && e_before < krem);
-    const int64_t pos = off_b + s_before + (e_before < krem ? e_before : krem);
-    if (i < len) {
-      if (kept && pos < a.cap) a.kept_idx[pos] = lo + i;
-      if (a.token_pos) a.token_pos[lo + i] = kept ? (int32_t)(pos < 0x7fffffff ? pos : 0x7fffffff) : -1;
+  for (int c0 = 0; c0 < nc; c0 += 4) {
+    uint32_t k4[4], pre4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      k4[j] = sh.keys[min((c0 + j) * kSelThreads + tid, len - 1)];
+      pre4[j] = sh.slot_cnt[min(c0 + j, nc - 1) * kSelWaves + wave];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = (c0 + j) * kSelThreads + tid;
+      bool st, eq;
+      classify(k4[j], i < len, st, eq);
+      const uint64_t bs = __ballot(st), be = __ballot(eq);
+      const int s_before = (int)(pre4[j] & 0xffffu) + __popcll(bs & lt_mask);
+      const int e_before = (int)(pre4[j] >> 16) + __popcll(be & lt_mask);
+      const bool kept = st || (eq && e_before < krem);
+      const int64_t pos = off_b + s_before + (e_before < krem ? e_before : krem);
+      if (i < len) {
+        if (kept && pos >= 0 && pos < a.cap) a.kept_idx[pos] = lo + i;
+        if (a.token_pos) a.token_pos[lo + i] = kept ? (int32_t)(pos < 0x7fffffff ? pos : 0x7fffffff) : -1;
+      }
     }
   }
   if (tid == 0) {
