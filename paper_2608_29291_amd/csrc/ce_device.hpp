@@ -209,13 +209,25 @@ __device__ __forceinline__ void seq_summary(const int32_t* __restrict__ offs, co
   const bool bad = o0 < 0 || o1 < o0 || o1 > T || (b == 0 && o0 != 0) || (b == B - 1 && o1 != T);
   const int lo = o0 < 0 ? 0 : (o0 > T ? T : o0);
   const int hi = o1 < lo ? lo : (o1 > T ? T : o1);
-  int64_t c = 0;
-  for (int i = lo + threadIdx.x; i < hi; i += blockDim.x) c += (flags[i] & 2) ? 1 : 0;
-  c = block_sum_i64(c, scratch);
+  // KEEP bits of [lo, hi): the 16-byte-aligned middle in 16-byte loads (one
+  // or two per thread for sequences of a few thousand tokens), the ends bytewise
+  int m0 = lo + (int)((16u - (uint32_t)(((uintptr_t)flags + (uintptr_t)lo) & 15u)) & 15u);
+  m0 = m0 > hi ? hi : m0;
+  const int m1 = m0 + ((hi - m0) & ~15);
+  int c = 0;
+  for (int i = lo + (int)threadIdx.x; i < m0; i += blockDim.x) c += (flags[i] >> 1) & 1;
+  for (int i = m1 + (int)threadIdx.x; i < hi; i += blockDim.x) c += (flags[i] >> 1) & 1;
+  const uint4* fw = reinterpret_cast<const uint4*>(flags + m0);
+  for (int i = threadIdx.x; i < (m1 - m0) >> 4; i += blockDim.x) {
+    const uint4 v = fw[i];
+    c += __popc(v.x & 0x02020202u) + __popc(v.y & 0x02020202u) + __popc(v.z & 0x02020202u) +
+         __popc(v.w & 0x02020202u);
+  }
+  const int64_t n_keep = block_sum_i64(c, scratch);
   if (threadIdx.x == 0) {
     info[3 * b + 0] = lo;
     info[3 * b + 1] = hi - lo;
-    info[3 * b + 2] = (int32_t)c | (bad ? (int32_t)0x80000000 : 0);
+    info[3 * b + 2] = (int32_t)n_keep | (bad ? (int32_t)0x80000000 : 0);
   }
 }
 

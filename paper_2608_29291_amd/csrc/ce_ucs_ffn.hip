@@ -274,7 +274,11 @@ struct SegSalArgs {
   uint8_t* row_flag;
 };
 
+constexpr int kMetaTiles = 64;  // token tiles whose segment lists are staged in LDS at a time
+
 __global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
+  __shared__ int32_t meta_s[kMetaTiles * (kSalSegs + 1)];
+  __shared__ int match_s[kMetaTiles];
   __shared__ float red[2][4];
   __shared__ int last_s;
   __shared__ float lam_s;
@@ -297,25 +301,62 @@ __global__ __launch_bounds__(256) void saliency_seg_kernel(SegSalArgs a) {
   const int t_lo = a.n_sets == 2 ? 0 : j0 / 256;
   const int t_hi = a.n_sets == 2 ? tiles : (j1 > j0 ? (j1 - 1) / 256 + 1 : t_lo);
   float tot = 0.0f, pm = 0.0f;
-  if (c < a.d_ff) {
-    float acc[2] = {0.0f, 0.0f};
-    for (int tt = t_lo; tt < t_hi; ++tt) {
-      const int set = tt < tiles0 ? 0 : 1;
-      const int32_t* meta = a.sal_meta + (int64_t)tt * (kSalSegs + 1);
-      const int cnt = meta[0];
-      if (cnt <= kSalSegs) {
-        for (int k = 0; k < cnt; ++k)
-          if (meta[1 + k] == b) acc[set] += a.sal_part[((int64_t)tt * kSalSegs + k) * a.d_ff + c];
-      } else {
-        const int lo = set == 0 ? tt * 256 : n0 + (tt - tiles0) * 256;
-        const int hi = min(lo + 256, set == 0 ? n0 : kt);
-        for (int j = lo; j < hi; ++j) {
-          const int p = a.grp ? a.grp[j] : j;
-          if (p >= 0 && p < a.cap && a.row_seq[p] == b)
-            acc[set] += fabsf(bf16_to_f32(reinterpret_cast<const uint16_t*>(a.act)[(int64_t)j * a.d_ff + c]));
+  float acc[2] = {0.0f, 0.0f};
+  for (int tb = t_lo; tb < t_hi; tb += kMetaTiles) {
+    const int nt = min(kMetaTiles, t_hi - tb);
+    // the segment lists of tiles tb .. tb + nt - 1 in one round of loads,
+    // then the segment of sequence b in each (-1: none; -2: the tile has more
+    // segments than the epilogue kept, or b in more than one)
+    __syncthreads();
+    for (int i = threadIdx.x; i < nt * (kSalSegs + 1); i += 256)
+      meta_s[i] = a.sal_meta[(int64_t)tb * (kSalSegs + 1) + i];
+    __syncthreads();
+    if ((int)threadIdx.x < nt) {
+      const int* m = meta_s + threadIdx.x * (kSalSegs + 1);
+      const int cnt = m[0];
+      int km = -1, hits = 0;
+      for (int k = 0; k < (cnt <= kSalSegs ? cnt : 0); ++k)
+        if (m[1 + k] == b) {
+          km = k;
+          ++hits;
+        }
+      match_s[threadIdx.x] = (cnt > kSalSegs || hits > 1) ? -2 : km;
+    }
+    __syncthreads();
+    if (c >= a.d_ff) continue;
+    // four tiles' sums loaded together (a tile without a segment of b reads
+    // its slot 0 and drops it), added in tile order
+#pragma unroll 1
+    for (int t0 = 0; t0 < nt; t0 += 4) {
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = min(t0 + j, nt - 1);
+        const int km = match_s[t];
+        v[j] = a.sal_part[((int64_t)(tb + t) * kSalSegs + (km > 0 ? km : 0)) * a.d_ff + c];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (t0 + j >= nt) break;
+        const int tt = tb + t0 + j;
+        const int set = tt < tiles0 ? 0 : 1;
+        const int km = match_s[t0 + j];
+        if (km >= 0) {
+          acc[set] += v[j];
+        } else if (km == -2) {
+          // the rows of b in this tile, from act
+          const int lo = set == 0 ? tt * 256 : n0 + (tt - tiles0) * 256;
+          const int hi = min(lo + 256, set == 0 ? n0 : kt);
+          for (int jr = lo; jr < hi; ++jr) {
+            const int p = a.grp ? a.grp[jr] : jr;
+            if (p >= 0 && p < a.cap && a.row_seq[p] == b)
+              acc[set] += fabsf(bf16_to_f32(reinterpret_cast<const uint16_t*>(a.act)[(int64_t)jr * a.d_ff + c]));
+          }
         }
       }
     }
+  }
+  if (c < a.d_ff) {
     const float n1c = a.n_sets == 2 ? a.norms[(int64_t)a.d_ff + c] : 0.0f;
     const float v = j1 > j0 ? (acc[0] * a.norms[c] + acc[1] * n1c) / (float)(j1 - j0) : 0.0f;
     a.saliency[(int64_t)b * a.d_ff + c] = v;
