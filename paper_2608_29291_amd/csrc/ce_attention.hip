@@ -39,8 +39,10 @@
 //     after the block's last query are skipped, and only tiles that reach past
 //     a wave's first visible limit are masked element by element;
 //   * the scale is folded into the exponent, p = 2^(s c - m c) with c = scale
-//     log2 e > 0 and m the running maximum of the raw scores, and the output
-//     is rescaled only when some lane's maximum moved.
+//     log2 e > 0 and m a running maximum of the raw scores that moves (and
+//     rescales the output and the sum) only when some lane's tile maximum
+//     exceeds it by more than 8 / c, so p < 2^8 and most tiles skip the
+//     rescale.
 #include <type_traits>
 
 #include "ce_device.hpp"
@@ -58,6 +60,7 @@ constexpr int kKBytes = kKT * kKRow;       // 16 KB
 constexpr int kVRow = kKT * 2;             // bytes per row of V^T (64 keys)
 constexpr int kVBlk = 32 * kVRow + 8;      // 32 rows of V^T, padded
 constexpr int kVBytes = 4 * kVBlk;         // 16 KB + 32
+constexpr float kLazy = 8.0f;              // headroom of the running maximum (exponent of 2)
 
 struct AttnArgs {
   const char* q;
@@ -253,9 +256,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb2][v]);
     mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float mc = m_new == -__builtin_inff() ? 0.0f : m_new * a.scale_log2;
-    const float alpha = __builtin_amdgcn_exp2f(m_run * a.scale_log2 - mc);
+    // The running maximum moves (and the output is rescaled) only when some
+    // lane's tile maximum exceeds it by more than kLazy in the exponent, so
+    // probabilities stay below 2^kLazy; the sum l uses the same maximum, so
+    // the quotient O / l does not depend on it.
+    if (__builtin_amdgcn_ballot_w64((mt - m_run) * a.scale_log2 > kLazy)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha =
+          m_new == -__builtin_inff() ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * a.scale_log2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
+      l_run *= alpha;
+      m_run = m_new;
+    }
+    const float mc = m_run == -__builtin_inff() ? 0.0f : m_run * a.scale_log2;
     float rs = 0.0f;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
@@ -272,12 +286,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         pf[st][i] = pack_bf16(sc[st >> 1][8 * (st & 1) + 2 * i], sc[st >> 1][8 * (st & 1) + 2 * i + 1]);
-    l_run = l_run * alpha + rs;
-    if (__builtin_amdgcn_ballot_w64(m_new != m_run)) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) oacc[i] *= alpha;
-    }
-    m_run = m_new;
+    l_run += rs;
     // ---- O^T += V^T P^T over 4 steps of 16 keys ----
     const char* vb = vbuf + kCur * kVBytes;
 #pragma unroll

@@ -80,6 +80,27 @@ def test_sharp_scores_and_scale(G):
         check(got, oa.attention(q, k, v, qo, ko, 2, True, scale), v)
 
 
+@pytest.mark.parametrize("step", [0.05, 0.7, 3.0])
+def test_rising_scores(G, step):
+    """Scores that grow along the keys (key j carries j * step times the
+    query's direction), so the running maximum climbs tile after tile: by
+    less than the kernel's headroom per tile (probabilities up to 2^8 before
+    a rescale), or by more (a rescale at every tile). Same bar."""
+    rng = np.random.default_rng(11)
+    n = 700
+    q, k, v, qo, ko = make_attention_inputs([n], [n], 4, 2, DH, seed=12)
+    u = rng.standard_normal(DH)
+    u /= np.linalg.norm(u)
+    q[:] = u * np.sqrt(DH)
+    k[:] = (np.arange(n)[:, None, None] * step / np.sqrt(DH)) * u[None, None, :] + 0.1 * k
+    from ce_workloads import bf16_round
+    q, k = bf16_round(q.astype(np.float32)), bf16_round(k.astype(np.float32))
+    for causal in (False, True):
+        got, scale = run(G, q, k, v, qo, ko, causal, scale=1.0 / np.sqrt(DH))
+        print(f"[attn rising step={step} causal={causal}]")
+        check(got, oa.attention(q, k, v, qo, ko, 2, causal, scale), v)
+
+
 def test_deterministic(G):
     q, k, v, qo, ko = make_attention_inputs([550, 300], [550, 300], 12, 2, DH, seed=6)
     a, _ = run(G, q, k, v, qo, ko, True)
