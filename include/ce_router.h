@@ -37,7 +37,8 @@
  *   one dtype (CE_F32 or CE_BF16); biases, second-layer scorer vectors,
  *   timesteps and logits are float32; indices are int32.
  * - Shape limits: d % 64 == 0, d_ff % 64 == 0, scorer ranks % 32 == 0 and
- *   r_core + r_exp <= 512, 1 <= n_seg <= 16, B >= 1, 0 <= T < 2^31.
+ *   r_core + r_exp <= 512, 1 <= n_seg <= 16, 1 <= B <= 65535 (more
+ *   sequences: CE_ERR_UNSUPPORTED), 0 <= T < 2^31.
  * - Matrices are row-major in the nn.Linear layout [out_features x in_features].
  * - Functions are stateless; concurrent calls on different streams are safe
  *   as long as they use different workspaces and outputs.

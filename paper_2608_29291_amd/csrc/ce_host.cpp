@@ -205,6 +205,7 @@ int32_t num_keep_host(float keep, int32_t n) {
 int check_batch(const ce_batch* b, bool need_t) {
   if (!b) return CE_ERR_INVALID_ARG;
   if (b->B < 1 || b->T < 0 || b->kept_capacity < 0) return CE_ERR_INVALID_ARG;
+  if (b->B > kMaxBatch) return CE_ERR_UNSUPPORTED;  // sequence index in a grid's y dimension
   if (!b->seq_offsets) return CE_ERR_INVALID_ARG;
   if (b->T > 0 && !b->flags) return CE_ERR_INVALID_ARG;
   if (need_t && !b->t) return CE_ERR_INVALID_ARG;

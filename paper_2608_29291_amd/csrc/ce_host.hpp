@@ -72,6 +72,8 @@ GemmSplit gemm_split(int64_t items, int ns);
 // superslabs, fewer than 3 of them, or 32-bit offsets overflowing).
 void gemm_items(int mode, int cap, int d, int d_ff, int n_sets, int elem, int64_t* items, int* ns);
 
+// Sequences per batch: some grids put the sequence index in their y dimension.
+constexpr int kMaxBatch = 65535;
 // The FFN-saliency reduction splits each sequence's rows over at most this
 // many workgroups (partial sums in the workspace, summed in a fixed order).
 constexpr int kSalSplits = 16;

@@ -97,6 +97,7 @@ def score(b, w, hidden=FAKE, logits=FAKE):
     (lambda b, w: (None, w), ce.CE_ERR_INVALID_ARG),
     (lambda b, w: (b, None), ce.CE_ERR_INVALID_ARG),
     (lambda b, w: (_batch(B=0), w), ce.CE_ERR_INVALID_ARG),
+    (lambda b, w: (_batch(B=65536), w), ce.CE_ERR_UNSUPPORTED),
     (lambda b, w: (_batch(T=-1), w), ce.CE_ERR_INVALID_ARG),
     (lambda b, w: (_batch(keep=1.5), w), ce.CE_ERR_INVALID_ARG),
     (lambda b, w: (_batch(keep=float("nan")), w), ce.CE_ERR_INVALID_ARG),
