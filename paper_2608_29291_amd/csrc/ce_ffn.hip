@@ -313,6 +313,21 @@ __global__ __launch_bounds__(64 * kWW * kWT) void ffn_gemm_kernel(FfnGemmArgs a,
   }
 }
 
+// Token tiles of a gate/up launch over n packed rows: 256 rows each, except
+// that with `absorb` a last tile of at most 32 rows joins the tile before it
+// (which then holds 257 to 288 rows). A tile of a few rows would stream a
+// whole weight tile through LDS for them; the joined tile reads those rows'
+// fragments straight into registers while the weight superslabs it holds
+// anyway are in LDS (one more 32 x 32 block per wave). Non-decreasing in n,
+// and tiles(n0) + tiles(n1) <= tiles(n0 + n1) + 1, so a grid sized for the
+// capacity covers any packed count below it, split over two weight sets too.
+__host__ __device__ inline int gateup_token_tiles(int n, bool absorb) {
+  if (n <= 0) return 0;
+  int t = (n + 255) / 256;
+  if (absorb && t >= 2 && n - 256 * (t - 1) <= 32) --t;
+  return t;
+}
+
 // Ping-pong bf16 kernel (the gate/up workhorse, and the down GEMM on large
 // grids): 8 waves, two per SIMD, over a 256 x 256 tile. Wave w owns weight
 // rows 128 (w & 1) .. +128 and token rows 64 (w >> 1) .. +64 (4 x 2 MFMA
@@ -400,18 +415,23 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   int n0 = *(two_sets ? a.n0_ptr : a.kt_ptr);
   kt = kt < 0 ? 0 : (kt > a.cap ? a.cap : kt);
   n0 = two_sets ? (n0 < 0 ? 0 : (n0 > kt ? kt : n0)) : kt;
-  const int tiles0 = (n0 + kTR - 1) / kTR;
+  const bool absorb = kMode == 0 && kSplit == 1 && sp.absorb != 0;
+  const int tiles0 = gateup_token_tiles(n0, absorb);
   int set, row_lo, row_hi;
   if (tt < tiles0) {
     set = 0;
     row_lo = tt * kTR;
-    row_hi = min(row_lo + kTR, n0);
+    row_hi = tt == tiles0 - 1 ? n0 : row_lo + kTR;
   } else {
     set = 1;
-    row_lo = n0 + (tt - tiles0) * kTR;
-    row_hi = min(row_lo + kTR, kt);
+    const int t1 = tt - tiles0, tiles1 = gateup_token_tiles(kt - n0, absorb);
+    if (t1 >= tiles1) return;
+    row_lo = n0 + t1 * kTR;
+    row_hi = t1 == tiles1 - 1 ? kt : row_lo + kTR;
   }
   if (row_lo >= row_hi) return;
+  // a tile holding the absorbed last rows [row_lo + 256, row_hi) of its set
+  const bool ext = absorb && row_hi - row_lo > kTR;
 
   const int n_feat = a.n_feat;
   constexpr int kFTile = (kMode == 0) ? kWR / 2 : kWR;
@@ -433,9 +453,11 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const bool is_w = wave < 4;
   const int r8 = lane >> 3;
   const int pch = lane & 7;
-  const __amdgpu_buffer_rsrc_t wr0 = make_rsrc(a.w0[set], (uint32_t)(n_feat * a.w_ld));
+  // (the set picked by a select: an index into the argument's arrays would
+  // put them on the stack)
+  const __amdgpu_buffer_rsrc_t wr0 = make_rsrc(set ? a.w0[1] : a.w0[0], (uint32_t)(n_feat * a.w_ld));
   const __amdgpu_buffer_rsrc_t wr1 =
-      (kMode == 0) ? make_rsrc(a.w1[set], (uint32_t)(n_feat * a.w_ld)) : wr0;
+      (kMode == 0) ? make_rsrc(set ? a.w1[1] : a.w1[0], (uint32_t)(n_feat * a.w_ld)) : wr0;
   // Token rows past the tile's last packed row (the final token tile is
   // partial) are fetched from past the resource's end: zeros and no memory
   // traffic. Their MFMAs then multiply zeros, which draws less power than
@@ -574,6 +596,27 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   const uint32_t rowa = (uint32_t)((ww * 128 + lrow) * kRow);
   const uint32_t rowb = (uint32_t)((wt * 64 + lrow) * kRow);
   u32x4_t fa[2][kMW], fb[2][kMT];
+  // Absorbed rows (a tile with rows past row_lo + 256): lane l reads 16-byte
+  // chunks of row row_lo + 256 + (l & 31) straight into registers, fx[H]
+  // holding K half H of the next superslab, in the chunk order of the B
+  // fragments; wave (ww, wt) multiplies them with its weight block wt (rows
+  // 128 ww + 32 wt ..), so the 8 waves cover the tile's 256 weight rows once.
+  constexpr bool kExt = kMode == 0 && kSplit == 1;
+  f32x16_t accx = f32x16_t{};
+  u32x4_t fx[2][2];
+  uint32_t xoff = 0x80000000u;  // past the token resource: zeros
+  if (kExt && ext) {
+    const int j = row_lo + kTR + lrow;
+    int src = j < row_hi ? j : -1;
+    if (src >= 0 && a.map1) src = a.map1[src];
+    if (src >= 0 && a.map2) src = a.map2[src];
+    if (src >= 0) xoff = (uint32_t)((int64_t)src * a.tok_ld + 16 * lhalf);
+  }
+  auto fxload = [&](int s, auto hc) __attribute__((always_inline)) {
+    constexpr int H = decltype(hc)::value;
+    fx[H][0] = bload16(trs, xoff + 64 * H, (uint32_t)(s * kRow));
+    fx[H][1] = bload16(trs, xoff + 64 * H + 32, (uint32_t)(s * kRow));
+  };
 
   // superslabs [s0, ns) of K: all of them, or this piece's range when the
   // tile is split (>= 3 per range, checked by the launcher)
@@ -596,7 +639,24 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     ns = a.ns_keep * (piece + 1) / pieces;
   }
   using T2 = std::integral_constant<int, kPrune ? 2 : 0>;
-  if (is_w) {
+  using I2 = std::integral_constant<int, 2>;
+  if (kExt && ext) {
+    // the absorbed rows' first fragments go out between the two halves of
+    // the last prologue DMA, so the K loop starts with the loads in flight
+    // of its steady state (the compiler's waits for fx count on that)
+    static_assert(!kExt || (kBufs0 == 2 && kBufs1 == 3), "the ext waits assume rings of 2 and 3");
+    if (is_w) {
+      dma(s0, 0, I1{}, I0{});
+      fxload(s0, I0{});
+      dma(s0, 0, I2{}, I0{});
+    } else {
+      dma(s0, 0, I0{}, I0{});
+      dma(s0 + 1, 1, I1{}, I0{});
+      fxload(s0, I0{});
+      dma(s0 + 1, 1, I2{}, I0{});
+    }
+    fxload(s0, I1{});
+  } else if (is_w) {
 #pragma unroll
     for (int q = 0; q < kBufs0 - 1; ++q) dma(s0 + q, q, I0{}, I0{});
   } else {
@@ -612,15 +672,27 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     if (pieces > 1 && a.ns_keep <= s0) ns = s0;
     else if (a.ns_keep - s0 >= 3) ns = a.ns_keep;
   }
-  if (is_w) wait_vmcnt<8 * (kBufs0 - 2)>();
-  else wait_vmcnt<8 * (kBufs1 - 2)>();
+  if (kExt && ext) {
+    // after superslab s0's DMA: fx (weights); superslab s0 + 1 and fx (tokens)
+    if (is_w) wait_vmcnt<2>();
+    else wait_vmcnt<12>();
+  } else if (is_w) {
+    wait_vmcnt<8 * (kBufs0 - 2)>();
+  } else {
+    wait_vmcnt<8 * (kBufs1 - 2)>();
+  }
   lds_barrier();  // superslab 0 is in LDS
   if (late) lds_barrier();
   int wb = 0, tb = 0;  // ring slots of superslab s
-  // one memory phase and one compute phase over K half H of superslab s
-  auto half = [&](int s, auto hc, auto on, auto tmode) __attribute__((always_inline)) {
+  // one memory phase and one compute phase over K half H of superslab s.
+  // xc: 0 = a tile without absorbed rows; with them: 1 = a superslab whose
+  // DMAs and fragment loads all have a superslab to fetch (s < ns - 2),
+  // 2 = superslab ns - 2 (weight DMAs and fragment loads only), 3 = the last
+  // (neither)
+  auto half = [&](int s, auto hc, auto on, auto tmode, auto xc) __attribute__((always_inline)) {
     constexpr int H = decltype(hc)::value;
     constexpr bool kOn = decltype(on)::value;
+    constexpr int X = decltype(xc)::value;
     // ---- memory phase: fragments of K half H of superslab s ----
     const char* sa = wsm + wb * kSlab;
     const char* sb = tsm + tb * kSlab;
@@ -641,7 +713,7 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     const int slot = is_w ? wb : tb;
     const int fill = s + nb - 1;
     const int fslot = slot == 0 ? nb - 1 : slot - 1;
-    if (fill < ns) {
+    if (X == 1 || (X != 3 && fill < ns)) {
       if (is_w) {
         if constexpr (kSpreadW) dma(fill, fslot, std::integral_constant<int, H + 1>{}, I0{});
         else if constexpr (H == 0) dma(fill, fslot, I0{}, I0{});
@@ -654,9 +726,19 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     // second compute phase and group B's second memory phase: each wave
     // waits for its part of it there, leaving the later superslabs in flight
     const bool more = H == 1 && s + 1 < ns && (min(ns - 1, fill) - (s + 1)) >= 1;
+    // With absorbed rows each half also loads the fragments of superslab
+    // s + 1 (2 loads, after the compute phase): 12 loads follow the last DMA
+    // of superslab s + 1 here in the steady state, 4 in superslab ns - 2
+    // (no DMA of s + 2).
     if (H == 1 && late && s + 1 < ns) {
-      if (more) wait_vmcnt<8>();
-      else wait_vmcnt<0>();
+      if constexpr (X == 1) {
+        wait_vmcnt<12>();
+      } else if constexpr (X == 2) {
+        wait_vmcnt<4>();
+      } else if constexpr (X == 0) {
+        if (more) wait_vmcnt<8>();
+        else wait_vmcnt<0>();
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
@@ -671,11 +753,25 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 #pragma unroll
           for (int j = 0; j < kMT; ++j) mfma_step<true>(acc[i][j], fa[step][i], fb[step][j]);
     }
+    if constexpr (X != 0) {
+      // the absorbed rows against weight block wt (a wave-uniform choice)
+#pragma unroll
+      for (int i = 0; i < kMW; ++i)
+        if (i == wt) {
+          mfma_step<true>(accx, fa[0][i], fx[H][0]);
+          mfma_step<true>(accx, fa[1][i], fx[H][1]);
+        }
+      if constexpr (X != 3) fxload(s + 1, hc);
+    }
     if constexpr (kPrio) __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_sched_barrier(0);
     if (H == 1 && !late && s + 1 < ns) {
-      if (more) wait_vmcnt<8>();
-      else wait_vmcnt<0>();
+      if constexpr (X == 1 || X == 2) {
+        wait_vmcnt<2>();  // only the fragment loads just issued stay in flight
+      } else if constexpr (X == 0) {
+        if (more) wait_vmcnt<8>();
+        else wait_vmcnt<0>();
+      }
     }
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
@@ -689,8 +785,8 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
   auto kloop = [&](auto on) __attribute__((always_inline)) {
     auto run = [&](int lo, int hi, auto tmode) __attribute__((always_inline)) {
       for (int s = lo; s < hi; ++s) {
-        half(s, I0{}, on, tmode);
-        half(s, I1{}, on, tmode);
+        half(s, I0{}, on, tmode, I0{});
+        half(s, I1{}, on, tmode, I0{});
         wb = wb + 1 == kBufs0 ? 0 : wb + 1;
         tb = tb + 1 == kBufs1 ? 0 : tb + 1;
       }
@@ -703,8 +799,32 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       run(s0, ns, I0{});
     }
   };
-  if (mfma_on) kloop(std::true_type{});
-  else kloop(std::false_type{});
+  // tiles with absorbed rows: a steady loop whose every half issues the same
+  // loads (so the compiler's waits for fx are exact), then the last two
+  // superslabs written out (a loop over them gets the most conservative
+  // waits of both)
+  auto kloop_x = [&]() __attribute__((always_inline)) {
+    auto superslab = [&](int s, auto xc) __attribute__((always_inline)) {
+      half(s, I0{}, std::true_type{}, I0{}, xc);
+      half(s, I1{}, std::true_type{}, I0{}, xc);
+      wb = wb + 1 == kBufs0 ? 0 : wb + 1;
+      tb = tb + 1 == kBufs1 ? 0 : tb + 1;
+    };
+    for (int s = s0; s < ns - 2; ++s) superslab(s, std::integral_constant<int, 1>{});
+    superslab(ns - 2, std::integral_constant<int, 2>{});
+    superslab(ns - 1, std::integral_constant<int, 3>{});
+  };
+  bool ran_x = false;
+  if constexpr (kExt) {
+    if (ext) {
+      kloop_x();
+      ran_x = true;
+    }
+  }
+  if (!ran_x) {
+    if (mfma_on) kloop(std::true_type{});
+    else kloop(std::false_type{});
+  }
 
   // K pieces of a tail tile meet through the workspace: each writes its
   // sums, then bumps the tile's arrival counter; the last to arrive adds the
@@ -824,6 +944,17 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
           }
       }
     };
+    // absorbed rows: each up wave (odd wt) leaves its block in LDS past the
+    // staged tile, lane-major, for the gate wave of the same features
+    float* const xst = reinterpret_cast<float*>(smem + 65536) + (2 * ww + (wt >> 1)) * 1024;
+    auto stage_x = [&]() __attribute__((always_inline)) {
+      if constexpr (kExt) {
+        if (ext && (wt & 1)) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) xst[e * 64 + lane] = accx[e];
+        }
+      }
+    };
     if (kSplit != 1 && pieces > 1) {
       // last piece of a split tile: every wave is in step and past the rings
       merge_block(0);
@@ -832,10 +963,12 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       lds_barrier();
     } else if (!late) {
       stage();
+      stage_x();
       lds_barrier();
       lds_barrier();
     } else {
       stage();
+      stage_x();
       lds_barrier();
     }
     // write-out: wave w stores rows 32w .. 32w + 31, 4 rows (16 lanes x 16
@@ -850,6 +983,26 @@ __global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2))) 
       if (jr < row_hi && fok)
         *reinterpret_cast<u32x4_t*>(a.out + (int64_t)map_row(jr, a.omap1, a.omap2) * a.out_ld +
                                     (int64_t)(f0 + 8 * cc) * 2) = v;
+    }
+    if constexpr (kExt) {
+      // absorbed rows: the gate waves (even wt) apply SwiGLU with the up
+      // values of their partner and store rows row_lo + 256 + (lane & 31)
+      const int jr = row_lo + kTR + lrow;
+      if (ext && !(wt & 1) && jr < row_hi) {
+        const int fb = f0 + 32 * (2 * ww + (wt >> 1)) + 4 * lhalf;
+        char* const orow = a.out + (int64_t)map_row(jr, a.omap1, a.omap2) * a.out_ld;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          if (fb + 8 * g >= n_feat) continue;
+          float v[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = silu_f32(accx[4 * g + k]) * xst[(4 * g + k) * 64 + lane];
+          u32x2_t o;
+          o.x = pack_bf16(v[0], v[1]);
+          o.y = pack_bf16(v[2], v[3]);
+          *reinterpret_cast<u32x2_t*>(orow + (int64_t)(fb + 8 * g) * 2) = o;
+        }
+      }
     }
     if (a.sal_part) {
       // ---- FFN-pruning signal (Eq. 8): per segment of the tile (a run of
@@ -1034,19 +1187,34 @@ __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, 
 // Split plan of a ping-pong launch: whole tiles in full rounds per XCD, the
 // partial last round as K pieces when the workspace holds their partial sums
 // (see GemmSplit).
+// Gate/up without the pruning sums absorbs a short last token tile
+// (gateup_token_tiles) when its plan runs whole tiles only.
 template <int kMode>
 GemmSplit pp2_plan(const FfnGemmArgs& a, int* n_tt, int* n_ft) {
   constexpr int kFTile = (kMode == 0) ? 128 : 256;
-  *n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
   *n_ft = (a.n_feat + kFTile - 1) / kFTile;
-  const int64_t items = (int64_t)*n_tt * *n_ft;
-  if (a.part && a.tile_cnt) return gemm_split(items, a.k_bytes / 128);
-  GemmSplit sp;
-  sp.per_x = (int)((items + kXcds - 1) / kXcds);
-  sp.whole_x = sp.per_x;
-  sp.tail_x = 0;
-  sp.pieces = 1;
-  return sp;
+  auto plan = [&](int ntt) {
+    const int64_t items = (int64_t)ntt * *n_ft;
+    if (a.part && a.tile_cnt) return gemm_split(items, a.k_bytes / 128);
+    GemmSplit sp;
+    sp.per_x = (int)((items + kXcds - 1) / kXcds);
+    sp.whole_x = sp.per_x;
+    sp.tail_x = 0;
+    sp.pieces = 1;
+    sp.absorb = 0;
+    return sp;
+  };
+  if (kMode == 0 && !a.sal_part) {
+    const int ntt = gateup_token_tiles(a.cap, true) + (a.n_sets - 1);
+    GemmSplit sp = plan(ntt);
+    if (sp.pieces == 1) {
+      sp.absorb = 1;
+      *n_tt = ntt;
+      return sp;
+    }
+  }
+  *n_tt = (a.cap + 255) / 256 + (a.n_sets - 1);
+  return plan(*n_tt);
 }
 
 template <int kMode, int kGroup, bool kPrio, int kWBufs = 2, bool kSpreadW = true, bool kSpreadT = true,

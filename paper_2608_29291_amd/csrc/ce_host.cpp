@@ -21,6 +21,7 @@ GemmSplit gemm_split(int64_t items, int ns) {
   sp.whole_x = sp.per_x;
   sp.tail_x = 0;
   sp.pieces = 1;
+  sp.absorb = 0;
   if (items <= 0 || ns < 6) return sp;
   const int full = sp.per_x / kCusPerXcd * kCusPerXcd;
   const int tail = sp.per_x - full;

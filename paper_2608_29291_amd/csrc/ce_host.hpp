@@ -58,6 +58,8 @@ struct GemmSplit {
   int whole_x;  // whole items per XCD
   int tail_x;   // split items per XCD
   int pieces;   // workgroups per split item
+  int absorb;   // gate/up, whole tiles only: a last token tile of at most 32
+                // rows joins the tile before it (see gateup_token_tiles)
 };
 // Chosen by a cost model in units of one superslab's K-loop time: a whole
 // tile costs ns + 3.5 (prologue, epilogue); a piece ns / S + 2 (its partial
