@@ -118,4 +118,3 @@ def test_block_absorbed_tail(G, kind, n):
     err, swaps = G.check_block(wl, r)
     print(f"[block tail {kind}] rows of the first set {n} (packed {int(r['koff'][-1])}) "
           f"rel err {err:.3e} swaps {swaps}", flush=True)
-
