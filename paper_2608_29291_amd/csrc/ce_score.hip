@@ -69,9 +69,15 @@ __device__ __forceinline__ void find_tile(const ScoreArgs& a, int tile, int* sh,
   lo = hi = 0;
   for (int s0 = 0; s0 < a.B; s0 += 256) {
     const int cnt = min(256, a.B - s0);
-    if (tid <= cnt) {
+    // offsets s0 .. s0 + cnt: one per thread, and the chunk's end offset (index
+    // cnt, which a full chunk of 256 has no thread for) from thread 0
+    if (tid < cnt) {
       int o = a.seq_offsets[s0 + tid];
       sh[tid] = o < 0 ? 0 : (o > a.T ? a.T : o);
+    }
+    if (tid == 0) {
+      int o = a.seq_offsets[s0 + cnt];
+      sh[cnt] = o < 0 ? 0 : (o > a.T ? a.T : o);
     }
     __syncthreads();
     int prev = sh[0];

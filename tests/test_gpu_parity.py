@@ -191,6 +191,53 @@ def test_topk_many_sequences(G):
     check_topk_exact(G, wl, l32)
 
 
+def _max_batch_workload(seed, n_sets=1):
+    """65535 sequences (the most the ABI takes: grids carry the sequence
+    index in y) of 0-3 tokens each, every flag combination."""
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, 4, size=65535)
+    kinds = rng.integers(0, 4, size=65535)
+    flag = [0, TOK_GEN, TOK_KEEP, TOK_KEEP | TOK_GEN]
+    segs = [[(int(n), flag[int(k)])] for n, k in zip(lens, kinds)]
+    return make_workload("max-batch", segs, d=64, F=64, r_c=32, r_e=32, keep=0.5, dtype="bf16", seed=seed + 1,
+                         n_sets=n_sets)
+
+
+def test_topk_max_batch(G):
+    """TopK and packing at the largest batch, bit-exact against the oracle's
+    selection on the same logits."""
+    wl = _max_batch_workload(11)
+    assert wl.B == 65535
+    l32 = np.random.default_rng(13).standard_normal(wl.T).astype(np.float32)
+    check_topk_exact(G, wl, l32)
+
+
+@pytest.mark.parametrize("n_sets", [1, 2])
+def test_block_max_batch(G, n_sets):
+    """The fused block at the largest batch (scorer summaries, TopK, MoT
+    grouping and both GEMMs over ~75K packed rows) against the oracle."""
+    wl = _max_batch_workload(21, n_sets)
+    r = run_block(G, wl)
+    err, swaps = check_block(G, wl, r)
+    print(f"[block max batch n_sets={n_sets}] T={wl.T} rel err {err:.3e} swaps {swaps}", flush=True)
+
+
+@pytest.mark.parametrize("nb", [255, 256, 257, 513])
+def test_block_sequence_chunk_edges(G, nb):
+    """Batches around the scorer's 256-sequence walk chunks (the last
+    sequence of a full chunk needs the chunk's end offset), against the
+    oracle."""
+    rng = np.random.default_rng(nb)
+    lens = rng.integers(1, 6, size=nb)
+    kinds = rng.integers(0, 4, size=nb)
+    flag = [0, TOK_GEN, TOK_KEEP, TOK_KEEP | TOK_GEN]
+    wl = make_workload("chunk-edges", [[(int(n), flag[int(k)])] for n, k in zip(lens, kinds)], d=64, F=64, r_c=32,
+                       r_e=32, keep=0.5, dtype="bf16", seed=nb + 1)
+    r = run_block(G, wl)
+    err, swaps = check_block(G, wl, r)
+    print(f"[block chunk edges B={nb}] rel err {err:.3e} swaps {swaps}", flush=True)
+
+
 def test_topk_gather(G):
     wl = small_workload("mixed", seed=5, dtype="bf16", d=192, F=64, r_c=32, r_e=32)
     _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
