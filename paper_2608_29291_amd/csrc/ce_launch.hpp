@@ -158,6 +158,9 @@ struct SelectArgs {
   // counters of the following gate/up launch, cleared by workgroup 0 (or NULL)
   int32_t* clear_cnt;
   int clear_n;
+  // set by launch_select: kept_offsets[b] and the status word were already
+  // written by the sequence-offset scan (large batches)
+  int offs_ready;
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream);
 

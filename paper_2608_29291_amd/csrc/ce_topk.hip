@@ -61,6 +61,7 @@ __device__ __forceinline__ int64_t seq_kept(const SelectArgs& a, int len, int w)
 // Packed offset of sequence b (sum of K_b' over b' < b) by one wave, given
 // the sizes of sequence `lane` (loaded early by the caller, zero past b).
 __device__ __forceinline__ int64_t seq_offset_wave(const SelectArgs& a, int b, int lane, int len0, int w0) {
+  if (a.offs_ready) return (int64_t)a.kept_offsets[b];  // from the sequence-offset scan
   int64_t part = lane < b ? seq_kept(a, len0, w0) : 0;
   for (int s = lane + 64; s < b; s += 64) part += seq_kept(a, a.info[3 * s + 1], a.info[3 * s + 2]);
   for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
@@ -228,9 +229,9 @@ __device__ __forceinline__ void select_body_lds(const SelectArgs& a, SelShared& 
   // wave 15 sums the packed offset of this sequence and wave 14 (sequence 0)
   // the batch status; the sizes of sequence `lane` are loaded now, so that
   // their latency overlaps the key loads below
-  const bool off_wave = wave == kSelWaves - 1, st_wave = wave == kSelWaves - 2 && b == 0;
+  const bool off_wave = wave == kSelWaves - 1, st_wave = wave == kSelWaves - 2 && b == 0 && !a.offs_ready;
   int len0 = 0, w0 = 0;
-  if ((off_wave && lane < b) || (st_wave && lane < a.B)) {
+  if ((off_wave && lane < b && !a.offs_ready) || (st_wave && lane < a.B)) {
     len0 = a.info[3 * lane + 1];
     w0 = a.info[3 * lane + 2];
   }
@@ -556,9 +557,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   }
 
   // ---- long sequence: packed offset of this sequence first ----
-  int64_t part = 0;
-  for (int s = tid; s < b; s += kSelThreads) part += seq_kept(a, a.info[3 * s + 1], a.info[3 * s + 2]);
-  const int64_t off_b = block_sum_i64(part, sh.scratch);
+  int64_t off_b;
+  if (a.offs_ready) {
+    off_b = (int64_t)a.kept_offsets[b];
+  } else {
+    int64_t part = 0;
+    for (int s = tid; s < b; s += kSelThreads) part += seq_kept(a, a.info[3 * s + 1], a.info[3 * s + 2]);
+    off_b = block_sum_i64(part, sh.scratch);
+  }
   const int64_t k_b = nkeep + num_keep_dev(a.keep, len - nkeep);
   if (tid == 0) {
     a.kept_offsets[b] = (int32_t)(off_b < 0x7fffffff ? off_b : 0x7fffffff);
@@ -567,11 +573,56 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
       a.kept_offsets[a.B] = (int32_t)(tot < 0x7fffffff ? tot : 0x7fffffff);
     }
   }
-  if (b == 0 && (tid >> 6) == 0) {
+  if (b == 0 && (tid >> 6) == 0 && !a.offs_ready) {
     const int l0 = (tid < a.B) ? a.info[3 * tid + 1] : 0, w0 = (tid < a.B) ? a.info[3 * tid + 2] : 0;
     batch_status_wave(a, tid & 63, l0, w0);
   }
   select_body_global(a, sh, lo, len, nkeep, off_b);
+}
+
+// Packed offset of every sequence for large batches, in one workgroup:
+// kept_offsets[b] = sum of the retained rows of sequences 0 .. b - 1 (the
+// value the select kernel writes there too), kept_offsets[B] = the total, and
+// the batch status word. Without it each select workgroup sums its earlier
+// sequences itself, which costs O(B) per workgroup. Thread t takes a run of
+// ceil(B / 1024) consecutive sequences; the runs are scanned in order.
+__global__ __launch_bounds__(1024) void seq_offsets_kernel(SelectArgs a) {
+  __shared__ int64_t wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int per = (a.B + 1023) / 1024;
+  const int s0 = min(tid * per, a.B), s1 = min(s0 + per, a.B);
+  int64_t loc = 0;
+  int bad = 0;
+  for (int s = s0; s < s1; ++s) {
+    const int w = a.info[3 * s + 2];
+    bad |= w < 0 ? 1 : 0;
+    loc += seq_kept(a, a.info[3 * s + 1], w);
+  }
+  int64_t incl = loc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  const int any_bad = __syncthreads_or(bad);
+  int64_t before = 0, total = 0;
+  for (int w = 0; w < 16; ++w) {
+    before += w < wave ? wsum[w] : 0;
+    total += wsum[w];
+  }
+  int64_t run = before + incl - loc;
+  for (int s = s0; s < s1; ++s) {
+    a.kept_offsets[s] = (int32_t)(run < 0x7fffffff ? run : 0x7fffffff);
+    run += seq_kept(a, a.info[3 * s + 1], a.info[3 * s + 2]);
+  }
+  if (tid == 0) {
+    a.kept_offsets[a.B] = (int32_t)(total < 0x7fffffff ? total : 0x7fffffff);
+    uint32_t st = 0;
+    if (any_bad) st |= 1u;
+    if (total > a.cap) st |= 2u;
+    *a.status = st;
+  }
 }
 
 // Stable partition of packed rows by FFN set: grp_rows lists set-0 rows first
@@ -649,8 +700,19 @@ hipError_t launch_seq_info(const int32_t* seq_offsets, const uint8_t* flags, int
   return hipGetLastError();
 }
 
+// Batches above this many sequences get the sequence-offset scan first.
+constexpr int kSeqScanMinB = 1024;
+
 hipError_t launch_select(const SelectArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3(a.B), dim3(kSelThreads), 0, stream, a);
+  SelectArgs s = a;
+  s.offs_ready = 0;
+  if (a.B > kSeqScanMinB) {
+    hipLaunchKernelGGL(seq_offsets_kernel, dim3(1), dim3(1024), 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    s.offs_ready = 1;
+  }
+  hipLaunchKernelGGL(select_kernel, dim3(s.B), dim3(kSelThreads), 0, stream, s);
   return hipGetLastError();
 }
 

@@ -212,6 +212,44 @@ def test_topk_max_batch(G):
     check_topk_exact(G, wl, l32)
 
 
+@pytest.mark.parametrize("nb", [1024, 1025, 3000])
+def test_topk_batch_offsets(G, nb):
+    """Batches on both sides of the size above which the packed offsets come
+    from one scan over the sequences instead of each select workgroup:
+    bit-exact against the oracle's selection."""
+    rng = np.random.default_rng(nb + 7)
+    lens = rng.integers(0, 9, size=nb)
+    kinds = rng.integers(0, 4, size=nb)
+    flag = [0, TOK_GEN, TOK_KEEP, TOK_KEEP | TOK_GEN]
+    wl = make_workload("batch-offsets", [[(int(n), flag[int(k)])] for n, k in zip(lens, kinds)], d=64, F=64,
+                       r_c=32, r_e=32, keep=0.4, dtype="bf16", seed=nb)
+    l32 = rng.standard_normal(wl.T).astype(np.float32)
+    check_topk_exact(G, wl, l32)
+
+
+def test_topk_overflow_large_batch(G):
+    """kept_capacity below Kt on a batch that takes the offset scan: the
+    status flag is set, nothing is written past the capacity, and the offsets
+    are the oracle's."""
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = _max_batch_workload(31)
+    l32 = np.random.default_rng(32).standard_normal(wl.T).astype(np.float32)
+    ref = oracle.select(l32, wl.flags, wl.seq_offsets, wl.keep)
+    cap = len(ref["kept_idx"]) - 1001
+    dw = G.DevWorkload(wl, kept_capacity=cap)
+    guard = torch.full((cap + 64,), -5, dtype=torch.int32, device="cuda")
+    kept_off = torch.empty(wl.B + 1, dtype=torch.int32, device="cuda")
+    ws = dw.ws(ce.CE_WS_TOPK)
+    ce.ce_topk_compact(dw.batch, G.to_dev(l32), guard[:cap], kept_off, ws)
+    torch.cuda.synchronize()
+    assert ce.ce_workspace_status(ws) & ce.CE_DEV_OVERFLOW
+    g = G.host(guard)
+    np.testing.assert_array_equal(g[:cap], ref["kept_idx"][:cap])
+    assert np.all(g[cap:] == -5)
+    np.testing.assert_array_equal(G.host(kept_off), ref["kept_offsets"])
+
+
 @pytest.mark.parametrize("n_sets", [1, 2])
 def test_block_max_batch(G, n_sets):
     """The fused block at the largest batch (scorer summaries, TopK, MoT
