@@ -56,47 +56,6 @@ __device__ __forceinline__ void wait_vm(int n) {
   else wait_vm_upto<48>(n);
 }
 
-// Locate tile `tile` among the per-sequence tilings into kTile tokens:
-// sequence b, tokens [lo, hi).
-// The offsets are read into LDS 256 sequences at a time (one load per thread),
-// then every thread walks them: one memory latency plus a few LDS reads per
-// sequence.
-template <int kTile>
-__device__ __forceinline__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo, int& hi) {
-  const int tid = threadIdx.x;
-  int base = 0;  // tiles before the current chunk of sequences
-  b = -1;
-  lo = hi = 0;
-  for (int s0 = 0; s0 < a.B; s0 += 256) {
-    const int cnt = min(256, a.B - s0);
-    // offsets s0 .. s0 + cnt: one per thread, and the chunk's end offset (index
-    // cnt, which a full chunk of 256 has no thread for) from thread 0
-    if (tid < cnt) {
-      int o = a.seq_offsets[s0 + tid];
-      sh[tid] = o < 0 ? 0 : (o > a.T ? a.T : o);
-    }
-    if (tid == 0) {
-      int o = a.seq_offsets[s0 + cnt];
-      sh[cnt] = o < 0 ? 0 : (o > a.T ? a.T : o);
-    }
-    __syncthreads();
-    int prev = sh[0];
-    for (int j = 0; j < cnt; ++j) {
-      int se = sh[j + 1];
-      se = se < prev ? prev : se;
-      const int nt = (se - prev + kTile - 1) / kTile;
-      if (b < 0 && tile < base + nt) {
-        b = s0 + j;
-        lo = prev + (tile - base) * kTile;
-        hi = min(lo + kTile, se);
-      }
-      base += nt;
-      prev = se;
-    }
-    __syncthreads();  // sh is refilled by the next chunk
-    if (b >= 0) return;
-  }
-}
 
 // Exclusive prefix sum over the 256 threads of a workgroup (4 waves), plus
 // the total; scr: 4 ints of LDS. Every thread must call it.
@@ -115,6 +74,54 @@ __device__ __forceinline__ int block_excl_scan(int v, int* scr, int& total) {
   total = (scr[0] + scr[1]) + (scr[2] + scr[3]);
   __syncthreads();  // scr is free again
   return before + x - v;
+}
+
+// Sequence b and token range [lo, hi) of token tile `tile`: the tiles of a
+// sequence are ceil(len / kTile) consecutive ones, sequences in order. The
+// walk takes 256 sequences at a time: one tile count per thread, a block scan,
+// and a chunk whose total lies below `tile` is skipped whole (the next
+// chunk's offsets are loaded before the scan, so their latency overlaps it).
+// Offsets are clamped into [0, T] and an end below its start counts as an
+// empty sequence. Every thread must call it; sh: 260 ints of LDS.
+template <int kTile>
+__device__ __forceinline__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo, int& hi) {
+  const int tid = threadIdx.x;
+  auto clampT = [&](int o) { return o < 0 ? 0 : (o > a.T ? a.T : o); };
+  int base = 0;  // tiles before the current chunk of sequences
+  int l0 = 0, l1 = 0;
+  if (tid < a.B) {
+    l0 = clampT(a.seq_offsets[tid]);
+    l1 = clampT(a.seq_offsets[tid + 1]);
+  }
+  for (int s0 = 0; s0 < a.B; s0 += 256) {
+    const int cnt = min(256, a.B - s0);
+    const int c0 = l0, c1 = l1 < l0 ? l0 : l1;
+    // the next chunk's offsets
+    if (s0 + 256 + tid < a.B) {
+      l0 = clampT(a.seq_offsets[s0 + 256 + tid]);
+      l1 = clampT(a.seq_offsets[s0 + 256 + tid + 1]);
+    }
+    const int nt = tid < cnt ? (c1 - c0 + kTile - 1) / kTile : 0;
+    int total;
+    const int ex = block_excl_scan(nt, sh + 256, total);
+    if (tile < base + total) {
+      if (tid < cnt && tile >= base + ex && tile < base + ex + nt) {
+        const int t0 = c0 + (tile - base - ex) * kTile;
+        sh[0] = s0 + tid;
+        sh[1] = t0;
+        sh[2] = min(t0 + kTile, c1);
+      }
+      __syncthreads();
+      b = sh[0];
+      lo = sh[1];
+      hi = sh[2];
+      __syncthreads();  // sh is free again
+      return;
+    }
+    base += total;
+  }
+  b = -1;
+  lo = hi = 0;
 }
 
 // The rank-tiled scorer's live work items. A token tile (kTile tokens of one
