@@ -75,6 +75,25 @@ struct AttnArgs {
 
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
+// Exclusive prefix sum over the 256 threads of the workgroup, plus the total
+// (scr: 4 ints of LDS). Every thread must call it.
+__device__ __forceinline__ int excl_scan256(int v, int* scr, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) scr[wave] = x;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += scr[w];
+  total = (scr[0] + scr[1]) + (scr[2] + scr[3]);
+  __syncthreads();
+  return before + x - v;
+}
+
 __device__ __forceinline__ uint32_t vkey_of(int d) { return (uint32_t)((d >> 1) & 15); }
 __device__ __forceinline__ uint32_t vt_off(int d, uint32_t unit) {  // byte offset of V^T row d, unit
   return (uint32_t)((d >> 5) * kVBlk + (d & 31) * kVRow) + ((unit ^ vkey_of(d)) << 3);
@@ -91,19 +110,63 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const int h = blockIdx.y;
   const int kvh = h / (a.H / a.Hkv);
 
-  // ---- which sequence and query tile: walk the per-sequence tile counts ----
-  int t = blockIdx.x, b = -1, q0 = 0, nq = 0, qbase = 0;
-  for (int s = 0; s < a.B; ++s) {
-    const int lo = clampi(a.qo[s], 0, a.q_cap), hi = clampi(a.qo[s + 1], lo, a.q_cap);
-    const int tiles = (hi - lo + kQT - 1) / kQT;
-    if (t < tiles) {
-      b = s;
-      q0 = (tiles - 1 - t) * kQT;  // last tiles first: under a causal mask they see the most keys
-      nq = hi - lo;
-      qbase = lo;
-      break;
+  // ---- which sequence and query tile: the per-sequence tile counts; for
+  //      more than 32 sequences 256 at a time (one per thread, a block scan;
+  //      a chunk below this workgroup's tile is skipped whole, and the next
+  //      chunk's offsets are loaded before the scan). The LDS is free until
+  //      the first K tile. ----
+  const int t = blockIdx.x;
+  int b = -1, q0 = 0, nq = 0, qbase = 0;
+  if (a.B <= 32) {
+    // a few sequences: every thread walks them (no barrier)
+    int tt = t;
+    for (int s = 0; s < a.B; ++s) {
+      const int lo = clampi(a.qo[s], 0, a.q_cap), hi = clampi(a.qo[s + 1], lo, a.q_cap);
+      const int tiles = (hi - lo + kQT - 1) / kQT;
+      if (tt < tiles) {
+        b = s;
+        q0 = (tiles - 1 - tt) * kQT;  // last tiles first: under a causal mask they see the most keys
+        nq = hi - lo;
+        qbase = lo;
+        break;
+      }
+      tt -= tiles;
     }
-    t -= tiles;
+  } else {
+    int* const wsh = reinterpret_cast<int*>(smem);
+    int lo = 0, hi = 0;
+    if (tid < a.B) {
+      lo = clampi(a.qo[tid], 0, a.q_cap);
+      hi = clampi(a.qo[tid + 1], lo, a.q_cap);
+    }
+    int base = 0;  // tiles of the chunks before
+    for (int s0 = 0; s0 < a.B; s0 += 256) {
+      const int cnt = min(256, a.B - s0);
+      const int clo = lo, chi = hi;
+      if (s0 + 256 + tid < a.B) {
+        lo = clampi(a.qo[s0 + 256 + tid], 0, a.q_cap);
+        hi = clampi(a.qo[s0 + 256 + tid + 1], lo, a.q_cap);
+      }
+      const int nt = tid < cnt ? (chi - clo + kQT - 1) / kQT : 0;
+      int total;
+      const int ex = excl_scan256(nt, wsh, total);
+      if (t < base + total) {
+        if (tid < cnt && t >= base + ex && t < base + ex + nt) {
+          wsh[4] = s0 + tid;
+          wsh[5] = (nt - 1 - (t - base - ex)) * kQT;  // last tiles first: under a causal mask they see the most keys
+          wsh[6] = chi - clo;
+          wsh[7] = clo;
+        }
+        __syncthreads();
+        b = wsh[4];
+        q0 = wsh[5];
+        nq = wsh[6];
+        qbase = wsh[7];
+        __syncthreads();  // the LDS goes to the K / V tiles
+        break;
+      }
+      base += total;
+    }
   }
   if (b < 0) return;
   b = __builtin_amdgcn_readfirstlane(b);

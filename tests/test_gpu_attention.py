@@ -55,6 +55,20 @@ def test_ragged_prefill(G, causal, H, Hkv):
     check(got, oa.attention(q, k, v, qo, ko, Hkv, causal, scale), v)
 
 
+@pytest.mark.parametrize("causal", [False, True])
+def test_many_sequences(G, causal):
+    """700 ragged sequences (several 256-sequence chunks of the workgroups'
+    tile walk, empty ones included)."""
+    rng = np.random.default_rng(70 + causal)
+    lens = [int(x) for x in rng.integers(0, 60, size=700)]
+    lens[255] = lens[256] = 0
+    lens[300] = lens[511] = 300  # several query tiles
+    q, k, v, qo, ko = make_attention_inputs(lens, lens, 4, 2, DH, seed=71 + causal)
+    got, scale = run(G, q, k, v, qo, ko, causal)
+    print(f"[attn many sequences causal={causal}] T={sum(lens)}")
+    check(got, oa.attention(q, k, v, qo, ko, 2, causal, scale), v)
+
+
 @pytest.mark.parametrize("q_lens,kv_lens", [([1, 1, 1, 1], [550, 2176, 1, 63]),       # decode steps
                                            ([200, 3, 64], [550, 3, 700]),            # chunked prefill
                                            ([5, 7], [0, 9]),                         # a sequence with no keys
