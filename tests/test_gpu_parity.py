@@ -276,6 +276,22 @@ def test_block_sequence_chunk_edges(G, nb):
     print(f"[block chunk edges B={nb}] rel err {err:.3e} swaps {swaps}", flush=True)
 
 
+@pytest.mark.parametrize("last", [260, 96])
+@pytest.mark.parametrize("only", ["understanding", "generation"])
+def test_block_mot_one_empty_set(G, only, last):
+    """Two FFN weight sets with every packed row in one of them (the other
+    set's row count is 0), on the ping-pong GEMMs (d = 256), against the
+    oracle; 352 packed rows, or 270 (a short last token tile that the gate/up
+    tile before it takes)."""
+    f = 0 if only == "understanding" else TOK_GEN
+    segs = [[(300, f), (20, f | TOK_KEEP)], [(97, f)], [(last, f), (3, f | TOK_KEEP)]]
+    wl = make_workload("mot-one-set", segs, d=256, F=512, r_c=32, r_e=32, keep=0.5, dtype="bf16", seed=44,
+                       n_sets=2)
+    r = run_block(G, wl)
+    err, swaps = check_block(G, wl, r)
+    print(f"[block MoT only {only}] Kt={int(r['koff'][-1])} rel err {err:.3e} swaps {swaps}", flush=True)
+
+
 def test_topk_gather(G):
     wl = small_workload("mixed", seed=5, dtype="bf16", d=192, F=64, r_c=32, r_e=32)
     _, l32 = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
