@@ -230,6 +230,7 @@ int routed_block_impl(const ce_batch* batch, const void* hidden_in, void* hidden
   //    bytes per workgroup; the TopK step adds them up.
   ScoreArgs sa = make_score_args(batch, hidden_in, scorer, logits, nullptr);
   sa.info = info;
+  sa.tile_start = at<int32_t>(ws, L.tile_start);
   int tm = 0, tn = 0;
   const bool tiled = bf16 && score_tiling(batch->B, batch->T, scorer->d, scorer->r_core, scorer->r_exp, elem,
                                           &tm, &tn, &sa.n_ct, &sa.n_rt);
@@ -343,6 +344,7 @@ int ce_score_ws(const ce_batch* batch, const void* hidden, const ce_scorer_w* w,
   if (batch->T == 0) return CE_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   ScoreArgs a = make_score_args(batch, hidden, w, logits, probs);
+  a.tile_start = at<int32_t>(ws, L.tile_start);
   const bool bf16 = w->dtype == CE_BF16;
   int tm = 0, tn = 0;
   if (!(bf16 && score_tiling(batch->B, batch->T, w->d, w->r_core, w->r_exp, elem, &tm, &tn, &a.n_ct, &a.n_rt)))

@@ -132,6 +132,7 @@ WsLayout ws_layout(int which, int B, int T, int cap, int d, int d_ff, int elem) 
   L.status = take(16);
   if (which == CE_WS_TOPK || block) L.seq_info = take(3 * sB * 4);
   if (which == CE_WS_SCORE) L.score_part = take((size_t)kScoreMaxTiles * sT * 4);
+  if (which == CE_WS_SCORE || block) L.tile_start = take((sB + 1) * 4);
   if (block) {
     L.kept_off = take((sB + 1) * 4);
     L.kept_idx = take(sC * 4);

@@ -18,6 +18,7 @@ constexpr int kMaxSeg = 16;
 struct WsLayout {
   size_t status;     // uint32 status word (+ padding)
   size_t seq_info;   // int32 [3 * B]
+  size_t tile_start; // int32 [B + 1] first token tile of each sequence (single-launch scorer, B > 1024)
   size_t kept_off;   // int32 [B + 1]  (block path, when the caller passes none)
   size_t kept_idx;   // int32 [cap]    (block path)
   size_t token_pos;  // int32 [T]      (block path)

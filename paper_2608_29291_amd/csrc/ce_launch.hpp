@@ -122,6 +122,10 @@ struct ScoreArgs {
   // 0 .. n_ct - 1 over the core ranks, the rest over the expansion ranks
   float* part;
   int n_ct, n_rt;
+  // single-launch scorer: room for the first token tile of each sequence
+  // [B + 1] (or NULL); above 1024 sequences launch_score fills it first and
+  // each workgroup looks its tile up there instead of walking the sequences
+  int32_t* tile_start;
 };
 hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream);
 // Rank-tiled scorer (bf16): tiles of tm tokens x tn ranks (tm, tn in {64, 128})

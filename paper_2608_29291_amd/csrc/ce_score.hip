@@ -87,6 +87,31 @@ template <int kTile>
 __device__ __forceinline__ void find_tile(const ScoreArgs& a, int tile, int* sh, int& b, int& lo, int& hi) {
   const int tid = threadIdx.x;
   auto clampT = [&](int o) { return o < 0 ? 0 : (o > a.T ? a.T : o); };
+  if (a.tile_start) {
+    // the first tiles of the sequences in the workspace (non-decreasing):
+    // sequence b is the last with tile_start[b] <= tile, found in two steps
+    // over 256 entries each (a count of the entries at or below `tile`)
+    const int* ts = a.tile_start;
+    const int C = (a.B + 256) / 256;  // entries 0 .. B in 256 runs of C
+    const int i0 = tid * C;
+    const int c1 = __syncthreads_count(i0 <= a.B && ts[min(i0, a.B)] <= tile);
+    const int r0 = (c1 - 1) * C;  // the answer lies in [r0, r0 + C)
+    const int j = r0 + tid;
+    const int c2 = __syncthreads_count(tid < C && j <= a.B && ts[min(j, a.B)] <= tile);
+    const int s = r0 + c2 - 1;
+    if (c1 == 0 || s >= a.B) {
+      b = -1;
+      lo = hi = 0;
+      return;
+    }
+    b = s;
+    const int s0 = clampT(a.seq_offsets[s]);
+    int s1 = clampT(a.seq_offsets[s + 1]);
+    s1 = s1 < s0 ? s0 : s1;
+    lo = s0 + (tile - ts[s]) * kTile;
+    hi = min(lo + kTile, s1);
+    return;
+  }
   int base = 0;  // tiles before the current chunk of sequences
   int l0 = 0, l1 = 0;
   if (tid < a.B) {
@@ -767,9 +792,60 @@ __global__ __launch_bounds__(256) void score_tile_kernel(ScoreArgs a) {
 
 }  // namespace
 
-hipError_t launch_score(const ScoreArgs& a, bool bf16, hipStream_t stream) {
-  if (a.T == 0 && !a.info) return hipSuccess;
+// First token tile of each sequence into out[0 .. B] (out[B] = all tiles),
+// in one workgroup: thread t takes a run of ceil(B / 1024) sequences, the runs
+// are scanned in order. Offsets are clamped as find_tile clamps them.
+__global__ __launch_bounds__(1024) void tile_start_kernel(const int32_t* __restrict__ offs, int B, int T,
+                                                         int tile, int32_t* __restrict__ out) {
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  auto clampT = [&](int o) { return o < 0 ? 0 : (o > T ? T : o); };
+  auto tiles_of = [&](int s) {
+    const int s0 = clampT(offs[s]);
+    int s1 = clampT(offs[s + 1]);
+    s1 = s1 < s0 ? s0 : s1;
+    return (s1 - s0 + tile - 1) / tile;
+  };
+  const int per = (B + 1023) / 1024;
+  const int r0 = min(tid * per, B), r1 = min(r0 + per, B);
+  int loc = 0;
+  for (int s = r0; s < r1; ++s) loc += tiles_of(s);
+  int incl = loc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int w = 0; w < 16; ++w) {
+    before += w < wave ? wsum[w] : 0;
+    total += wsum[w];
+  }
+  int run = before + incl - loc;
+  for (int s = r0; s < r1; ++s) {
+    out[s] = run;
+    run += tiles_of(s);
+  }
+  if (tid == 0) out[B] = total;
+}
+
+// Batches above this many sequences look their tiles up in tile_start.
+constexpr int kTileScanMinB = 1024;
+
+hipError_t launch_score(const ScoreArgs& a0, bool bf16, hipStream_t stream) {
+  if (a0.T == 0 && !a0.info) return hipSuccess;
+  ScoreArgs a = a0;
   const int tm = score_token_tile(a.B, a.T, a.k_bytes / (bf16 ? 2 : 4), a.r_core, a.r_exp, bf16 ? 2 : 4);
+  if (a.tile_start && a.B > kTileScanMinB) {
+    hipLaunchKernelGGL(tile_start_kernel, dim3(1), dim3(1024), 0, stream, a.seq_offsets, a.B, a.T, tm,
+                       a.tile_start);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else {
+    a.tile_start = nullptr;
+  }
   const int tiles = (a.T + tm - 1) / tm + a.B + (a.info ? a.B : 0);  // >= the tile count (+ summaries)
   if (bf16 && tm == 128)
     hipLaunchKernelGGL((score_kernel<true, 128>), dim3(tiles), dim3(256), 0, stream, a);

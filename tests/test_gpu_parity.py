@@ -250,6 +250,50 @@ def test_topk_overflow_large_batch(G):
     np.testing.assert_array_equal(G.host(kept_off), ref["kept_offsets"])
 
 
+def _many_sequences(nb, seed, n_sets=1):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, 7, size=nb)
+    kinds = rng.integers(0, 4, size=nb)
+    flag = [0, TOK_GEN, TOK_KEEP, TOK_KEEP | TOK_GEN]
+    return make_workload("many-seq", [[(int(n), flag[int(k)])] for n, k in zip(lens, kinds)], d=64, F=64, r_c=32,
+                         r_e=32, keep=0.5, dtype="bf16", seed=seed + 1, n_sets=n_sets)
+
+
+def test_score_tile_lookup_matches_walk(G):
+    """Above 1024 sequences the workspace scorer (ce_score_ws) looks its token
+    tiles up in a scanned table; the workspace-free ce_score walks the
+    sequences. Same kernel otherwise: logits and probs equal bit for bit, and
+    the oracle's logits within the bar."""
+    import torch
+    import paper_2608_29291_amd as ce
+    wl = _many_sequences(3000, 61)
+    dw = G.DevWorkload(wl)
+    outs = []
+    for with_ws in (False, True):
+        lg = torch.full((wl.T,), float("nan"), device="cuda")
+        pr = torch.full((wl.T,), float("nan"), device="cuda")
+        if with_ws:
+            ce.ce_score_ws(dw.batch, dw.hidden, dw.scorer, lg, dw.ws(ce.CE_WS_SCORE), probs=pr)
+        else:
+            ce.ce_score(dw.batch, dw.hidden, dw.scorer, lg, probs=pr)
+        torch.cuda.synchronize()
+        outs.append((G.host(lg), G.host(pr)))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+    l64, _ = oracle.score(wl.hidden, wl.flags, wl.seq_offsets, wl.t, wl.scorer)
+    assert G.logit_err(outs[1][0], l64) <= G.LOGIT_TOL["bf16"]
+
+
+@pytest.mark.parametrize("n_sets", [1, 2])
+def test_block_many_sequences(G, n_sets):
+    """The fused block at 2000 sequences (table lookup of the scorer's tiles,
+    offsets of the select step from one scan) against the oracle."""
+    wl = _many_sequences(2000, 71, n_sets)
+    r = run_block(G, wl)
+    err, swaps = check_block(G, wl, r)
+    print(f"[block 2000 sequences n_sets={n_sets}] rel err {err:.3e} swaps {swaps}", flush=True)
+
+
 @pytest.mark.parametrize("n_sets", [1, 2])
 def test_block_max_batch(G, n_sets):
     """The fused block at the largest batch (scorer summaries, TopK, MoT
